@@ -1,0 +1,212 @@
+"""Benchmark of the mixed-task batched forward on one MI355X.
+
+One step = one whole forward of a mixed batch: input rows -> every backbone
+layer (shared projections + per-task LoRA + per-request attention) -> final
+norm, pooling and per-task heads.  Default workload: the ViT-B-shaped encoder
+(12 layers, d 768, 64 requests x 197 tokens, 16 tasks with Zipf(1.1) task ids,
+LoRA rank 16 on q/k/v/o, per-task heads of 10..1000 classes), inputs already
+resident in HBM.
+
+Prints ONE JSON line.  `value` is tokens/s of the whole step; `roofline` is
+the dominant kernel's achieved rate (algorithmic FLOPs or bytes per launch /
+its average duration from hipEvents recorded around its launches inside the
+timed region) against the MI355X peak; `cpu_baseline` times the fp64 oracle
+on a bounded sample of the same batch on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 (matrix / vector)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "mixed-task backbone forward tokens/s at 1 GPU; % of bf16 MFMA / HBM roofline"
+
+
+# --------------------------------------------------------------------------
+# algorithmic work (what the method must do; no padding or recomputation)
+# --------------------------------------------------------------------------
+def algorithmic_work(w, batch, ranks, heads_n_out):
+    """Per-step FLOPs by kernel class and HBM bytes of the decode step."""
+    T = batch.total_rows
+    d, f, H, dh, L = w.d, w.d_ff, w.n_heads, w.head_dim, w.n_layers
+    lens = batch.seq_len.astype(np.float64)
+    rk = ranks[batch.task_id].astype(np.float64)          # rank of each request's task
+    rows_r = float((lens * rk).sum())                      # sum over rows of their rank
+    tgt = set(w.lora_targets)
+
+    def lora(p, d_in, d_out):
+        return 2.0 * rows_r * (d_in + d_out) if p in tgt else 0.0
+
+    fl = {}
+    fl["gemm_qkv"] = 2.0 * T * d * 3 * d + sum(2.0 * rows_r * d for p in ("q", "k", "v") if p in tgt)
+    fl["gemm_o"] = 2.0 * T * d * d + (2.0 * rows_r * d if "o" in tgt else 0.0)
+    n_up = 2 if w.family == "decoder" else 1
+    fl["gemm_up"] = 2.0 * T * d * f * n_up + sum(2.0 * rows_r * f for p in ("gate", "up") if p in tgt)
+    fl["gemm_down"] = 2.0 * T * f * d + (2.0 * rows_r * d if "down" in tgt else 0.0)
+    fl["shrink"] = sum(2.0 * rows_r * (d if p != "down" else f) for p in tgt)
+    if w.mode == "decode":
+        keys = batch.ctx.astype(np.float64) + 1.0
+        fl["attn"] = float((4.0 * keys * dh * H).sum())
+    elif w.causal:
+        fl["attn"] = float((2.0 * dh * H * lens * (lens + 1)).sum())
+    else:
+        fl["attn"] = float((4.0 * dh * H * lens * lens).sum())
+    per_step = {k: v * L for k, v in fl.items()}
+    head_flops = float(sum(2.0 * d * heads_n_out[t] for t in batch.task_id)) if heads_n_out is not None else 0.0
+    total = sum(per_step.values()) + head_flops
+    # decode bytes: KV read + write, weights once, adapters of distinct tasks, heads
+    es = 2 if w.dtype == "bf16" else 4
+    kv_read = float((batch.ctx.astype(np.float64) + 1).sum() * d * 2 * es) if w.mode == "decode" else 0.0
+    weights = (3 * d * d + d * d + n_up * f * d + f * d) * es
+    distinct = np.unique(batch.task_id)
+    ad_bytes = 0.0
+    for p in tgt:
+        d_in, d_out = (d, d) if p in ("q", "k", "v", "o") else ((d, f) if p in ("gate", "up") else (f, d))
+        ad_bytes += float(ranks[distinct].sum()) * (d_in + d_out) * es
+    step_bytes = L * (kv_read + weights + ad_bytes)
+    return {"per_launch_flops": fl, "step_flops": total, "kv_read_bytes_per_layer": kv_read,
+            "step_bytes": step_bytes}
+
+
+# --------------------------------------------------------------------------
+# CPU baseline: the fp64 oracle on a bounded sample of the same batch
+# --------------------------------------------------------------------------
+def cpu_baseline(w, batch, model, inp, budget_s=15.0):
+    import torch
+    from oracle import vfm_oracle as O
+    from tests.gpu_common import expected_embed, oracle_plan
+    from tests.helpers import np64, oracle_adapter, oracle_weights, spec_of
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
+    x_all = expected_embed(w, batch, inp, pl)
+    Ws = [oracle_weights(model.layers[i]) for i in range(w.n_layers)]   # bf16 -> fp64 outside timing
+    spec = spec_of(w)
+    cu = pl["cu_seqlens"]
+    inv = np.argsort(pl["order"])
+    done_tokens, done_req = 0, 0
+    t0 = time.perf_counter()
+    for i in range(batch.n_req):                 # original request order, whole requests only
+        p = int(inv[i])
+        t = int(pl["task"][p])
+        x = x_all[int(cu[p]):int(cu[p + 1])]
+        pos = pl["pos"][int(cu[p]):int(cu[p + 1])]
+        for li in range(w.n_layers):
+            x = O.layer(spec, Ws[li], oracle_adapter(model.adapters[li], t), x, pos=pos)[0]
+        if model.heads is not None:
+            xn = O.final(spec, np64(model.final["w"]), np64(model.final["b"]), x)
+            O.head(O.pool(xn, w.pool), np64(model.heads.W[t]), np64(model.heads.b[t]))
+        done_tokens += x.shape[0]
+        done_req += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": done_tokens / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {done_req} of {batch.n_req} requests (original order), "
+                      f"{done_tokens} tokens, all {w.n_layers} layers + head, fp64 numpy, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-task forward "
+              "shards by request with no cross-GPU exchange, and this build measures one GPU's "
+              "share.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_09643_amd import binding as B
+    from paper_2606_09643_amd import runner as R
+    from paper_2606_09643_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    batch = wl.draw_batch(w)
+    model = R.Model(w)
+    inp = R.Inputs(w, batch)
+    kv = R.KVCache(w, batch, w.n_layers) if w.mode == "decode" else None
+    pb = R.make_batch(w, batch, model.heads, kv)
+    fwd = R.Forward(model, pb, inp, kv)
+    ranks = wl.task_ranks(w)
+    work = algorithmic_work(w, batch, ranks, model.heads.n_out if model.heads is not None else None)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        fwd(stream)
+    torch.cuda.synchronize()
+
+    # the dominant kernel class is timed with hipEvents inside the timed region
+    dom = "attn" if w.mode == "decode" else "gemm_up"
+    B.vfm_profile_enable([dom])
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        fwd(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    prof = B.vfm_profile_read()
+    B.vfm_profile_enable([])
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    tokens = batch.total_rows
+    value = tokens / (ms_step * 1e-3)
+
+    dom_ms, dom_n = prof[dom]
+    avg_ms = dom_ms / max(dom_n, 1)
+    if w.mode == "decode":
+        per_launch = work["kv_read_bytes_per_layer"]
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+    else:
+        per_launch = work["per_launch_flops"][dom]
+        peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+        achieved = per_launch / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak, "traffic": None}
+    roof.update({"kernel": f"{dom} GEMM" if dom.startswith("gemm") else dom,
+                 "avg_launch_ms": avg_ms, "launches": dom_n, "per_launch": per_launch})
+
+    step_tflops = work["step_flops"] / (ms_step * 1e-3) / 1e12
+    peak_step = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_FP32_TFLOPS
+    out = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": w.name, "n_req": w.n_req, "tokens": tokens,
+                   "n_tasks": w.n_tasks, "distinct_tasks": int(len(np.unique(batch.task_id))),
+                   "layers": w.n_layers, "d_model": w.d, "d_ff": w.d_ff, "lora_rank": w.rank,
+                   "lora_targets": list(w.lora_targets)},
+        "step_tflops": step_tflops,
+        "step_roofline_frac": step_tflops / peak_step if w.mode != "decode" else
+        (work["step_bytes"] / (ms_step * 1e-3) / 1e9) / PEAK_HBM_GBS,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, batch, model, inp)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

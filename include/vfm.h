@@ -1,0 +1,254 @@
+/*
+ * vfm.h -- C ABI of the mixed-task batched forward on MI355X (gfx950).
+ *
+ * FMplex (arxiv 2606.09643) serves many per-task "virtual FMs" over ONE shared
+ * physical backbone.  A scheduler batch concatenates requests of several tasks;
+ * the shared backbone runs once over all of them and each task's adapter
+ * difference is then applied to that task's requests only (Section 4.2,
+ * "Batch-aware Fair Scheduling", last paragraph; example (c) of Fig. 5).  A
+ * task extends the backbone with a PEFT adapter (LoRA) and a decoder head
+ * (Section 2.2; Section 4.1 "Task Extensions"; Table 1 attach_adapter /
+ * add_decoder; Appendix A LoraConfig).  This library runs that batch forward.
+ *
+ * Conventions shared by every entry point
+ *   - All tensors are row-major.  Linear weights use the nn.Linear layout
+ *     [d_out, d_in]: y = x W^T + b.  LoRA factors: A_t [r_t, d_in],
+ *     B_t [d_out, r_t]; the difference is scale_t * (x A_t^T) B_t^T.
+ *   - "dtype" (VFM_F32 or VFM_BF16) is the type of weights, adapters, heads
+ *     and stored activations.  The residual stream x is ALWAYS float32.
+ *   - Rows inside the layer calls are in PLAN order (requests sorted by task
+ *     id, ties in arrival order, see vfm_plan).  vfm_embed_forward reads the
+ *     caller's rows in ORIGINAL order and vfm_head_forward writes outputs in
+ *     ORIGINAL order.
+ *   - Every pointer documented as "device" must point to device memory owned
+ *     by the caller and stay valid until the stream has executed the work.
+ *     "host" pointers are read during the call only.  The library allocates
+ *     no device memory and keeps no pointer after returning.
+ *   - stream is a hipStream_t (NULL = the null stream).  All launches are
+ *     asynchronous on it.
+ *   - Errors: every argument is checked on the host before anything is
+ *     enqueued; on failure a negative vfm_status is returned and nothing is
+ *     launched.  A launch failure returns VFM_ERR_HIP.  No C++ exception
+ *     crosses the ABI.  Calls are reentrant; concurrent calls must not share
+ *     a workspace.
+ */
+#ifndef VFM_H
+#define VFM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  VFM_OK = 0,
+  VFM_ERR_ARG = -1,         /* null pointer or bad enum value */
+  VFM_ERR_SHAPE = -2,       /* sizes inconsistent or outside the supported set */
+  VFM_ERR_TASK = -3,        /* task id out of range */
+  VFM_ERR_UNSUPPORTED = -4, /* valid request this build does not implement */
+  VFM_ERR_WORKSPACE = -5,   /* workspace missing or too small */
+  VFM_ERR_HIP = -6          /* HIP runtime error at launch */
+} vfm_status;
+
+enum { VFM_F32 = 0, VFM_BF16 = 1 };
+enum { VFM_NORM_LAYER = 0, VFM_NORM_RMS = 1 };
+enum { VFM_MLP_GELU = 0, VFM_MLP_SWIGLU = 1 };
+enum { VFM_ATTN_BIDIR = 0, VFM_ATTN_CAUSAL = 1, VFM_ATTN_DECODE = 2 };
+enum { VFM_Q = 0, VFM_K = 1, VFM_V = 2, VFM_O = 3, VFM_GATE = 4, VFM_UP = 5, VFM_DOWN = 6,
+       VFM_NPROJ = 7 };
+enum { VFM_POOL_MEAN = 0, VFM_POOL_FIRST = 1, VFM_POOL_LAST = 2 };
+enum { VFM_EMBED_ROWS = 0, VFM_EMBED_TOKENS = 1, VFM_EMBED_PATCHES = 2 };
+
+/* Rows per tile of the per-task segmented kernels; also the query block of
+ * prefill attention.  Exposed because the plan's tile counts depend on it. */
+#define VFM_ROW_TILE 64
+#define VFM_MAX_RANK 64
+
+/* Backbone shape.  Supported: d_model = n_heads * head_dim, head_dim in
+ * {64, 128}, d_model and d_ff multiples of 64, d_model <= 8192. */
+typedef struct vfm_cfg {
+  int32_t dtype;      /* VFM_F32 | VFM_BF16 */
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t head_dim;
+  int32_t d_ff;
+  int32_t norm;       /* VFM_NORM_LAYER (encoder) | VFM_NORM_RMS (decoder) */
+  int32_t mlp;        /* VFM_MLP_GELU: u = GELU_erf(h W_up^T + b_up)
+                         VFM_MLP_SWIGLU: u = SiLU(h W_gate^T) * (h W_up^T) */
+  int32_t attn;       /* VFM_ATTN_BIDIR | VFM_ATTN_CAUSAL | VFM_ATTN_DECODE */
+  int32_t has_bias;   /* 1: every backbone linear has a bias */
+  float norm_eps;
+  float rope_theta;   /* 0: no rotary embedding; else RoPE base (rotate-half) */
+} vfm_cfg;
+
+/* ------------------------------------------------------------------------
+ * a0. Plan: segment a batch by task (host, integer, deterministic).
+ *
+ * The paper's scheduler forms a batch of requests from several vFMs and
+ * applies each adapter difference per task (Section 4.2).  vfm_plan turns
+ * the batch's task ids into contiguous per-task segments.
+ *
+ * Plan buffer (int32, caller-owned, n_ints from vfm_plan_size), in order:
+ *   header[16]   n_req, n_tasks, T, max_seqlen, n_qblocks, n_rtiles,
+ *                total_outputs, 0...
+ *   order[n_req]        plan position p -> original request index
+ *   task[n_req]         task id at plan position p
+ *   cu_seqlens[n_req+1] first row of plan position p (plan order)
+ *   seg_req[n_tasks+1]  first plan position of task t
+ *   seg_row[n_tasks+1]  first row of task t
+ *   cu_orig[n_req+1]    first row of request i in ORIGINAL order
+ *   out_off[n_req+1]    first head output of request i, ORIGINAL order
+ *   ctx[n_req]          cached context length at plan position p (0: prefill)
+ *   kv_start[n_req]     first KV slot of plan position p (0 if none)
+ *   qblk_off[n_req+1]   exclusive scan of ceil(len/VFM_ROW_TILE), plan order
+ *   rtile_off[n_tasks+1] exclusive scan of ceil(rows_t/VFM_ROW_TILE)
+ *   row_task[T], row_req[T], pos[T]  per plan-order row: task, plan position,
+ *                       position in its request (+ ctx when decoding)
+ * Requests are ordered by task id ascending, ties in arrival order; tasks
+ * without requests get empty segments.
+ * ---------------------------------------------------------------------- */
+#define VFM_PLAN_HEADER 16
+
+int vfm_plan_size(int32_t n_req, int32_t n_tasks, int64_t total_rows, size_t* n_ints);
+
+/* task_id, seq_len: host [n_req], original order; seq_len >= 1.
+ * ctx_len, kv_start: host [n_req] or NULL (decode: cached tokens and the
+ * first cache slot of each request; the new token's K/V go to slot
+ * kv_start + ctx_len).  n_out: host [n_tasks] head widths or NULL.
+ * Returns VFM_ERR_TASK for an id outside [0, n_tasks). */
+int vfm_plan(const int32_t* task_id, const int32_t* seq_len, const int32_t* ctx_len,
+             const int32_t* kv_start, const int32_t* n_out, int32_t n_req, int32_t n_tasks,
+             int32_t* plan, size_t n_ints);
+
+/* A planned batch: the same plan buffer on the host (for launch sizes) and a
+ * device copy of it (read by the kernels). */
+typedef struct vfm_batch {
+  const int32_t* plan_host;   /* host */
+  const int32_t* plan_dev;    /* device */
+  size_t n_ints;
+} vfm_batch;
+
+/* ------------------------------------------------------------------------
+ * Shared backbone weights of one layer (device, dtype unless noted).
+ * ---------------------------------------------------------------------- */
+typedef struct vfm_layer_weights {
+  const void* norm1_w;   /* [d] */
+  const void* norm1_b;   /* [d] LayerNorm shift, NULL for RMSNorm */
+  const void* w_qkv;     /* [3d, d]: rows of W_q, then W_k, then W_v */
+  const void* b_qkv;     /* [3d] or NULL */
+  const void* w_o;       /* [d, d] */
+  const void* b_o;       /* [d] or NULL */
+  const void* norm2_w;   /* [d] */
+  const void* norm2_b;   /* [d] or NULL */
+  const void* w_gate;    /* [d_ff, d] (SwiGLU) or NULL */
+  const void* w_up;      /* [d_ff, d] */
+  const void* b_up;      /* [d_ff] or NULL */
+  const void* w_down;    /* [d, d_ff] */
+  const void* b_down;    /* [d] or NULL */
+} vfm_layer_weights;
+
+/* Per-task LoRA adapters of one layer (the vFM's "Task Extensions",
+ * Section 4.1; LoRA of Hu et al., Section 2.2).  A[p] / B[p] are device
+ * arrays of n_tasks device pointers (an entry may be NULL when rank[t] is 0);
+ * a NULL A[p] means projection p carries no adapters.  Entries can be
+ * replaced between calls to attach or remove a task's adapter without
+ * touching the backbone. */
+typedef struct vfm_lora_table {
+  int32_t n_tasks;
+  int32_t max_rank;            /* >= every rank[t]; multiple of 8, <= 64 */
+  const int32_t* rank;         /* device [n_tasks]: 0 or a multiple of 8 <= max_rank */
+  const float* scale;          /* device [n_tasks]: lora_alpha / r or any scale */
+  const void* const* A[VFM_NPROJ];  /* device [n_tasks] -> A_t [rank_t, d_in] */
+  const void* const* B[VFM_NPROJ];  /* device [n_tasks] -> B_t [d_out, rank_t] */
+} vfm_lora_table;
+
+/* Per-task linear heads (the vFM's decoder, Section 2.2). */
+typedef struct vfm_head_table {
+  int32_t n_tasks;
+  int32_t pool;                /* VFM_POOL_MEAN | VFM_POOL_FIRST | VFM_POOL_LAST */
+  int32_t max_out;             /* >= every n_out[t] */
+  const int32_t* n_out;        /* device [n_tasks]; must equal the n_out given to vfm_plan */
+  const void* const* W;        /* device [n_tasks] -> W_t [n_out_t, d] */
+  const void* const* b;        /* device [n_tasks] -> b_t [n_out_t], entries may be NULL */
+} vfm_head_table;
+
+const char* vfm_status_string(int status);
+
+/* Device workspace needed by vfm_layer_forward / vfm_lora_apply /
+ * vfm_head_forward for this batch (lora may be NULL). */
+int vfm_workspace_size(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_lora_table* lora,
+                       size_t* bytes);
+
+/* ------------------------------------------------------------------------
+ * a1. Input rows -> fp32 residual stream x [T, d] in plan order.
+ *   VFM_EMBED_ROWS:    src [T, d] (dtype) in original order; x = permuted src.
+ *   VFM_EMBED_TOKENS:  src int32 [T] token ids (original order), table
+ *                      [vocab, d] (dtype) with vocab = src_width; x = table[id].
+ *                      Ids outside [0, vocab) give zero rows.
+ *   VFM_EMBED_PATCHES: src float32 [T, src_width] patches (original order),
+ *                      table = W_pe [d, src_width], bias [d] (dtype);
+ *                      x = W_pe patch + b_pe.  src_width <= 64.
+ * ---------------------------------------------------------------------- */
+int vfm_embed_forward(const vfm_cfg* cfg, const vfm_batch* batch, int32_t mode, const void* src,
+                      int32_t src_width, const void* table, const void* bias, float* x,
+                      void* stream);
+
+/* ------------------------------------------------------------------------
+ * a2-a10. One backbone layer over the whole mixed batch, in place on x.
+ *   x: device float32 [T, d], plan order (residual stream).
+ *   lora: NULL for the bare backbone.
+ *   k_cache, v_cache: device [kv_slots, d] (dtype), rotated keys; used when
+ *     cfg->attn is VFM_ATTN_DECODE (required) or VFM_ATTN_CAUSAL (optional,
+ *     NULL to skip): each row's K/V is written at slot kv_start + pos.
+ *   workspace: device, >= vfm_workspace_size bytes, 256-byte aligned.
+ * Per layer: h = Norm1(x); [q|k|v] = h W_qkv^T + b (+ per-task LoRA);
+ * RoPE; attention per request; x += attn W_o^T + b_o (+ LoRA_o);
+ * h2 = Norm2(x); u = MLP(h2) (+ LoRA on gate/up); x += u W_down^T + b_down
+ * (+ LoRA_down).
+ * ---------------------------------------------------------------------- */
+int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
+                      const vfm_batch* batch, float* x, void* k_cache, void* v_cache,
+                      int64_t kv_slots, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * a4. Segmented LoRA on one projection: for every plan-order row m of task
+ * t with rank_t > 0,  y[m, :] += scale_t * (x[m, :] A_{t,proj}^T) B_{t,proj}^T.
+ *   x: device [T, d_in] (dtype), plan order.  y: device float32 [T, d_out].
+ * ---------------------------------------------------------------------- */
+int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t d_out,
+                   const vfm_lora_table* lora, const vfm_batch* batch, const void* x, float* y,
+                   void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * a11-a12. Final norm, pooling and per-task heads.
+ *   x: device float32 [T, d] plan order (the last layer's output).
+ *   heads != NULL: out = device float32 [total_outputs]; request i's
+ *     outputs W_t pool(Norm(x_i)) + b_t start at out_off[i] (original order).
+ *   heads == NULL: out = device float32 [T, d], the final-normed rows in
+ *     original order.
+ * ---------------------------------------------------------------------- */
+int vfm_head_forward(const vfm_cfg* cfg, const void* final_norm_w, const void* final_norm_b,
+                     const vfm_head_table* heads, const vfm_batch* batch, const float* x,
+                     float* out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing for benchmarks (not part of the forward).  While a class's
+ * bit is set in the mask, every launch of that class made by the calls above
+ * is bracketed by two hipEvents on its stream; vfm_profile_read waits for
+ * the recorded events and returns, per class, the summed milliseconds and
+ * the launch count since the last reset.  Process-global state: enable and
+ * read from one thread.  Classes: */
+enum { VFM_PROF_GEMM_QKV = 0, VFM_PROF_GEMM_O = 1, VFM_PROF_GEMM_UP = 2, VFM_PROF_GEMM_DOWN = 3,
+       VFM_PROF_ATTN = 4, VFM_PROF_NORM = 5, VFM_PROF_SHRINK = 6, VFM_PROF_OTHER = 7,
+       VFM_PROF_NCLASS = 8 };
+
+int vfm_profile_enable(uint32_t class_mask);   /* 0 disables; also resets the counters */
+int vfm_profile_read(double* ms, int64_t* launches, int32_t n_classes); /* host arrays */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VFM_H */

@@ -1,0 +1,294 @@
+"""ctypes binding of ``libvfm.so`` (declared in ``include/vfm.h``).
+
+Argument marshalling only: every step of the forward runs inside the HIP
+library.  PyTorch provides device memory and the stream.  The functions keep
+the C names (``vfm_plan``, ``vfm_layer_forward``, ...); the small classes
+below build the C structs (plan buffers, per-task pointer tables) from torch
+tensors and keep those tensors alive while the structs are in use.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libvfm.so")
+
+VFM_OK, VFM_ERR_ARG, VFM_ERR_SHAPE, VFM_ERR_TASK = 0, -1, -2, -3
+VFM_ERR_UNSUPPORTED, VFM_ERR_WORKSPACE, VFM_ERR_HIP = -4, -5, -6
+VFM_F32, VFM_BF16 = 0, 1
+VFM_NORM_LAYER, VFM_NORM_RMS = 0, 1
+VFM_MLP_GELU, VFM_MLP_SWIGLU = 0, 1
+VFM_ATTN_BIDIR, VFM_ATTN_CAUSAL, VFM_ATTN_DECODE = 0, 1, 2
+VFM_POOL_MEAN, VFM_POOL_FIRST, VFM_POOL_LAST = 0, 1, 2
+VFM_EMBED_ROWS, VFM_EMBED_TOKENS, VFM_EMBED_PATCHES = 0, 1, 2
+VFM_NPROJ = 7
+VFM_PLAN_HEADER = 16
+VFM_ROW_TILE = 64
+PROJ = ("q", "k", "v", "o", "gate", "up", "down")
+
+EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size",
+           "vfm_embed_forward", "vfm_layer_forward", "vfm_lora_apply", "vfm_head_forward",
+           "vfm_profile_enable", "vfm_profile_read")
+PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
+
+
+class VfmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {_lib_handle().vfm_status_string(status).decode()} ({status})")
+
+
+class vfm_cfg(C.Structure):
+    _fields_ = [("dtype", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("d_ff", C.c_int32), ("norm", C.c_int32),
+                ("mlp", C.c_int32), ("attn", C.c_int32), ("has_bias", C.c_int32),
+                ("norm_eps", C.c_float), ("rope_theta", C.c_float)]
+
+
+class vfm_batch(C.Structure):
+    _fields_ = [("plan_host", C.POINTER(C.c_int32)), ("plan_dev", C.c_void_p),
+                ("n_ints", C.c_size_t)]
+
+
+class vfm_layer_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("norm1_w", "norm1_b", "w_qkv", "b_qkv", "w_o", "b_o",
+                                           "norm2_w", "norm2_b", "w_gate", "w_up", "b_up",
+                                           "w_down", "b_down")]
+
+
+class vfm_lora_table(C.Structure):
+    _fields_ = [("n_tasks", C.c_int32), ("max_rank", C.c_int32), ("rank", C.c_void_p),
+                ("scale", C.c_void_p), ("A", C.c_void_p * VFM_NPROJ), ("B", C.c_void_p * VFM_NPROJ)]
+
+
+class vfm_head_table(C.Structure):
+    _fields_ = [("n_tasks", C.c_int32), ("pool", C.c_int32), ("max_out", C.c_int32),
+                ("n_out", C.c_void_p), ("W", C.c_void_p), ("b", C.c_void_p)]
+
+
+_LIB = None
+
+
+def _lib_handle():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"HIP library {LIB_PATH} is not built; run "
+                               "`python -m paper_2606_09643_amd.build` (no CPU fallback exists)")
+        lib = C.CDLL(LIB_PATH)
+        lib.vfm_status_string.restype = C.c_char_p
+        lib.vfm_status_string.argtypes = [C.c_int]
+        lib.vfm_plan_size.argtypes = [C.c_int32, C.c_int32, C.c_int64, C.POINTER(C.c_size_t)]
+        lib.vfm_plan.argtypes = [C.c_void_p] * 5 + [C.c_int32, C.c_int32, C.c_void_p, C.c_size_t]
+        lib.vfm_workspace_size.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_batch),
+                                           C.POINTER(vfm_lora_table), C.POINTER(C.c_size_t)]
+        lib.vfm_embed_forward.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_batch), C.c_int32,
+                                          C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                          C.c_void_p, C.c_void_p]
+        lib.vfm_layer_forward.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_layer_weights),
+                                          C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
+                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
+                                          C.c_void_p, C.c_size_t, C.c_void_p]
+        lib.vfm_lora_apply.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                       C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
+                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
+        lib.vfm_head_forward.argtypes = [C.POINTER(vfm_cfg), C.c_void_p, C.c_void_p,
+                                         C.POINTER(vfm_head_table), C.POINTER(vfm_batch),
+                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                         C.c_void_p]
+        lib.vfm_profile_enable.argtypes = [C.c_uint32]
+        lib.vfm_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
+        for name in EXPORTS:
+            getattr(lib, name).restype = C.c_int if name != "vfm_status_string" else C.c_char_p
+        _LIB = lib
+    return _LIB
+
+
+def lib():
+    """The loaded library (raises if it was not built)."""
+    return _lib_handle()
+
+
+def _check(st: int, where: str):
+    if st != VFM_OK:
+        raise VfmError(st, where)
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        return t.data_ptr()
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return int(t)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+# --------------------------------------------------------------------------
+# C entry points
+# --------------------------------------------------------------------------
+def vfm_status_string(status: int) -> str:
+    return _lib_handle().vfm_status_string(status).decode()
+
+
+def vfm_plan_size(n_req: int, n_tasks: int, total_rows: int) -> int:
+    n = C.c_size_t()
+    _check(_lib_handle().vfm_plan_size(n_req, n_tasks, total_rows, C.byref(n)), "vfm_plan_size")
+    return n.value
+
+
+def vfm_plan(task_id, seq_len, n_tasks, ctx_len=None, kv_start=None, n_out=None) -> np.ndarray:
+    """Host plan buffer (int32) for a batch; see include/vfm.h for its layout."""
+    a = lambda v: None if v is None else np.ascontiguousarray(v, dtype=np.int32)
+    task_id, seq_len, ctx_len, kv_start, n_out = map(a, (task_id, seq_len, ctx_len, kv_start, n_out))
+    n_req = int(task_id.shape[0])
+    n = vfm_plan_size(n_req, n_tasks, int(seq_len.astype(np.int64).sum()))
+    out = np.zeros(n, np.int32)
+    st = _lib_handle().vfm_plan(_ptr(task_id), _ptr(seq_len), _ptr(ctx_len), _ptr(kv_start),
+                                _ptr(n_out), n_req, n_tasks, _ptr(out), n)
+    _check(st, "vfm_plan")
+    return out
+
+
+def vfm_workspace_size(cfg: vfm_cfg, batch: vfm_batch, lora: vfm_lora_table | None = None) -> int:
+    n = C.c_size_t()
+    st = _lib_handle().vfm_workspace_size(C.byref(cfg), C.byref(batch),
+                                          C.byref(lora) if lora is not None else None, C.byref(n))
+    _check(st, "vfm_workspace_size")
+    return n.value
+
+
+def vfm_embed_forward(cfg, batch, mode, src, src_width, table, bias, x, stream=None):
+    st = _lib_handle().vfm_embed_forward(C.byref(cfg), C.byref(batch), mode, _ptr(src), src_width,
+                                         _ptr(table), _ptr(bias), _ptr(x), _stream(stream))
+    _check(st, "vfm_embed_forward")
+
+
+def vfm_layer_forward(cfg, weights, lora, batch, x, k_cache=None, v_cache=None, kv_slots=0,
+                      workspace=None, stream=None):
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) \
+        if workspace is not None else (None, 0)
+    st = _lib_handle().vfm_layer_forward(C.byref(cfg), C.byref(weights),
+                                         C.byref(lora) if lora is not None else None,
+                                         C.byref(batch), _ptr(x), _ptr(k_cache), _ptr(v_cache),
+                                         kv_slots, ws_ptr, ws_bytes, _stream(stream))
+    _check(st, "vfm_layer_forward")
+
+
+def vfm_lora_apply(dtype, proj, d_in, d_out, lora, batch, x, y, workspace, stream=None):
+    st = _lib_handle().vfm_lora_apply(dtype, proj, d_in, d_out, C.byref(lora), C.byref(batch),
+                                      _ptr(x), _ptr(y), workspace.data_ptr(),
+                                      workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "vfm_lora_apply")
+
+
+def vfm_head_forward(cfg, final_norm_w, final_norm_b, heads, batch, x, out, workspace, stream=None):
+    ws_ptr, ws_bytes = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) \
+        if workspace is not None else (None, 0)
+    st = _lib_handle().vfm_head_forward(C.byref(cfg), _ptr(final_norm_w), _ptr(final_norm_b),
+                                        C.byref(heads) if heads is not None else None,
+                                        C.byref(batch), _ptr(x), _ptr(out), ws_ptr, ws_bytes,
+                                        _stream(stream))
+    _check(st, "vfm_head_forward")
+
+
+def vfm_profile_enable(classes=()) -> None:
+    """Bracket launches of the named kernel classes with hipEvents (0 = off)."""
+    mask = 0
+    for c in classes:
+        mask |= 1 << PROF_CLASSES.index(c)
+    _check(_lib_handle().vfm_profile_enable(mask), "vfm_profile_enable")
+
+
+def vfm_profile_read() -> dict:
+    """{class: (total_ms, launches)} since the last vfm_profile_enable."""
+    n = len(PROF_CLASSES)
+    ms = np.zeros(n, np.float64)
+    cnt = np.zeros(n, np.int64)
+    _check(_lib_handle().vfm_profile_read(ms.ctypes.data, cnt.ctypes.data, n), "vfm_profile_read")
+    return {c: (float(ms[i]), int(cnt[i])) for i, c in enumerate(PROF_CLASSES)}
+
+
+# --------------------------------------------------------------------------
+# struct builders (keep the tensors they point to alive)
+# --------------------------------------------------------------------------
+def make_cfg(dtype, d_model, n_heads, head_dim, d_ff, norm, mlp, attn, has_bias, norm_eps,
+             rope_theta) -> vfm_cfg:
+    return vfm_cfg(dtype, d_model, n_heads, head_dim, d_ff, norm, mlp, attn, int(has_bias),
+                   norm_eps, rope_theta)
+
+
+class Batch:
+    """A planned batch: host plan, its device copy and the C struct."""
+
+    def __init__(self, task_id, seq_len, n_tasks, ctx_len=None, kv_start=None, n_out=None,
+                 device="cuda"):
+        self.host = vfm_plan(task_id, seq_len, n_tasks, ctx_len, kv_start, n_out)
+        self.dev = torch.from_numpy(self.host).to(device)
+        self.c = vfm_batch(self.host.ctypes.data_as(C.POINTER(C.c_int32)), self.dev.data_ptr(),
+                           self.host.size)
+
+    @property
+    def n_req(self):
+        return int(self.host[0])
+
+    @property
+    def T(self):
+        return int(self.host[2])
+
+    @property
+    def total_outputs(self):
+        return int(self.host[6])
+
+
+def layer_weights(W: dict) -> vfm_layer_weights:
+    return vfm_layer_weights(*[_ptr(W.get(n)) for n, _ in vfm_layer_weights._fields_])
+
+
+class LoraTable:
+    """Device pointer tables of per-task LoRA factors for one layer.
+
+    factors: {proj: (list of A_t tensors or None, list of B_t tensors or None)}.
+    """
+
+    def __init__(self, n_tasks, ranks, scales, factors: dict, max_rank=None, device="cuda"):
+        ranks = np.asarray(ranks, np.int32)
+        self.rank = torch.from_numpy(ranks).to(device)
+        self.scale = torch.as_tensor(np.asarray(scales, np.float32)).to(device)
+        mr = int(ranks.max()) if max_rank is None else int(max_rank)
+        self._keep = []
+        A = (C.c_void_p * VFM_NPROJ)()
+        B = (C.c_void_p * VFM_NPROJ)()
+        for p, name in enumerate(PROJ):
+            if name not in factors:
+                continue
+            As, Bs = factors[name]
+            pa = torch.tensor([_ptr(a) if a is not None and a.numel() else 0 for a in As],
+                              dtype=torch.int64).to(device)
+            pb = torch.tensor([_ptr(b) if b is not None and b.numel() else 0 for b in Bs],
+                              dtype=torch.int64).to(device)
+            self._keep += [pa, pb, As, Bs]
+            A[p] = pa.data_ptr()
+            B[p] = pb.data_ptr()
+        self.c = vfm_lora_table(n_tasks, mr, self.rank.data_ptr(), self.scale.data_ptr(), A, B)
+
+
+class HeadTable:
+    def __init__(self, n_out, Ws, bs, pool, device="cuda"):
+        n_out = np.asarray(n_out, np.int32)
+        self.n_out = torch.from_numpy(n_out).to(device)
+        self._keep = [Ws, bs]
+        self.pw = torch.tensor([_ptr(w) if w is not None else 0 for w in Ws], dtype=torch.int64).to(device)
+        self.pb = torch.tensor([_ptr(b) if b is not None else 0 for b in bs], dtype=torch.int64).to(device)
+        self.c = vfm_head_table(len(n_out), pool, int(n_out.max()) if n_out.size else 0,
+                                self.n_out.data_ptr(), self.pw.data_ptr(), self.pb.data_ptr())

@@ -1,0 +1,331 @@
+// C ABI entry points: argument validation, workspace carving and the launch
+// sequence of one backbone layer over a mixed-task batch.
+#include <algorithm>
+
+#include "vfm_internal.h"
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+inline size_t align_up(size_t v) { return (v + ALIGN - 1) / ALIGN * ALIGN; }
+
+inline size_t elem_size(int dtype) { return dtype == VFM_BF16 ? 2 : 4; }
+
+int check_cfg(const vfm_cfg* c) {
+  if (!c) return VFM_ERR_ARG;
+  if (c->dtype != VFM_F32 && c->dtype != VFM_BF16) return VFM_ERR_ARG;
+  if (c->norm != VFM_NORM_LAYER && c->norm != VFM_NORM_RMS) return VFM_ERR_ARG;
+  if (c->mlp != VFM_MLP_GELU && c->mlp != VFM_MLP_SWIGLU) return VFM_ERR_ARG;
+  if (c->attn < VFM_ATTN_BIDIR || c->attn > VFM_ATTN_DECODE) return VFM_ERR_ARG;
+  if (c->head_dim != 64 && c->head_dim != 128) return VFM_ERR_UNSUPPORTED;
+  if (c->n_heads < 1 || (int64_t)c->n_heads * c->head_dim != c->d_model) return VFM_ERR_SHAPE;
+  if (c->d_model % 64 || c->d_model > 8192 || c->d_ff < 64 || c->d_ff % 64) return VFM_ERR_SHAPE;
+  if (c->mlp == VFM_MLP_SWIGLU && c->has_bias) return VFM_ERR_UNSUPPORTED;
+  if (!(c->norm_eps >= 0.f) || !(c->rope_theta >= 0.f)) return VFM_ERR_ARG;
+  return VFM_OK;
+}
+
+int check_batch(const vfm_batch* b, Plan* out) {
+  if (!b || !b->plan_host || !b->plan_dev) return VFM_ERR_ARG;
+  if (b->n_ints < VFM_PLAN_HEADER) return VFM_ERR_SHAPE;
+  const int32_t* h = b->plan_host;
+  if (h[0] < 1 || h[1] < 1 || h[2] < h[0]) return VFM_ERR_SHAPE;
+  if ((size_t)plan_offsets(h[0], h[1], h[2]).total > b->n_ints) return VFM_ERR_SHAPE;
+  *out = make_plan(h, b->plan_dev);
+  return VFM_OK;
+}
+
+// host-side view of the plan arrays (for validation of cache bounds)
+inline const int32_t* host_arr(const vfm_batch* b, int64_t off) { return b->plan_host + off; }
+
+int check_lora(const vfm_lora_table* l, const Plan& pl) {
+  if (!l) return VFM_OK;
+  if (l->n_tasks != pl.n_tasks) return VFM_ERR_SHAPE;
+  if (l->max_rank < 0 || l->max_rank > VFM_MAX_RANK || l->max_rank % 8) return VFM_ERR_SHAPE;
+  if (!l->rank || !l->scale) return VFM_ERR_ARG;
+  for (int p = 0; p < VFM_NPROJ; ++p)
+    if ((l->A[p] == nullptr) != (l->B[p] == nullptr)) return VFM_ERR_ARG;
+  return VFM_OK;
+}
+
+inline int rpad_of(const vfm_lora_table* l) {
+  if (!l || l->max_rank == 0) return 0;
+  return l->max_rank <= 32 ? 32 : 64;
+}
+
+struct LayerWs {
+  size_t h, big, attn, u, total;
+};
+
+LayerWs layer_ws(const vfm_cfg& c, const Plan& pl, const vfm_lora_table* l) {
+  const size_t es = elem_size(c.dtype);
+  const size_t T = (size_t)pl.T;
+  LayerWs w;
+  size_t off = 0;
+  w.h = off;    off += align_up(T * c.d_model * es);
+  w.big = off;  off += align_up(T * std::max<size_t>(3 * (size_t)c.d_model, c.d_ff) * es);
+  w.attn = off; off += align_up(T * c.d_model * es);
+  w.u = off;    off += align_up(T * VFM_NPROJ * rpad_of(l) * es);
+  w.total = off;
+  return w;
+}
+
+size_t head_ws(const vfm_cfg& c, const Plan& pl) {
+  return align_up((size_t)pl.n_req * c.d_model * elem_size(c.dtype));
+}
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? VFM_OK : VFM_ERR_HIP; }
+
+#define VFM_TRY(expr)              \
+  do {                             \
+    int _st = (expr);              \
+    if (_st != VFM_OK) return _st; \
+  } while (0)
+#define VFM_HIP(expr)                               \
+  do {                                              \
+    hipError_t _e = (expr);                         \
+    if (_e != hipSuccess) return VFM_ERR_HIP;       \
+  } while (0)
+// a launch bracketed by the optional timing hooks
+#define VFM_TIMED(cls, expr)                        \
+  do {                                              \
+    const int _pi = prof_begin((cls), s);           \
+    hipError_t _e = (expr);                         \
+    prof_end(_pi, s);                               \
+    if (_e != hipSuccess) return VFM_ERR_HIP;       \
+  } while (0)
+
+}  // namespace
+
+extern "C" const char* vfm_status_string(int status) {
+  switch (status) {
+    case VFM_OK: return "ok";
+    case VFM_ERR_ARG: return "invalid argument (null pointer or bad enum)";
+    case VFM_ERR_SHAPE: return "inconsistent or unsupported sizes";
+    case VFM_ERR_TASK: return "task id out of range";
+    case VFM_ERR_UNSUPPORTED: return "configuration not supported by this build";
+    case VFM_ERR_WORKSPACE: return "workspace missing or too small";
+    case VFM_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+extern "C" int vfm_workspace_size(const vfm_cfg* cfg, const vfm_batch* batch,
+                                  const vfm_lora_table* lora, size_t* bytes) {
+  if (!bytes) return VFM_ERR_ARG;
+  VFM_TRY(check_cfg(cfg));
+  Plan pl;
+  VFM_TRY(check_batch(batch, &pl));
+  VFM_TRY(check_lora(lora, pl));
+  size_t need = layer_ws(*cfg, pl, lora).total;
+  need = std::max(need, head_ws(*cfg, pl));
+  *bytes = need;
+  return VFM_OK;
+}
+
+extern "C" int vfm_embed_forward(const vfm_cfg* cfg, const vfm_batch* batch, int32_t mode,
+                                 const void* src, int32_t src_width, const void* table,
+                                 const void* bias, float* x, void* stream) {
+  VFM_TRY(check_cfg(cfg));
+  Plan pl;
+  VFM_TRY(check_batch(batch, &pl));
+  if (!src || !x) return VFM_ERR_ARG;
+  if (mode == VFM_EMBED_TOKENS) {
+    if (!table) return VFM_ERR_ARG;
+    if (src_width < 1) return VFM_ERR_SHAPE;
+  } else if (mode == VFM_EMBED_PATCHES) {
+    if (!table) return VFM_ERR_ARG;
+    if (src_width < 1 || src_width > 64) return VFM_ERR_SHAPE;
+  } else if (mode != VFM_EMBED_ROWS) {
+    return VFM_ERR_ARG;
+  }
+  return hip_status(launch_embed(cfg->dtype, pl, mode, src, src_width, table, bias, cfg->d_model, x,
+                                 (hipStream_t)stream));
+}
+
+extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
+                                 const vfm_lora_table* lora, const vfm_batch* batch, float* x,
+                                 void* k_cache, void* v_cache, int64_t kv_slots, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  VFM_TRY(check_cfg(cfg));
+  Plan pl;
+  VFM_TRY(check_batch(batch, &pl));
+  VFM_TRY(check_lora(lora, pl));
+  if (!w || !x) return VFM_ERR_ARG;
+  if (!w->norm1_w || !w->norm2_w || !w->w_qkv || !w->w_o || !w->w_up || !w->w_down)
+    return VFM_ERR_ARG;
+  if (cfg->mlp == VFM_MLP_SWIGLU && !w->w_gate) return VFM_ERR_ARG;
+  const vfm_cfg& c = *cfg;
+  const int d = c.d_model, f = c.d_ff, T = pl.T;
+
+  // KV-cache bounds (host copy of the plan)
+  const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
+  if (c.attn == VFM_ATTN_DECODE) {
+    if (!k_cache || !v_cache) return VFM_ERR_ARG;
+    if (pl.max_seqlen != 1) return VFM_ERR_UNSUPPORTED;
+  }
+  if (k_cache || v_cache) {
+    if (!k_cache || !v_cache) return VFM_ERR_ARG;
+    const int32_t* ctx = host_arr(batch, po.ctx);
+    const int32_t* kvs = host_arr(batch, po.kv_start);
+    const int32_t* cu = host_arr(batch, po.cu_seqlens);
+    for (int p = 0; p < pl.n_req; ++p) {
+      const int64_t end = (int64_t)kvs[p] + ctx[p] + (cu[p + 1] - cu[p]);
+      if (end > kv_slots) return VFM_ERR_SHAPE;
+    }
+  }
+  const LayerWs ws = layer_ws(c, pl, lora);
+  if (!workspace || ws_bytes < ws.total || ((uintptr_t)workspace % ALIGN)) return VFM_ERR_WORKSPACE;
+
+  hipStream_t s = (hipStream_t)stream;
+  char* base = (char*)workspace;
+  void* h = base + ws.h;
+  void* qkv = base + ws.big;
+  void* act = base + ws.big;  // the MLP activation reuses the qkv region
+  void* attn = base + ws.attn;
+  void* U = base + ws.u;
+  const int rpad = rpad_of(lora);
+  const int ldu = VFM_NPROJ * rpad;
+  const bool use_lora = lora && rpad > 0;
+
+  auto has = [&](int p) { return use_lora && lora->A[p] != nullptr; };
+  auto shrink = [&](const void* X, int K, std::initializer_list<int> projs) -> hipError_t {
+    ShrinkArgs a = {};
+    a.X = X; a.ldx = K; a.K = K; a.U = U; a.ldu = ldu; a.rpad = rpad;
+    a.rank = lora->rank; a.scale = lora->scale;
+    for (int p : projs) {
+      if (!has(p)) continue;
+      a.A[a.n_proj] = lora->A[p];
+      a.ucol[a.n_proj] = p * rpad;
+      a.n_proj++;
+    }
+    return launch_lora_shrink(c.dtype, pl, a, s);
+  };
+  auto gl = [&](std::initializer_list<int> projs, int slot_width) {
+    GemmLora L = {};
+    int i = 0;
+    bool any = false;
+    for (int p : projs) {
+      if (has(p)) {
+        L.B[i] = lora->B[p];
+        any = true;
+      }
+      L.ucol[i] = p * rpad;
+      ++i;
+    }
+    if (!any) return L;
+    L.enabled = 1;
+    L.U = U; L.ldu = ldu; L.slot_width = slot_width;
+    L.rank = lora->rank; L.row_task = pl.row_task; L.seg_row = pl.seg_row;
+    L.max_rank = lora->max_rank;
+    return L;
+  };
+
+  // a2: pre-norm 1
+  VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm1_w, w->norm1_b, c.norm, c.norm_eps, h, s));
+  // a3 + a4: shared QKV projection with the per-task LoRA of q, k, v
+  if (has(VFM_Q) || has(VFM_K) || has(VFM_V)) VFM_TIMED(VFM_PROF_SHRINK, shrink(h, d, {VFM_Q, VFM_K, VFM_V}));
+  {
+    GemmArgs g = {};
+    g.X = h; g.ldx = d; g.W = w->w_qkv; g.bias = w->b_qkv;
+    g.M = T; g.N = 3 * d; g.K = d; g.epi = EPI_STORE; g.out = qkv; g.ldo = 3 * d;
+    g.lora = gl({VFM_Q, VFM_K, VFM_V}, d);
+    VFM_TIMED(VFM_PROF_GEMM_QKV, launch_gemm(c.dtype, g, s));
+  }
+  // a5: rotary embedding of q and k
+  if (c.rope_theta > 0.f)
+    VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta, s));
+  // a6: attention per request (and the KV-cache write)
+  VFM_TIMED(VFM_PROF_ATTN, launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, nullptr, 0, s));
+  // a7: output projection + LoRA_o + residual
+  if (has(VFM_O)) VFM_TIMED(VFM_PROF_SHRINK, shrink(attn, d, {VFM_O}));
+  {
+    GemmArgs g = {};
+    g.X = attn; g.ldx = d; g.W = w->w_o; g.bias = w->b_o;
+    g.M = T; g.N = d; g.K = d; g.epi = EPI_RESID; g.out = x; g.ldo = d;
+    g.lora = gl({VFM_O}, d);
+    VFM_TIMED(VFM_PROF_GEMM_O, launch_gemm(c.dtype, g, s));
+  }
+  // a8: pre-norm 2
+  VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm2_w, w->norm2_b, c.norm, c.norm_eps, h, s));
+  // a9: MLP up (+ gate) with LoRA and the activation fused
+  if (c.mlp == VFM_MLP_SWIGLU) {
+    if (has(VFM_GATE) || has(VFM_UP)) VFM_TIMED(VFM_PROF_SHRINK, shrink(h, d, {VFM_GATE, VFM_UP}));
+    GemmArgs g = {};
+    g.X = h; g.ldx = d; g.W = w->w_gate; g.W2 = w->w_up;
+    g.M = T; g.N = f; g.K = d; g.epi = EPI_SWIGLU; g.out = act; g.ldo = f;
+    g.lora = gl({VFM_GATE, VFM_UP}, f);
+    VFM_TIMED(VFM_PROF_GEMM_UP, launch_gemm(c.dtype, g, s));
+  } else {
+    if (has(VFM_UP)) VFM_TIMED(VFM_PROF_SHRINK, shrink(h, d, {VFM_UP}));
+    GemmArgs g = {};
+    g.X = h; g.ldx = d; g.W = w->w_up; g.bias = w->b_up;
+    g.M = T; g.N = f; g.K = d; g.epi = EPI_GELU; g.out = act; g.ldo = f;
+    g.lora = gl({VFM_UP}, f);
+    VFM_TIMED(VFM_PROF_GEMM_UP, launch_gemm(c.dtype, g, s));
+  }
+  // a10: down projection + LoRA_down + residual
+  if (has(VFM_DOWN)) VFM_TIMED(VFM_PROF_SHRINK, shrink(act, f, {VFM_DOWN}));
+  {
+    GemmArgs g = {};
+    g.X = act; g.ldx = f; g.W = w->w_down; g.bias = w->b_down;
+    g.M = T; g.N = d; g.K = f; g.epi = EPI_RESID; g.out = x; g.ldo = d;
+    g.lora = gl({VFM_DOWN}, d);
+    VFM_TIMED(VFM_PROF_GEMM_DOWN, launch_gemm(c.dtype, g, s));
+  }
+  return VFM_OK;
+}
+
+extern "C" int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t d_out,
+                              const vfm_lora_table* lora, const vfm_batch* batch, const void* x,
+                              float* y, void* workspace, size_t ws_bytes, void* stream) {
+  if (dtype != VFM_F32 && dtype != VFM_BF16) return VFM_ERR_ARG;
+  if (proj < 0 || proj >= VFM_NPROJ) return VFM_ERR_ARG;
+  if (!lora || !x || !y) return VFM_ERR_ARG;
+  Plan pl;
+  VFM_TRY(check_batch(batch, &pl));
+  VFM_TRY(check_lora(lora, pl));
+  if (!lora->A[proj]) return VFM_ERR_ARG;
+  if (d_in < 32 || d_in % 32 || d_out < 4 || d_out % 4) return VFM_ERR_SHAPE;
+  const int rpad = rpad_of(lora);
+  if (rpad == 0) return VFM_OK;
+  const size_t need = align_up((size_t)pl.T * rpad * elem_size(dtype));
+  if (!workspace || ws_bytes < need || ((uintptr_t)workspace % ALIGN)) return VFM_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  ShrinkArgs a = {};
+  a.X = x; a.ldx = d_in; a.K = d_in; a.U = workspace; a.ldu = rpad; a.rpad = rpad;
+  a.rank = lora->rank; a.scale = lora->scale;
+  a.A[0] = lora->A[proj]; a.ucol[0] = 0; a.n_proj = 1;
+  VFM_HIP(launch_lora_shrink(dtype, pl, a, s));
+  ExpandArgs e = {};
+  e.U = workspace; e.ldu = rpad; e.ucol = 0; e.B = lora->B[proj]; e.N = d_out;
+  e.Y = y; e.ldy = d_out; e.rank = lora->rank; e.max_rank = lora->max_rank;
+  VFM_HIP(launch_lora_expand(dtype, pl, e, s));
+  return VFM_OK;
+}
+
+extern "C" int vfm_head_forward(const vfm_cfg* cfg, const void* final_norm_w,
+                                const void* final_norm_b, const vfm_head_table* heads,
+                                const vfm_batch* batch, const float* x, float* out,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  VFM_TRY(check_cfg(cfg));
+  Plan pl;
+  VFM_TRY(check_batch(batch, &pl));
+  if (!final_norm_w || !x || !out) return VFM_ERR_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const vfm_cfg& c = *cfg;
+  if (!heads) {
+    return hip_status(launch_norm_pool(c.dtype, pl, x, c.d_model, final_norm_w, final_norm_b,
+                                       c.norm, c.norm_eps, -1, nullptr, out, s));
+  }
+  if (heads->n_tasks != pl.n_tasks || !heads->n_out || !heads->W) return VFM_ERR_ARG;
+  if (heads->pool < VFM_POOL_MEAN || heads->pool > VFM_POOL_LAST) return VFM_ERR_ARG;
+  if (heads->max_out < 0) return VFM_ERR_SHAPE;
+  if ((size_t)c.d_model * elem_size(c.dtype) > 64 * 1024) return VFM_ERR_UNSUPPORTED;
+  const size_t need = head_ws(c, pl);
+  if (!workspace || ws_bytes < need || ((uintptr_t)workspace % ALIGN)) return VFM_ERR_WORKSPACE;
+  VFM_HIP(launch_norm_pool(c.dtype, pl, x, c.d_model, final_norm_w, final_norm_b, c.norm,
+                           c.norm_eps, heads->pool, workspace, nullptr, s));
+  VFM_HIP(launch_heads(c.dtype, pl, workspace, c.d_model, *heads, out, s));
+  return VFM_OK;
+}

@@ -1,0 +1,387 @@
+// Attention per request (a6), RoPE (a5) and the KV-cache write.
+//
+// Attention never mixes requests: every kernel below maps a block to rows of
+// ONE request (plan cu_seqlens), so co-batched tasks cannot influence each
+// other (the isolation the paper's shared batch must keep, Section 3.1 R3).
+//
+// Prefill (bf16, MFMA): one block = 64 queries of one request and one head,
+// 4 waves x 16 queries, online softmax over 64-key blocks staged in LDS.
+// The score tile is computed transposed, S^T = K Q^T (K rows in the MFMA A
+// slot, the wave's 16 queries in the B slot), so each lane holds 4 keys of
+// ONE query; the max / sum reductions are in-lane plus two cross-lane
+// shuffles, and exp(S^T) is already laid out as the B operand of
+// O^T = V^T P^T (V is staged transposed in LDS).  Each lane finishes with 4
+// consecutive head dims of one query: 8-byte stores.
+//
+// Decode (memory bound): one block per (request, head); 16 lane-groups of
+// 16 lanes stream the request's cached keys, 16 bytes per lane per key row,
+// each group with its own running max / sum / output, merged through LDS.
+#include <algorithm>
+
+#include "vfm_internal.h"
+
+namespace {
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr float NEG_BIG = -1e30f;
+
+// ---------------------------------------------------------------------------
+// RoPE, rotate-half: (x_i, x_{i+dh/2}) rotated by pos * theta^(-2i/dh).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv, int d, int H, int dh,
+                                                   float log2_theta) {
+  const int half = dh >> 1;
+  const int64_t total = (int64_t)pl.T * H * half;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int i = (int)(e % half);
+    const int hh = (int)((e / half) % H);
+    const int r = (int)(e / ((int64_t)half * H));
+    const float inv = exp2f(-(2.0f * (float)i / (float)dh) * log2_theta);
+    const float ang = (float)pl.pos[r] * inv;
+    float sn, cs;
+    sincosf(ang, &sn, &cs);
+    T* row = qkv + (int64_t)r * 3 * d + hh * dh;
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {  // q, then k
+      T* x = row + part * d;
+      const float a = to_f32(x[i]), b = to_f32(x[i + half]);
+      x[i] = from_f32<T>(a * cs - b * sn);
+      x[i + half] = from_f32<T>(a * sn + b * cs);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// KV-cache write: row r's k / v go to slot kv_start[p] + pos[r].
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void kv_write_kernel(Plan pl, const T* __restrict__ qkv, int d,
+                                                       T* __restrict__ kc, T* __restrict__ vc) {
+  const int r = blockIdx.x;
+  const int p = pl.row_req[r];
+  const int64_t slot = (int64_t)pl.kv_start[p] + pl.pos[r];
+  const T* src = qkv + (int64_t)r * 3 * d;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    kc[slot * d + c] = src[d + c];
+    vc[slot * d + c] = src[2 * d + c];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Prefill attention, bf16, MFMA.
+// ---------------------------------------------------------------------------
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
+                                                                int d, bf16* __restrict__ out,
+                                                                float scale_log2) {
+  constexpr int KP = DH + 8;   // padded LDS row of K (bf16)
+  constexpr int VP = 64 + 8;   // padded LDS row of V^T
+  __shared__ __attribute__((aligned(16))) bf16 Ks[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
+  const int b = blockIdx.x, h = blockIdx.y;
+  const int p = upper_index(pl.qblk_off, pl.n_req + 1, b);
+  const int R = pl.cu_seqlens[p];
+  const int L = pl.cu_seqlens[p + 1] - R;
+  const int q0 = (b - pl.qblk_off[p]) * 64;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4;
+  const int qi = q0 + wave * 16 + (lane & 15);  // this lane's query (B-operand column)
+  const int64_t ld = 3 * (int64_t)d;
+
+  bf16x8 qf[DH / 32];
+  {
+    const bf16* qrow = qkv + (int64_t)(R + min(qi, L - 1)) * ld + h * DH + 8 * g;
+#pragma unroll
+    for (int s = 0; s < DH / 32; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(qrow + s * 32);
+  }
+  f32x4 o[DH / 16];
+#pragma unroll
+  for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = NEG_BIG, l_run = 0.f;
+
+  const int kend = CAUSAL ? min(L, q0 + 64) : L;
+  for (int kb = 0; kb < kend; kb += 64) {
+    // stage K (row-major) and V^T into LDS; rows past the request are zero
+    constexpr int CH = DH / 8;  // 16-byte chunks per key row
+    for (int c = tid; c < 64 * CH; c += 256) {
+      const int key = c / CH, ch = c % CH;
+      bf16x8 kv = {}, vv = {};
+      if (kb + key < L) {
+        const bf16* src = qkv + (int64_t)(R + kb + key) * ld + h * DH + ch * 8;
+        kv = *reinterpret_cast<const bf16x8*>(src + d);
+        vv = *reinterpret_cast<const bf16x8*>(src + 2 * d);
+      }
+      *reinterpret_cast<bf16x8*>(&Ks[key * KP + ch * 8]) = kv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(ch * 8 + e) * VP + key] = vv[e];
+    }
+    __syncthreads();
+
+    f32x4 st[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      st[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DH / 32; ++s) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(ks * 16 + (lane & 15)) * KP + s * 32 + 8 * g]);
+        st[ks] = mfma16(kf, qf[s], st[ks]);
+      }
+    }
+    // scale, mask, block max
+    float mb = NEG_BIG;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kb + ks * 16 + 4 * g + i;
+        float v = st[ks][i] * scale_log2;
+        const bool masked = key >= L || (CAUSAL && key > qi);
+        v = masked ? -INFINITY : v;
+        st[ks][i] = v;
+        mb = fmaxf(mb, v);
+      }
+    mb = fmaxf(mb, __shfl_xor(mb, 16, 64));
+    mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
+    const float m_new = fmaxf(m_run, mb);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float lsum = 0.f;
+    bf16x8 pf[2];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float e = exp2f(st[ks][i] - m_new);
+        lsum += e;
+        pf[ks >> 1][(ks & 1) * 4 + i] = (bf16)e;
+      }
+    l_run = l_run * alpha + lsum;
+#pragma unroll
+    for (int i = 0; i < DH / 16; ++i) o[i] *= alpha;
+    // O^T += V^T P^T over two 32-key steps
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int ds = 0; ds < DH / 16; ++ds) {
+        const bf16* vrow = &Vt[(ds * 16 + (lane & 15)) * VP + 32 * u + 4 * g];
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
+        bf16x8 vf;
+        vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
+        vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
+        o[ds] = mfma16(vf, pf[u], o[ds]);
+      }
+    }
+    __syncthreads();
+  }
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  if (qi < L) {
+    const float inv = 1.f / l_run;
+    bf16* orow = out + (int64_t)(R + qi) * d + h * DH + 4 * g;
+#pragma unroll
+    for (int ds = 0; ds < DH / 16; ++ds) {
+      bf16x4 v;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = (bf16)(o[ds][i] * inv);
+      *reinterpret_cast<bf16x4*>(orow + ds * 16) = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Prefill attention, generic SIMT (fp32 workloads): 64 queries per block,
+// 4 threads per query, each owning DH/4 dims; keys staged in LDS.
+// ---------------------------------------------------------------------------
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void attn_prefill_simt_kernel(Plan pl, const T* __restrict__ qkv,
+                                                                int d, T* __restrict__ out,
+                                                                float scale_log2, int causal) {
+  constexpr int DQ = DH / 4;
+  __shared__ float Ks[64][DH + 1];
+  __shared__ float Vs[64][DH + 1];
+  const int b = blockIdx.x, h = blockIdx.y;
+  const int p = upper_index(pl.qblk_off, pl.n_req + 1, b);
+  const int R = pl.cu_seqlens[p];
+  const int L = pl.cu_seqlens[p + 1] - R;
+  const int q0 = (b - pl.qblk_off[p]) * 64;
+  const int tid = threadIdx.x, qi = q0 + (tid >> 2), part = tid & 3;
+  const int64_t ld = 3 * (int64_t)d;
+  float q[DQ], o[DQ];
+  const T* qrow = qkv + (int64_t)(R + min(qi, L - 1)) * ld + h * DH + part * DQ;
+#pragma unroll
+  for (int i = 0; i < DQ; ++i) { q[i] = to_f32(qrow[i]); o[i] = 0.f; }
+  float m_run = NEG_BIG, l_run = 0.f;
+  const int kend = causal ? min(L, q0 + 64) : L;
+  for (int kb = 0; kb < kend; kb += 64) {
+    for (int e = tid; e < 64 * DH; e += 256) {
+      const int key = e / DH, c = e % DH;
+      float kv = 0.f, vv = 0.f;
+      if (kb + key < L) {
+        const T* src = qkv + (int64_t)(R + kb + key) * ld + h * DH + c;
+        kv = to_f32(src[d]);
+        vv = to_f32(src[2 * d]);
+      }
+      Ks[key][c] = kv;
+      Vs[key][c] = vv;
+    }
+    __syncthreads();
+    const int nk = min(64, kend - kb);
+    for (int j = 0; j < nk; ++j) {
+      const int key = kb + j;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < DQ; ++i) s += q[i] * Ks[j][part * DQ + i];
+      s += __shfl_xor(s, 1, 64);
+      s += __shfl_xor(s, 2, 64);
+      s *= scale_log2;
+      if (causal && key > qi) continue;
+      const float m_new = fmaxf(m_run, s);
+      const float alpha = exp2f(m_run - m_new), e = exp2f(s - m_new);
+      l_run = l_run * alpha + e;
+#pragma unroll
+      for (int i = 0; i < DQ; ++i) o[i] = o[i] * alpha + e * Vs[j][part * DQ + i];
+      m_run = m_new;
+    }
+    __syncthreads();
+  }
+  if (qi < L) {
+    T* orow = out + (int64_t)(R + qi) * d + h * DH + part * DQ;
+#pragma unroll
+    for (int i = 0; i < DQ; ++i) orow[i] = from_f32<T>(o[i] / l_run);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Decode attention: one query row per request against its cached keys
+// (slots kv_start .. kv_start + ctx, the last one just written).
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ inline void load8(const T* p, float (&v)[8]);
+template <>
+__device__ inline void load8<bf16>(const bf16* p, float (&v)[8]) {
+  const bf16x8 x = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (float)x[i];
+}
+template <>
+__device__ inline void load8<float>(const float* p, float (&v)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+template <typename T, int DH>
+__global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __restrict__ qkv, int d,
+                                                          const T* __restrict__ kc,
+                                                          const T* __restrict__ vc,
+                                                          T* __restrict__ out, float scale_log2) {
+  constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
+  constexpr int NG = 256 / LPK;        // key streams per block
+  __shared__ float sm[NG], sl[NG];
+  __shared__ float so[NG][DH + 1];
+  const int p = blockIdx.x, h = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int grp = tid / LPK, sub = tid % LPK;
+  const int R = pl.cu_seqlens[p];            // the request's (single) query row
+  const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
+  const int64_t base = (int64_t)pl.kv_start[p];
+  float q[8];
+  load8<T>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8, q);
+  float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
+  for (int k = grp; k < nkeys; k += NG) {
+    float kv[8], vv[8];
+    const int64_t off = (base + k) * d + h * DH + sub * 8;
+    load8<T>(kc + off, kv);
+    load8<T>(vc + off, vv);
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += q[i] * kv[i];
+#pragma unroll
+    for (int w = LPK / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+    s *= scale_log2;
+    const float m_new = fmaxf(m_run, s);
+    const float alpha = exp2f(m_run - m_new), e = exp2f(s - m_new);
+    l_run = l_run * alpha + e;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = o[i] * alpha + e * vv[i];
+    m_run = m_new;
+  }
+  if (sub == 0) { sm[grp] = m_run; sl[grp] = l_run; }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) so[grp][sub * 8 + i] = o[i];
+  __syncthreads();
+  if (tid < DH) {
+    float M = NEG_BIG;
+    for (int gq = 0; gq < NG; ++gq) M = fmaxf(M, sm[gq]);
+    float lsum = 0.f, acc = 0.f;
+    for (int gq = 0; gq < NG; ++gq) {
+      const float w = exp2f(sm[gq] - M);
+      lsum += sl[gq] * w;
+      acc += so[gq][tid] * w;
+    }
+    out[(int64_t)R * d + h * DH + tid] = from_f32<T>(acc / lsum);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
+                       float theta, hipStream_t s) {
+  const int64_t total = (int64_t)pl.T * n_heads * (head_dim / 2);
+  const int grid = (int)std::min<int64_t>((total + 255) / 256, 65536);
+  const float l2t = log2f(theta);
+  if (dtype == VFM_BF16)
+    hipLaunchKernelGGL(rope_kernel<bf16>, dim3(grid), dim3(256), 0, s, pl, (bf16*)qkv, d, n_heads, head_dim, l2t);
+  else
+    hipLaunchKernelGGL(rope_kernel<float>, dim3(grid), dim3(256), 0, s, pl, (float*)qkv, d, n_heads, head_dim, l2t);
+  return hipGetLastError();
+}
+
+size_t attention_workspace(const vfm_cfg&, const Plan&) { return 0; }
+
+hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv, void* out,
+                            void* k_cache, void* v_cache, void*, size_t, hipStream_t s) {
+  const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
+  const float scale_log2 = LOG2E / sqrtf((float)DH);
+  if (k_cache && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
+    if (dtype == VFM_BF16)
+      hipLaunchKernelGGL(kv_write_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (const bf16*)qkv, d,
+                         (bf16*)k_cache, (bf16*)v_cache);
+    else
+      hipLaunchKernelGGL(kv_write_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (const float*)qkv, d,
+                         (float*)k_cache, (float*)v_cache);
+  }
+  if (c.attn == VFM_ATTN_DECODE) {
+    dim3 grid(pl.n_req, H);
+#define DEC(TT, D_)                                                                          \
+  hipLaunchKernelGGL((attn_decode_kernel<TT, D_>), grid, dim3(256), 0, s, pl, (const TT*)qkv, d, \
+                     (const TT*)k_cache, (const TT*)v_cache, (TT*)out, scale_log2)
+    if (dtype == VFM_BF16) { if (DH == 64) DEC(bf16, 64); else DEC(bf16, 128); }
+    else { if (DH == 64) DEC(float, 64); else DEC(float, 128); }
+#undef DEC
+    return hipGetLastError();
+  }
+  dim3 grid(pl.n_qblocks, H);
+  const bool causal = c.attn == VFM_ATTN_CAUSAL;
+  if (dtype == VFM_BF16) {
+#define PRE(D_, C_)                                                                            \
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<D_, C_>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
+                     d, (bf16*)out, scale_log2)
+    if (DH == 64) { if (causal) PRE(64, true); else PRE(64, false); }
+    else { if (causal) PRE(128, true); else PRE(128, false); }
+#undef PRE
+  } else {
+    if (DH == 64)
+      hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 64>), grid, dim3(256), 0, s, pl,
+                         (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
+    else
+      hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 128>), grid, dim3(256), 0, s, pl,
+                         (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
+  }
+  return hipGetLastError();
+}

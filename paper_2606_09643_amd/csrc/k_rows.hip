@@ -1,0 +1,289 @@
+// Row-wise kernels: LayerNorm / RMSNorm (a2, a8), input embedding and
+// permutation into plan order (a1), final norm + pooling (a11).
+//
+// All of these are HBM-bound streaming passes over [T, d] rows.  One wave64
+// owns one row: each lane holds d/256 float4 chunks in registers, the mean and
+// variance are wave-level butterfly reductions, and every global access is a
+// coalesced 16-byte (fp32) or 8-byte (bf16x4) vector access.
+#include "vfm_internal.h"
+
+namespace {
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <typename T> __device__ inline float4 load4(const T* p);
+template <> __device__ inline float4 load4<float>(const float* p) {
+  return *reinterpret_cast<const float4*>(p);
+}
+template <> __device__ inline float4 load4<bf16>(const bf16* p) {
+  bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+  return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+}
+template <typename T> __device__ inline void store4(T* p, float4 v);
+template <> __device__ inline void store4<float>(float* p, float4 v) {
+  *reinterpret_cast<float4*>(p) = v;
+}
+template <> __device__ inline void store4<bf16>(bf16* p, float4 v) {
+  bf16x4 o;
+  o[0] = (bf16)v.x; o[1] = (bf16)v.y; o[2] = (bf16)v.z; o[3] = (bf16)v.w;
+  *reinterpret_cast<bf16x4*>(p) = o;
+}
+
+// Normalise one fp32 row held by one wave; MAXI = max float4 chunks per lane.
+template <typename TW, int MAXI>
+__device__ inline void norm_row_regs(const float* xr, int d, const TW* g, const TW* b, int kind,
+                                     float eps, float4 (&v)[MAXI]) {
+  const int lane = threadIdx.x & 63;
+  const int nch = d >> 2;
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nch) {
+      v[i] = *reinterpret_cast<const float4*>(xr + 4 * c);
+      sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+  }
+  float mean = 0.f;
+  if (kind == VFM_NORM_LAYER) mean = wave_sum(sum) / (float)d;
+  float sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nch) {
+      const float a = v[i].x - mean, bb = v[i].y - mean, cc = v[i].z - mean, dd = v[i].w - mean;
+      sq += (a * a + bb * bb) + (cc * cc + dd * dd);
+    }
+  }
+  const float rstd = rsqrtf(wave_sum(sq) / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nch) {
+      const float4 gg = load4<TW>(g + 4 * c);
+      float4 bb = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (b) bb = load4<TW>(b + 4 * c);
+      v[i].x = (v[i].x - mean) * rstd * gg.x + bb.x;
+      v[i].y = (v[i].y - mean) * rstd * gg.y + bb.y;
+      v[i].z = (v[i].z - mean) * rstd * gg.z + bb.z;
+      v[i].w = (v[i].w - mean) * rstd * gg.w + bb.w;
+    }
+  }
+}
+
+template <typename T, int MAXI>
+__global__ __launch_bounds__(256) void norm_rows_kernel(const float* __restrict__ x, int n_rows,
+                                                        int d, const T* __restrict__ g,
+                                                        const T* __restrict__ b, int kind,
+                                                        float eps, T* __restrict__ out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  float4 v[MAXI];
+  norm_row_regs<T, MAXI>(x + (int64_t)row * d, d, g, b, kind, eps, v);
+  const int lane = threadIdx.x & 63;
+  T* o = out + (int64_t)row * d;
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < (d >> 2)) store4<T>(o + 4 * c, v[i]);
+  }
+}
+
+// Final norm of every row, written fp32 in ORIGINAL request order.
+template <typename T, int MAXI>
+__global__ __launch_bounds__(256) void norm_rows_unpermute_kernel(
+    Plan pl, const float* __restrict__ x, int d, const T* __restrict__ g, const T* __restrict__ b,
+    int kind, float eps, float* __restrict__ out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= pl.T) return;
+  float4 v[MAXI];
+  norm_row_regs<T, MAXI>(x + (int64_t)row * d, d, g, b, kind, eps, v);
+  const int p = pl.row_req[row];
+  const int dst = pl.cu_orig[pl.order[p]] + (row - pl.cu_seqlens[p]);
+  const int lane = threadIdx.x & 63;
+  float* o = out + (int64_t)dst * d;
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < (d >> 2)) store4<float>(o + 4 * c, v[i]);
+  }
+}
+
+// Final norm + pooling: one block (4 waves) per request in plan order.
+template <typename T, int MAXI>
+__global__ __launch_bounds__(256) void norm_pool_kernel(Plan pl, const float* __restrict__ x,
+                                                        int d, const T* __restrict__ g,
+                                                        const T* __restrict__ b, int kind,
+                                                        float eps, int pool,
+                                                        T* __restrict__ pooled) {
+  extern __shared__ float acc[];  // [d]
+  const int p = blockIdx.x;
+  const int r0 = pl.cu_seqlens[p], r1 = pl.cu_seqlens[p + 1];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int i = threadIdx.x; i < d; i += 256) acc[i] = 0.f;
+  __syncthreads();
+  int first = r0, last = r1;
+  if (pool == VFM_POOL_FIRST) last = r0 + 1;
+  if (pool == VFM_POOL_LAST) first = r1 - 1;
+  float4 s[MAXI];
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) s[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int r = first + wave; r < last; r += 4) {
+    float4 v[MAXI];
+    norm_row_regs<T, MAXI>(x + (int64_t)r * d, d, g, b, kind, eps, v);
+#pragma unroll
+    for (int i = 0; i < MAXI; ++i) {
+      s[i].x += v[i].x; s[i].y += v[i].y; s[i].z += v[i].z; s[i].w += v[i].w;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < (d >> 2)) {
+      atomicAdd(&acc[4 * c + 0], s[i].x);
+      atomicAdd(&acc[4 * c + 1], s[i].y);
+      atomicAdd(&acc[4 * c + 2], s[i].z);
+      atomicAdd(&acc[4 * c + 3], s[i].w);
+    }
+  }
+  __syncthreads();
+  const float inv = 1.f / (float)(last - first);
+  for (int i = threadIdx.x; i < d; i += 256)
+    pooled[(int64_t)p * d + i] = from_f32<T>(acc[i] * inv);
+}
+
+// Map a plan-order row to its row in the caller's original order.
+__device__ inline int orig_row(const Plan& pl, int row) {
+  const int p = pl.row_req[row];
+  return pl.cu_orig[pl.order[p]] + (row - pl.cu_seqlens[p]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_rows_kernel(Plan pl, const T* __restrict__ src, int d,
+                                                         float* __restrict__ x) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= pl.T) return;
+  const int lane = threadIdx.x & 63;
+  const T* s = src + (int64_t)orig_row(pl, row) * d;
+  float* o = x + (int64_t)row * d;
+  for (int c = lane; c < (d >> 2); c += 64) store4<float>(o + 4 * c, load4<T>(s + 4 * c));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void embed_tokens_kernel(Plan pl, const int32_t* __restrict__ ids,
+                                                           int vocab, const T* __restrict__ table,
+                                                           int d, float* __restrict__ x) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= pl.T) return;
+  const int lane = threadIdx.x & 63;
+  const int id = ids[orig_row(pl, row)];
+  float* o = x + (int64_t)row * d;
+  if (id < 0 || id >= vocab) {
+    for (int c = lane; c < (d >> 2); c += 64) store4<float>(o + 4 * c, make_float4(0.f, 0.f, 0.f, 0.f));
+    return;
+  }
+  const T* s = table + (int64_t)id * d;
+  for (int c = lane; c < (d >> 2); c += 64) store4<float>(o + 4 * c, load4<T>(s + 4 * c));
+}
+
+// Patch embedding x = W_pe patch + b_pe, one wave per row, width <= 64.
+template <typename T>
+__global__ __launch_bounds__(256) void embed_patches_kernel(Plan pl, const float* __restrict__ src,
+                                                            int width, const T* __restrict__ W,
+                                                            const T* __restrict__ bias, int d,
+                                                            float* __restrict__ x) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= pl.T) return;
+  const int lane = threadIdx.x & 63;
+  const float* s = src + (int64_t)orig_row(pl, row) * width;
+  const float mine = lane < width ? s[lane] : 0.f;
+  float* o = x + (int64_t)row * d;
+  for (int n = lane; n < d; n += 64) {
+    const T* w = W + (int64_t)n * width;
+    float acc = bias ? to_f32(bias[n]) : 0.f;
+    for (int k = 0; k < width; ++k) acc += to_f32(w[k]) * __shfl(mine, k, 64);
+    o[n] = acc;
+  }
+}
+
+inline int maxi_for(int d) { return d <= 1024 ? 4 : (d <= 4096 ? 16 : 32); }
+
+}  // namespace
+
+hipError_t launch_norm(int dtype, const float* x, int T, int d, const void* g, const void* b,
+                       int kind, float eps, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  dim3 grid((T + 3) / 4), block(256);
+  const int mi = maxi_for(d);
+#define NORM_LAUNCH(TT, MI)                                                                   \
+  hipLaunchKernelGGL((norm_rows_kernel<TT, MI>), grid, block, 0, s, x, T, d, (const TT*)g,  \
+                     (const TT*)b, kind, eps, (TT*)out)
+  if (dtype == VFM_BF16) {
+    if (mi == 4) NORM_LAUNCH(bf16, 4); else if (mi == 16) NORM_LAUNCH(bf16, 16); else NORM_LAUNCH(bf16, 32);
+  } else {
+    if (mi == 4) NORM_LAUNCH(float, 4); else if (mi == 16) NORM_LAUNCH(float, 16); else NORM_LAUNCH(float, 32);
+  }
+#undef NORM_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_pool(int dtype, const Plan& pl, const float* x, int d, const void* g,
+                            const void* b, int kind, float eps, int pool, void* pooled,
+                            float* rows_out, hipStream_t s) {
+  const int mi = maxi_for(d);
+  if (pool < 0) {
+    dim3 grid((pl.T + 3) / 4), block(256);
+#define NP_LAUNCH(TT, MI)                                                                      \
+  hipLaunchKernelGGL((norm_rows_unpermute_kernel<TT, MI>), grid, block, 0, s, pl, x, d,      \
+                     (const TT*)g, (const TT*)b, kind, eps, rows_out)
+    if (dtype == VFM_BF16) {
+      if (mi == 4) NP_LAUNCH(bf16, 4); else if (mi == 16) NP_LAUNCH(bf16, 16); else NP_LAUNCH(bf16, 32);
+    } else {
+      if (mi == 4) NP_LAUNCH(float, 4); else if (mi == 16) NP_LAUNCH(float, 16); else NP_LAUNCH(float, 32);
+    }
+#undef NP_LAUNCH
+    return hipGetLastError();
+  }
+  dim3 grid(pl.n_req), block(256);
+  const size_t lds = (size_t)d * sizeof(float);
+#define PL_LAUNCH(TT, MI)                                                                     \
+  hipLaunchKernelGGL((norm_pool_kernel<TT, MI>), grid, block, lds, s, pl, x, d, (const TT*)g, \
+                     (const TT*)b, kind, eps, pool, (TT*)pooled)
+  if (dtype == VFM_BF16) {
+    if (mi == 4) PL_LAUNCH(bf16, 4); else if (mi == 16) PL_LAUNCH(bf16, 16); else PL_LAUNCH(bf16, 32);
+  } else {
+    if (mi == 4) PL_LAUNCH(float, 4); else if (mi == 16) PL_LAUNCH(float, 16); else PL_LAUNCH(float, 32);
+  }
+#undef PL_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_embed(int dtype, const Plan& pl, int mode, const void* src, int width,
+                        const void* table, const void* bias, int d, float* x, hipStream_t s) {
+  dim3 grid((pl.T + 3) / 4), block(256);
+  if (mode == VFM_EMBED_ROWS) {
+    if (dtype == VFM_BF16)
+      hipLaunchKernelGGL(embed_rows_kernel<bf16>, grid, block, 0, s, pl, (const bf16*)src, d, x);
+    else
+      hipLaunchKernelGGL(embed_rows_kernel<float>, grid, block, 0, s, pl, (const float*)src, d, x);
+  } else if (mode == VFM_EMBED_TOKENS) {
+    if (dtype == VFM_BF16)
+      hipLaunchKernelGGL(embed_tokens_kernel<bf16>, grid, block, 0, s, pl, (const int32_t*)src,
+                         width, (const bf16*)table, d, x);
+    else
+      hipLaunchKernelGGL(embed_tokens_kernel<float>, grid, block, 0, s, pl, (const int32_t*)src,
+                         width, (const float*)table, d, x);
+  } else {
+    if (dtype == VFM_BF16)
+      hipLaunchKernelGGL(embed_patches_kernel<bf16>, grid, block, 0, s, pl, (const float*)src,
+                         width, (const bf16*)table, (const bf16*)bias, d, x);
+    else
+      hipLaunchKernelGGL(embed_patches_kernel<float>, grid, block, 0, s, pl, (const float*)src,
+                         width, (const float*)table, (const float*)bias, d, x);
+  }
+  return hipGetLastError();
+}

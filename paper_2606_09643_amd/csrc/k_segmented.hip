@@ -1,0 +1,246 @@
+// Per-task segmented kernels: LoRA shrink (a4), LoRA expand (the standalone
+// vfm_lora_apply), and the per-task linear heads (a12).
+//
+// Rows are in plan order, so every task owns one contiguous segment of rows
+// (and of requests).  Work is split into VFM_ROW_TILE-row tiles that never
+// cross a task boundary (the plan's rtile_off), so a skewed task mix (a Zipf
+// head task holding a third of the rows) still spreads over many blocks, and
+// each block reads exactly one task's factors.  The task's A / B / head
+// weights are gathered through the per-task pointer tables, so attaching or
+// removing a task is a pointer update (paper Section 4.1 task extensions;
+// Table 1 attach_adapter / remove_adapter).
+//
+// bf16: v_mfma_f32_16x16x32_bf16 with operands read straight from global
+// memory (16-byte per-lane loads); the adapter factor feeds the MFMA A slot,
+// the activation rows the B slot, so each lane ends with 4 consecutive
+// output columns of one row.  fp32: plain per-thread dot products.
+#include "vfm_internal.h"
+
+namespace {
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Locate the task and row range of segmented tile `bid`.
+__device__ inline void tile_rows(const Plan& pl, int bid, int& t, int& r0, int& r1) {
+  t = upper_index(pl.rtile_off, pl.n_tasks + 1, bid);
+  r0 = pl.seg_row[t] + (bid - pl.rtile_off[t]) * VFM_ROW_TILE;
+  r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
+}
+
+// ---------------------------------------------------------------------------
+// shrink: U[m, ucol + j] = s_t * X[m, :] . A_t[j, :]   (j < rpad, zero past r_t)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
+  int t, r0, r1;
+  tile_rows(pl, blockIdx.x, t, r0, r1);
+  const int p = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rank = min(a.rank[t], a.rpad) & ~7;
+  const float sc = a.scale[t];
+  const bf16* X = (const bf16*)a.X;
+  const bf16* At = rank > 0 ? (const bf16*)a.A[p][t] : nullptr;
+  bf16* U = (bf16*)a.U;
+  const int mrow = r0 + wave * 16 + (lane & 15);
+  const int nsub = a.rpad >> 4;
+  f32x4 acc[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) acc[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (rank > 0 && r0 + wave * 16 < r1) {
+    const bf16* xrow = X + (int64_t)min(mrow, r1 - 1) * a.ldx + 8 * (lane >> 4);
+#pragma unroll 4
+    for (int k = 0; k < a.K; k += 32) {
+      const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s >= nsub) break;
+        const int j = s * 16 + (lane & 15);
+        bf16x8 af = {};
+        if (j < rank) af = *reinterpret_cast<const bf16x8*>(At + (int64_t)j * a.K + k + 8 * (lane >> 4));
+        acc[s] = mfma16(af, xf, acc[s]);
+      }
+    }
+  }
+  const int m = r0 + wave * 16 + (lane & 15);
+  if (m < r1) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s >= nsub) break;
+      bf16x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[s][i] * sc);
+      *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[p] + s * 16 + 4 * (lane >> 4)) = o;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void shrink_f32_kernel(Plan pl, ShrinkArgs a) {
+  int t, r0, r1;
+  tile_rows(pl, blockIdx.x, t, r0, r1);
+  const int p = blockIdx.y;
+  const int rank = min(a.rank[t], a.rpad) & ~7;
+  const float sc = a.scale[t];
+  const float* X = (const float*)a.X;
+  const float* At = rank > 0 ? (const float*)a.A[p][t] : nullptr;
+  float* U = (float*)a.U;
+  const int rows = r1 - r0;
+  for (int e = threadIdx.x; e < rows * a.rpad; e += 256) {
+    const int m = r0 + e / a.rpad, j = e % a.rpad;
+    float s = 0.f;
+    if (j < rank) {
+      const float* x = X + (int64_t)m * a.ldx;
+      const float* w = At + (int64_t)j * a.K;
+      for (int k = 0; k < a.K; ++k) s += x[k] * w[k];
+    }
+    U[(int64_t)m * a.ldu + a.ucol[p] + j] = s * sc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// expand: Y[m, n] += U[m, ucol + :r] . B_t[n, :r]     (fp32 Y)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void expand_bf16_kernel(Plan pl, ExpandArgs a) {
+  int t, r0, r1;
+  tile_rows(pl, blockIdx.x, t, r0, r1);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rank = min(a.rank[t], a.max_rank) & ~7;
+  const int wr0 = r0 + wave * 16;
+  if (rank <= 0 || wr0 >= r1) return;
+  const int n0 = blockIdx.y * 64;
+  const bf16* U = (const bf16*)a.U;
+  const bf16* Bt = (const bf16*)a.B[t];
+  f32x4 acc[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) acc[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int m = wr0 + (lane & 15);
+  for (int kk = 0; kk < rank; kk += 32) {
+    const int kof = kk + 8 * (lane >> 4);
+    bf16x8 xf = {};
+    if (m < r1 && kof < rank) xf = *reinterpret_cast<const bf16x8*>(U + (int64_t)m * a.ldu + a.ucol + kof);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int n = n0 + s * 16 + (lane & 15);
+      bf16x8 wf = {};
+      if (n < a.N && kof < rank) wf = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)n * rank + kof);
+      acc[s] = mfma16(wf, xf, acc[s]);
+    }
+  }
+  if (m >= r1) return;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int n = n0 + s * 16 + 4 * (lane >> 4);
+    if (n >= a.N) continue;
+    float4* dst = reinterpret_cast<float4*>(a.Y + (int64_t)m * a.ldy + n);
+    float4 o = *dst;
+    o.x += acc[s][0]; o.y += acc[s][1]; o.z += acc[s][2]; o.w += acc[s][3];
+    *dst = o;
+  }
+}
+
+__global__ __launch_bounds__(256) void expand_f32_kernel(Plan pl, ExpandArgs a) {
+  int t, r0, r1;
+  tile_rows(pl, blockIdx.x, t, r0, r1);
+  const int rank = min(a.rank[t], a.max_rank) & ~7;
+  if (rank <= 0) return;
+  const int n0 = blockIdx.y * 64;
+  const float* U = (const float*)a.U;
+  const float* Bt = (const float*)a.B[t];
+  for (int e = threadIdx.x; e < (r1 - r0) * 64; e += 256) {
+    const int m = r0 + e / 64, n = n0 + e % 64;
+    if (n >= a.N) continue;
+    float s = 0.f;
+    for (int j = 0; j < rank; ++j) s += U[(int64_t)m * a.ldu + a.ucol + j] * Bt[(int64_t)n * rank + j];
+    a.Y[(int64_t)m * a.ldy + n] += s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// heads: out[out_off[order[p]] + n] = pooled[p] . W_t[n] + b_t[n]
+// One block per (task, 64-column chunk); the block walks the task's
+// requests 16 at a time; each wave owns 16 of the 64 columns.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void heads_bf16_kernel(Plan pl, const bf16* __restrict__ pooled,
+                                                         int d, vfm_head_table h,
+                                                         float* __restrict__ out) {
+  const int t = blockIdx.x;
+  const int n_out = h.n_out[t];
+  const int n0 = blockIdx.y * 64;
+  const int p0 = pl.seg_req[t], p1 = pl.seg_req[t + 1];
+  if (p0 == p1 || n0 >= n_out) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bf16* Wt = (const bf16*)h.W[t];
+  const bf16* bt = h.b ? (const bf16*)h.b[t] : nullptr;
+  const int nrow = n0 + wave * 16 + (lane & 15);
+  const bf16* wrow = Wt + (int64_t)min(nrow, n_out - 1) * d + 8 * (lane >> 4);
+  for (int pb = p0; pb < p1; pb += 16) {
+    const int p = pb + (lane & 15);
+    const bf16* xrow = pooled + (int64_t)min(p, p1 - 1) * d + 8 * (lane >> 4);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int k = 0; k < d; k += 32) {
+      const bf16x8 wf = *reinterpret_cast<const bf16x8*>(wrow + k);
+      const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
+      acc = mfma16(wf, xf, acc);
+    }
+    if (p < p1) {
+      const int req = pl.order[p];
+      const int lim = min(n_out, pl.out_off[req + 1] - pl.out_off[req]);
+      float* o = out + pl.out_off[req];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int n = n0 + wave * 16 + 4 * (lane >> 4) + i;
+        if (n < lim) o[n] = acc[i] + (bt ? (float)bt[n] : 0.f);
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void heads_f32_kernel(Plan pl, const float* __restrict__ pooled,
+                                                        int d, vfm_head_table h,
+                                                        float* __restrict__ out) {
+  const int t = blockIdx.x;
+  const int n_out = h.n_out[t];
+  const int n0 = blockIdx.y * 64;
+  const int p0 = pl.seg_req[t], p1 = pl.seg_req[t + 1];
+  if (p0 == p1 || n0 >= n_out) return;
+  const float* Wt = (const float*)h.W[t];
+  const float* bt = h.b ? (const float*)h.b[t] : nullptr;
+  for (int e = threadIdx.x; e < (p1 - p0) * 64; e += 256) {
+    const int p = p0 + e / 64, n = n0 + e % 64;
+    const int req = pl.order[p];
+    if (n >= min(n_out, pl.out_off[req + 1] - pl.out_off[req])) continue;
+    float s = bt ? bt[n] : 0.f;
+    for (int k = 0; k < d; ++k) s += pooled[(int64_t)p * d + k] * Wt[(int64_t)n * d + k];
+    out[pl.out_off[req] + n] = s;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s) {
+  if (pl.n_rtiles == 0 || a.n_proj == 0) return hipSuccess;
+  dim3 grid(pl.n_rtiles, a.n_proj);
+  if (dtype == VFM_BF16) hipLaunchKernelGGL(shrink_bf16_kernel, grid, dim3(256), 0, s, pl, a);
+  else hipLaunchKernelGGL(shrink_f32_kernel, grid, dim3(256), 0, s, pl, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_expand(int dtype, const Plan& pl, const ExpandArgs& a, hipStream_t s) {
+  if (pl.n_rtiles == 0) return hipSuccess;
+  dim3 grid(pl.n_rtiles, (a.N + 63) / 64);
+  if (dtype == VFM_BF16) hipLaunchKernelGGL(expand_bf16_kernel, grid, dim3(256), 0, s, pl, a);
+  else hipLaunchKernelGGL(expand_f32_kernel, grid, dim3(256), 0, s, pl, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_heads(int dtype, const Plan& pl, const void* pooled, int d,
+                        const vfm_head_table& h, float* out, hipStream_t s) {
+  dim3 grid(h.n_tasks, (h.max_out + 63) / 64);
+  if (grid.y == 0) return hipSuccess;
+  if (dtype == VFM_BF16)
+    hipLaunchKernelGGL(heads_bf16_kernel, grid, dim3(256), 0, s, pl, (const bf16*)pooled, d, h, out);
+  else
+    hipLaunchKernelGGL(heads_f32_kernel, grid, dim3(256), 0, s, pl, (const float*)pooled, d, h, out);
+  return hipGetLastError();
+}

@@ -1,0 +1,177 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "vfm.h"
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+#define VFM_WAVE 64
+
+// Offsets of the plan arrays inside the int32 plan buffer (layout documented
+// in vfm.h).  Shared by host and device code.
+struct PlanOffsets {
+  int64_t order, task, cu_seqlens, seg_req, seg_row, cu_orig, out_off, ctx, kv_start, qblk_off,
+      rtile_off, row_task, row_req, pos, total;
+};
+
+__host__ __device__ inline PlanOffsets plan_offsets(int64_t n_req, int64_t n_tasks, int64_t T) {
+  PlanOffsets o;
+  int64_t p = VFM_PLAN_HEADER;
+  o.order = p;      p += n_req;
+  o.task = p;       p += n_req;
+  o.cu_seqlens = p; p += n_req + 1;
+  o.seg_req = p;    p += n_tasks + 1;
+  o.seg_row = p;    p += n_tasks + 1;
+  o.cu_orig = p;    p += n_req + 1;
+  o.out_off = p;    p += n_req + 1;
+  o.ctx = p;        p += n_req;
+  o.kv_start = p;   p += n_req;
+  o.qblk_off = p;   p += n_req + 1;
+  o.rtile_off = p;  p += n_tasks + 1;
+  o.row_task = p;   p += T;
+  o.row_req = p;    p += T;
+  o.pos = p;        p += T;
+  o.total = p;
+  return o;
+}
+
+// Device-side view of a plan.
+struct Plan {
+  const int32_t *order, *task, *cu_seqlens, *seg_req, *seg_row, *cu_orig, *out_off, *ctx,
+      *kv_start, *qblk_off, *rtile_off, *row_task, *row_req, *pos;
+  int32_t n_req, n_tasks, T, max_seqlen, n_qblocks, n_rtiles, total_outputs;
+};
+
+inline Plan make_plan(const int32_t* host, const int32_t* dev) {
+  Plan p;
+  p.n_req = host[0];
+  p.n_tasks = host[1];
+  p.T = host[2];
+  p.max_seqlen = host[3];
+  p.n_qblocks = host[4];
+  p.n_rtiles = host[5];
+  p.total_outputs = host[6];
+  PlanOffsets o = plan_offsets(p.n_req, p.n_tasks, p.T);
+  p.order = dev + o.order;
+  p.task = dev + o.task;
+  p.cu_seqlens = dev + o.cu_seqlens;
+  p.seg_req = dev + o.seg_req;
+  p.seg_row = dev + o.seg_row;
+  p.cu_orig = dev + o.cu_orig;
+  p.out_off = dev + o.out_off;
+  p.ctx = dev + o.ctx;
+  p.kv_start = dev + o.kv_start;
+  p.qblk_off = dev + o.qblk_off;
+  p.rtile_off = dev + o.rtile_off;
+  p.row_task = dev + o.row_task;
+  p.row_req = dev + o.row_req;
+  p.pos = dev + o.pos;
+  return p;
+}
+
+// Largest i in [0, n) with arr[i] <= v, for a non-decreasing arr (arr[0] <= v).
+__device__ inline int upper_index(const int32_t* arr, int n, int v) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (arr[mid] <= v) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ inline float to_f32(float v) { return v; }
+__device__ inline float to_f32(bf16 v) { return (float)v; }
+template <typename T> __device__ inline T from_f32(float v);
+template <> __device__ inline float from_f32<float>(float v) { return v; }
+template <> __device__ inline bf16 from_f32<bf16>(float v) { return (bf16)v; }
+
+// Benchmark timing hooks (profile.hip): bracket one launch of class `cls`.
+int prof_begin(int cls, hipStream_t s);
+void prof_end(int idx, hipStream_t s);
+
+// ---- launchers implemented in the kernel translation units ---------------
+// All return hipSuccess or the launch error.  Shapes are validated by the API
+// layer before any of these is called.
+
+// LayerNorm / RMSNorm of fp32 rows into dtype rows.
+hipError_t launch_norm(int dtype, const float* x, int T, int d, const void* g, const void* b,
+                       int kind, float eps, void* out, hipStream_t s);
+
+// Segmented LoRA shrink: U[m, ucol[p] + j] = scale_t * sum_k X[m,k] A_{t,p}[j,k]
+// for j < rank_t, zero for rank_t <= j < rpad; p over n_proj projections.
+struct ShrinkArgs {
+  const void* X; int ldx; int K;
+  const void* const* A[3]; int ucol[3]; int n_proj;
+  void* U; int ldu; int rpad;
+  const int32_t* rank; const float* scale;
+};
+hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s);
+
+// Segmented LoRA expand into fp32: Y[m, n] += sum_j U[m, ucol + j] B_t[n, j].
+struct ExpandArgs {
+  const void* U; int ldu; int ucol;
+  const void* const* B; int N;
+  float* Y; int ldy;
+  const int32_t* rank; int max_rank;
+};
+hipError_t launch_lora_expand(int dtype, const Plan& pl, const ExpandArgs& a, hipStream_t s);
+
+// Shared GEMM  C[m, n] = sum_k X[m, k] W[n, k]  with a fused epilogue.
+enum GemmEpi {
+  EPI_STORE = 0,      // out(dtype)[m, n] = acc + bias
+  EPI_GELU = 1,       // out(dtype)[m, n] = GELU(acc + bias)
+  EPI_RESID = 2,      // x(fp32)[m, n] += acc + bias
+  EPI_SWIGLU = 3      // out(dtype)[m, j] = SiLU(gate) * up; W = gate rows, W2 = up rows
+};
+struct GemmLora {
+  // Optional per-task LoRA expand fused into the GEMM, up to 3 column slots
+  // (q/k/v of a stacked projection, or gate/up of SwiGLU).  Column n belongs
+  // to slot n / slot_width (SwiGLU: gate = slot 0, up = slot 1).
+  int enabled;
+  const void* U; int ldu; int ucol[3];
+  const void* const* B[3];
+  int slot_width;
+  const int32_t* rank; const int32_t* row_task; const int32_t* seg_row;
+  int max_rank;
+};
+struct GemmArgs {
+  const void* X; int ldx;
+  const void* W; const void* W2;   // W2: SwiGLU up weights
+  const void* bias;                // [N] dtype or NULL
+  int M, N, K;                     // N = output columns (SwiGLU: d_ff)
+  int epi;
+  void* out; int ldo;              // EPI_STORE/GELU/SWIGLU (dtype) or EPI_RESID (fp32)
+  GemmLora lora;
+};
+hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
+
+// In-place rotary embedding of the q and k parts of qkv [T, 3d].
+hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
+                       float theta, hipStream_t s);
+
+// Attention per request over qkv [T, 3d] (plan order) into out [T, d].
+hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv,
+                            void* out, void* k_cache, void* v_cache, void* ws, size_t ws_bytes,
+                            hipStream_t s);
+size_t attention_workspace(const vfm_cfg& c, const Plan& pl);
+
+// Input rows into the fp32 residual stream (plan order).
+hipError_t launch_embed(int dtype, const Plan& pl, int mode, const void* src, int width,
+                        const void* table, const void* bias, int d, float* x, hipStream_t s);
+
+// Final norm + pooling into pooled [n_req, d] (dtype, plan order), or the
+// final-normed rows [T, d] fp32 in original order when pool < 0.
+hipError_t launch_norm_pool(int dtype, const Plan& pl, const float* x, int d, const void* g,
+                            const void* b, int kind, float eps, int pool, void* pooled,
+                            float* rows_out, hipStream_t s);
+
+// Per-task heads on pooled rows: out[out_off[i] + j] = pooled[p] . W_t[j] + b_t[j].
+hipError_t launch_heads(int dtype, const Plan& pl, const void* pooled, int d,
+                        const vfm_head_table& h, float* out, hipStream_t s);

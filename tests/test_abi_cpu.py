@@ -1,0 +1,135 @@
+"""Host-side checks of the C ABI (no GPU): the library loads and exports every
+entry point declared in include/vfm.h; vfm_plan (host integer code) equals the
+oracle's plan bit for bit; argument validation rejects bad calls before any
+launch."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import vfm_oracle as O
+from paper_2606_09643_amd import binding as B
+from paper_2606_09643_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for f in os.listdir(os.path.join(ROOT, "include")):
+        if f.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", f)).read()
+            names |= set(re.findall(r"^\s*(?:int|const char\*)\s+(vfm_\w+)\s*\(", src, re.M))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    decl = _declared()
+    assert {"vfm_plan", "vfm_layer_forward", "vfm_lora_apply", "vfm_head_forward"} <= decl
+    for name in decl:
+        assert hasattr(lib, name), name
+    assert set(B.EXPORTS) == decl
+
+
+def _unpack(host):
+    n_req, n_tasks, T = int(host[0]), int(host[1]), int(host[2])
+    p = B.VFM_PLAN_HEADER
+    out = {}
+    for name, n in [("order", n_req), ("task", n_req), ("cu_seqlens", n_req + 1),
+                    ("seg_req", n_tasks + 1), ("seg_row", n_tasks + 1), ("cu_orig", n_req + 1),
+                    ("logit_off", n_req + 1), ("ctx", n_req), ("kv_start", n_req),
+                    ("qblk_off", n_req + 1), ("rtile_off", n_tasks + 1), ("row_task", T),
+                    ("row_req", T), ("pos", T)]:
+        out[name] = host[p:p + n].astype(np.int64)
+        p += n
+    assert p == host.size
+    return out
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_plan_matches_oracle_bit_exact(idx):
+    w = wl.WORKLOADS[idx]
+    b = wl.draw_batch(w)
+    n_out = wl.draw_head_sizes(w)
+    kvs = wl.kv_offsets(b).astype(np.int32) if b.ctx is not None else None
+    host = B.vfm_plan(b.task_id, b.seq_len, w.n_tasks, b.ctx, kvs, n_out)
+    got = _unpack(host)
+    ref = O.plan(b.task_id, b.seq_len, w.n_tasks, ctx=b.ctx, n_out=n_out)
+    for k in ("order", "task", "cu_seqlens", "seg_req", "seg_row", "cu_orig", "logit_off",
+              "pos", "row_req"):
+        assert np.array_equal(got[k], ref[k]), k
+    assert np.array_equal(got["row_task"], ref["task"][ref["row_req"]])
+    lens = b.seq_len[ref["order"]]
+    assert np.array_equal(np.diff(got["qblk_off"]), (lens + 63) // 64)
+    rows_t = np.diff(ref["seg_row"])
+    assert np.array_equal(np.diff(got["rtile_off"]), (rows_t + 63) // 64)
+    assert host[0] == w.n_req and host[1] == w.n_tasks and host[2] == b.total_rows
+    assert host[3] == b.seq_len.max() and host[6] == ref["logit_off"][-1]
+
+
+def test_plan_random_and_edges():
+    r = np.random.default_rng(0)
+    for _ in range(200):
+        n_tasks = int(r.integers(1, 9))
+        n_req = int(r.integers(1, 40))
+        tid = r.integers(0, n_tasks, size=n_req)
+        lens = r.integers(1, 300, size=n_req)
+        host = B.vfm_plan(tid, lens, n_tasks)
+        got, ref = _unpack(host), O.plan(tid, lens, n_tasks)
+        for k in ("order", "cu_seqlens", "seg_req", "seg_row", "pos", "row_req"):
+            assert np.array_equal(got[k], ref[k])
+
+
+def test_plan_rejects_bad_input():
+    with pytest.raises(B.VfmError) as e:
+        B.vfm_plan([0, 4], [1, 1], 4)
+    assert e.value.status == B.VFM_ERR_TASK
+    with pytest.raises(B.VfmError) as e:
+        B.vfm_plan([0, 1], [1, 0], 4)
+    assert e.value.status == B.VFM_ERR_SHAPE
+    with pytest.raises(B.VfmError):
+        B.vfm_plan_size(0, 4, 0)
+
+
+def _batch_c(host):
+    return B.vfm_batch(host.ctypes.data_as(C.POINTER(C.c_int32)), 1 << 20, host.size)
+
+
+def test_validation_rejects_before_launch():
+    """Every call below fails host-side validation, so nothing reaches the GPU."""
+    w = wl.WORKLOADS[2]
+    host = B.vfm_plan([0, 1, 1], [5, 3, 2], 2)
+    bc = _batch_c(host)
+    lib = B.lib()
+    cfg = B.make_cfg(B.VFM_BF16, 768, 12, 64, 3072, 0, 0, 0, 1, 1e-5, 0.0)
+    n = C.c_size_t()
+    assert lib.vfm_workspace_size(C.byref(cfg), C.byref(bc), None, C.byref(n)) == 0 and n.value > 0
+    bad = B.make_cfg(B.VFM_BF16, 768, 8, 96, 3072, 0, 0, 0, 1, 1e-5, 0.0)
+    assert lib.vfm_workspace_size(C.byref(bad), C.byref(bc), None, C.byref(n)) == B.VFM_ERR_UNSUPPORTED
+    bad = B.make_cfg(B.VFM_BF16, 768, 11, 64, 3072, 0, 0, 0, 1, 1e-5, 0.0)
+    assert lib.vfm_workspace_size(C.byref(bad), C.byref(bc), None, C.byref(n)) == B.VFM_ERR_SHAPE
+    bad = B.make_cfg(7, 768, 12, 64, 3072, 0, 0, 0, 1, 1e-5, 0.0)
+    assert lib.vfm_workspace_size(C.byref(bad), C.byref(bc), None, C.byref(n)) == B.VFM_ERR_ARG
+    weights = B.vfm_layer_weights(*([1 << 20] * 13))
+    x = 1 << 20
+    # workspace missing
+    st = lib.vfm_layer_forward(C.byref(cfg), C.byref(weights), None, C.byref(bc), x, None, None, 0,
+                               None, 0, None)
+    assert st == B.VFM_ERR_WORKSPACE
+    # decode without a cache
+    dec = B.make_cfg(B.VFM_BF16, 768, 12, 64, 3072, 0, 0, B.VFM_ATTN_DECODE, 1, 1e-5, 0.0)
+    st = lib.vfm_layer_forward(C.byref(dec), C.byref(weights), None, C.byref(bc), x, None, None, 0,
+                               1 << 20, 1 << 40, None)
+    assert st == B.VFM_ERR_ARG
+    # lora table for the wrong number of tasks
+    lt = B.vfm_lora_table(5, 16, 1 << 20, 1 << 20)
+    st = lib.vfm_layer_forward(C.byref(cfg), C.byref(weights), C.byref(lt), C.byref(bc), x, None,
+                               None, 0, 1 << 20, 1 << 40, None)
+    assert st == B.VFM_ERR_SHAPE
+    # SwiGLU with biases is not supported
+    sw = B.make_cfg(B.VFM_BF16, 768, 12, 64, 3072, 1, 1, 1, 1, 1e-6, 1e4)
+    assert lib.vfm_workspace_size(C.byref(sw), C.byref(bc), None, C.byref(n)) == B.VFM_ERR_UNSUPPORTED
+    assert B.vfm_status_string(B.VFM_ERR_TASK) == "task id out of range"

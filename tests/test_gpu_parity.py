@@ -1,0 +1,308 @@
+"""GPU parity of the HIP path against the fp64 oracle, call by call.
+
+Every case feeds the oracle exactly the tensors the GPU received (the GPU
+layer's own input rows are downloaded before each layer), and compares with
+the row-normwise relative error (max over rows of max|g - o| / max|o|):
+2e-2 for bf16 workloads, 1e-5 for the fp32 one.  Integer plan outputs are
+checked bit-exact on the host (tests/test_abi_cpu.py).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import vfm_oracle as O
+from paper_2606_09643_amd import binding as B
+from paper_2606_09643_amd import runner as R
+from paper_2606_09643_amd import workloads as wl
+from tests.gpu_common import (expected_embed, log, oracle_heads, oracle_layer_rows, oracle_plan,
+                              pick_requests, tol)
+from tests.helpers import np64, oracle_adapter, oracle_weights
+
+pytestmark = pytest.mark.gpu
+
+
+def _batch(w, task_id, seq_len, ctx=None):
+    return wl.Batch(np.asarray(task_id, np.int32), np.asarray(seq_len, np.int32),
+                    None if ctx is None else np.asarray(ctx, np.int32))
+
+
+# Small cases per workload: real widths, few requests, ragged lengths.
+SMALL = {
+    1: dict(task_id=[3, 0, 1, 1, 2, 0, 3, 2], seq_len=[64] * 8),
+    2: dict(task_id=[5, 0, 5, 2, 9, 0], seq_len=[197] * 6),
+    3: dict(task_id=[1, 1, 7, 0, 31, 7], seq_len=[64] * 6),
+    4: dict(task_id=[3, 0, 3, 63], seq_len=[1, 130, 64, 77]),
+    5: dict(task_id=[2, 2, 0, 127, 5], seq_len=[1] * 5, ctx=[0, 63, 300, 64, 2048]),
+}
+
+
+def _setup(idx, n_layers=1, b_std=0.01, ranks=None, case=None):
+    w = wl.WORKLOADS[idx]
+    case = case or SMALL[idx]
+    batch = _batch(w, **case)
+    model = R.Model(w, n_layers=n_layers, b_std=b_std, ranks=ranks)
+    inp = R.Inputs(w, batch)
+    kv = R.KVCache(w, batch, n_layers) if w.mode == "decode" else None
+    pb = R.make_batch(w, batch, model.heads, kv)
+    fwd = R.Forward(model, pb, inp, kv)
+    pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
+    return w, batch, model, inp, kv, pb, fwd, pl
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_embed_exact(idx):
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(idx)
+    log(f"embed workload {idx} T={pb.T}")
+    fwd.embed()
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    ref = expected_embed(w, batch, inp, pl)
+    if inp.mode == B.VFM_EMBED_PATCHES:
+        assert O.row_rel_error(got, ref) < 1e-5
+    else:
+        assert np.array_equal(got, ref)
+
+
+# b_std 0.1 makes the adapters' difference about as large as the shared
+# projection itself (std ~0.8 vs ~1), so a LoRA slip cannot hide under the
+# tolerance; much larger factors (0.3) push the attention logits' spread to
+# ~7 where the bf16 rounding of q and k alone moves outputs by ~3%.
+@pytest.mark.parametrize("idx,b_std", [(1, 0.01), (1, 0.3), (2, 0.01), (2, 0.1), (3, 0.01),
+                                       (3, 0.1), (4, 0.01), (4, 0.1), (5, 0.01), (5, 0.1)])
+def test_layer_parity(idx, b_std):
+    ranks = None
+    if b_std > 0.01:  # strong adapters, mixed ranks incl. zero
+        w = wl.WORKLOADS[idx]
+        ranks = np.array([(8 * (t % 3)) for t in range(w.n_tasks)], np.int32)
+        ranks[ranks == 0] = 0
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, b_std=b_std, ranks=ranks)
+    log(f"layer workload {idx} b_std={b_std} T={pb.T}")
+    fwd.embed()
+    x_in = fwd.x.double().cpu().numpy()
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    W_np = oracle_weights(model.layers[0])
+    reqs = list(range(batch.n_req))
+    kvc = (kv.k[0], kv.v[0]) if kv is not None else None
+    res = oracle_layer_rows(w, W_np, model.adapters[0], pl, x_in, reqs, kv=kvc,
+                            kv_start=kv.kv_start if kv is not None else None)
+    cu = pl["cu_seqlens"]
+    worst = 0.0
+    for p in reqs:
+        e = O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0])
+        worst = max(worst, e)
+    log(f"  max row rel err {worst:.3e}")
+    assert worst < tol(w)
+    if kv is not None:  # the new K / V rows landed in their slots
+        for p in reqs:
+            i = int(pl["order"][p])
+            slot = int(kv.kv_start[i] + batch.ctx[i])
+            kg = kv.k[0][slot].double().cpu().numpy()[None]
+            vg = kv.v[0][slot].double().cpu().numpy()[None]
+            assert O.row_rel_error(kg, res[p][1]) < tol(w)
+            assert O.row_rel_error(vg, res[p][2]) < tol(w)
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 5])
+def test_head_parity(idx):
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(idx)
+    log(f"head workload {idx}")
+    fwd.embed()
+    torch.cuda.synchronize()
+    fwd.x.normal_()
+    fwd.head()
+    torch.cuda.synchronize()
+    got = fwd.out.cpu().numpy()
+    x_plan = fwd.x.double().cpu().numpy()
+    ref = oracle_heads(w, model, pl, x_plan, model.heads.n_out)
+    off = pl["logit_off"]
+    worst = max(O.row_rel_error(got[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
+    log(f"  max rel err {worst:.3e}")
+    assert worst < tol(w)
+
+
+def test_final_hidden_unpermuted():
+    """Decoder prefill returns the final-normed rows in original order."""
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(4)
+    fwd.embed()
+    torch.cuda.synchronize()
+    fwd.head()
+    torch.cuda.synchronize()
+    got = fwd.out.double().cpu().numpy()
+    x_plan = fwd.x.double().cpu().numpy()
+    cu, cu_o = pl["cu_seqlens"], pl["cu_orig"]
+    fw = np64(model.final["w"])
+    for p, i in enumerate(pl["order"]):
+        ref = O.rms_norm(x_plan[cu[p]:cu[p + 1]], fw, w.norm_eps)
+        assert O.row_rel_error(got[cu_o[i]:cu_o[i + 1]], ref) < tol(w)
+
+
+@pytest.mark.parametrize("dtype,idx", [("f32", 1), ("bf16", 2), ("bf16", 5)])
+def test_lora_apply(dtype, idx):
+    """vfm_lora_apply alone: y += s_t (x A_t^T) B_t^T per task segment,
+    ranks 0 / 8 / 16 / 64 mixed."""
+    w = wl.WORKLOADS[idx]
+    n_tasks = 6
+    w = w.replace(n_tasks=n_tasks)
+    ranks = np.array([0, 8, 16, 64, 8, 0], np.int32)
+    ad = wl.adapters_layer(w, 0, device="cuda", ranks=ranks, b_std=0.1, targets=("q", "down"))
+    tab = R.lora_table(w, ad)
+    r = np.random.default_rng(3)
+    task_id = r.integers(0, n_tasks, size=23)
+    seq_len = r.integers(1, 90, size=23)
+    pb = B.Batch(task_id, seq_len, n_tasks)
+    pl = O.plan(task_id, seq_len, n_tasks)
+    for proj in ("q", "down"):
+        d_in, d_out = wl.proj_dims(w, proj)
+        x = torch.randn(pb.T, d_in, device="cuda").to(w.torch_dtype)
+        y0 = torch.randn(pb.T, d_out, device="cuda")
+        y = y0.clone()
+        ws = torch.empty(pb.T * 64 * 4 + 4096, dtype=torch.uint8, device="cuda")
+        B.vfm_lora_apply(B.VFM_BF16 if dtype == "bf16" else B.VFM_F32, wl.PROJ_INDEX[proj], d_in,
+                         d_out, tab.c, pb.c, x, y, ws)
+        torch.cuda.synchronize()
+        delta = (y - y0).double().cpu().numpy()
+        xn = np64(x)
+        worst = 0.0
+        for t in range(n_tasks):
+            r0, r1 = int(pl["seg_row"][t]), int(pl["seg_row"][t + 1])
+            if r1 == r0:
+                continue
+            if ranks[t] == 0:
+                assert np.array_equal(y[r0:r1].cpu().numpy(), y0[r0:r1].cpu().numpy())
+                continue
+            ref = O.lora_delta(xn[r0:r1], np64(ad.a(proj, t)), np64(ad.b(proj, t)), float(ad.scale[t]))
+            worst = max(worst, O.row_rel_error(delta[r0:r1], ref))
+        log(f"lora_apply {dtype} {proj} max rel err {worst:.3e}")
+        assert worst < (2e-2 if dtype == "bf16" else 1e-5)
+
+
+@pytest.mark.parametrize("idx", [2, 4])
+def test_batch_invariance_and_zero_rank_bit_exact(idx):
+    """A task's rows are bit-identical whether co-batched with other tasks or
+    run alone, and a rank-0 task equals the bare backbone bit for bit."""
+    w = wl.WORKLOADS[idx]
+    ranks = np.full(w.n_tasks, w.rank, np.int32)
+    ranks[0] = 0
+    case = SMALL[idx]
+    w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, ranks=ranks, b_std=0.1)
+    fwd.embed()
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    mixed = fwd.x.cpu().numpy()
+    src = inp.src
+    for t in sorted(set(case["task_id"])):
+        keep = [i for i, tt in enumerate(case["task_id"]) if tt == t]
+        sub = _batch(w, [case["task_id"][i] for i in keep], [case["seq_len"][i] for i in keep])
+        pbs = R.make_batch(w, sub, model.heads)
+        inps = R.Inputs(w, sub)
+        # the same input rows as in the mixed batch
+        cu_o = pl["cu_orig"]
+        if inp.mode == B.VFM_EMBED_ROWS:
+            inps.src = torch.cat([src[cu_o[i]:cu_o[i + 1]] for i in keep])
+        else:
+            inps.src = torch.cat([src[cu_o[i]:cu_o[i + 1]] for i in keep])
+            inps.table = inp.table
+        f2 = R.Forward(model, pbs, inps)
+        f2.embed()
+        f2.layer(0)
+        torch.cuda.synchronize()
+        alone = f2.x.cpu().numpy()
+        seg = slice(int(pl["seg_row"][t]), int(pl["seg_row"][t + 1]))
+        assert np.array_equal(mixed[seg], alone), f"task {t}"
+        if t == 0:  # rank 0: equals the backbone with no adapters at all
+            bare = R.Model(w, n_layers=1, with_lora=False)
+            f3 = R.Forward(bare, pbs, inps)
+            f3.embed()
+            f3.layer(0)
+            torch.cuda.synchronize()
+            assert np.array_equal(f3.x.cpu().numpy(), alone)
+
+
+def test_merged_weights_match_adapter_path():
+    """Running the bare path on W + s B A (merged in fp32, rounded once) agrees
+    with the unmerged per-task path for a batch of one task."""
+    w = wl.WORKLOADS[2]
+    case = dict(task_id=[5, 5], seq_len=[197, 197])
+    w_, batch, model, inp, kv, pb, fwd, pl = _setup(2, n_layers=1, b_std=0.1, case=case)
+    fwd.embed()
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    bare = R.Model(w, n_layers=1, with_lora=False)
+    W = bare.layers[0]
+    ad = model.adapters[0]
+    d = w.d
+    t = 5
+    with torch.no_grad():
+        for p, (lo, hi) in (("q", (0, d)), ("k", (d, 2 * d)), ("v", (2 * d, 3 * d))):
+            m = W["w_qkv"][lo:hi].float() + float(ad.scale[t]) * (ad.b(p, t).float() @ ad.a(p, t).float())
+            W["w_qkv"][lo:hi] = m.to(W["w_qkv"].dtype)
+        W["w_o"].copy_((W["w_o"].float() + float(ad.scale[t]) * (ad.b("o", t).float() @ ad.a("o", t).float())).to(W["w_o"].dtype))
+    bare.c_layers[0] = B.layer_weights(W)
+    f2 = R.Forward(bare, pb, inp)
+    f2.embed()
+    f2.layer(0)
+    torch.cuda.synchronize()
+    assert O.row_rel_error(f2.x.double().cpu().numpy(), got) < tol(w)
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3])
+def test_end_to_end_small(idx):
+    """All layers + head from the initial input against the oracle chain."""
+    w = wl.WORKLOADS[idx]
+    n_layers = w.n_layers if idx != 3 else 6
+    w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=n_layers)
+    log(f"end-to-end workload {idx} layers={n_layers}")
+    out = fwd().cpu().numpy()
+    torch.cuda.synchronize()
+    x = expected_embed(w, batch, inp, pl)
+    cu = pl["cu_seqlens"]
+    for li in range(n_layers):
+        W_np = oracle_weights(model.layers[li])
+        res = oracle_layer_rows(w, W_np, model.adapters[li], pl, x, range(batch.n_req))
+        x = np.concatenate([res[p][0] for p in range(batch.n_req)])
+    ref = oracle_heads(w, model, pl, x, model.heads.n_out)
+    off = pl["logit_off"]
+    worst = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
+    log(f"  end-to-end logits max rel err {worst:.3e}")
+    assert worst < tol(w)
+
+
+def test_bench_workload_full_size_sampled():
+    """The benchmarked workload (ViT-B-shaped, 64 requests x 197 tokens,
+    16 tasks, 12 layers) in the bench's launch configuration: every layer's
+    output on sampled requests against the oracle run on that layer's GPU
+    input, and every request's head outputs."""
+    w = wl.WORKLOADS[2]
+    batch = wl.draw_batch(w)
+    model = R.Model(w)
+    inp = R.Inputs(w, batch)
+    pb = R.make_batch(w, batch, model.heads)
+    fwd = R.Forward(model, pb, inp)
+    pl = oracle_plan(w, batch, model.heads.n_out)
+    reqs = pick_requests(pl)
+    log(f"full-size bench workload, sampled plan positions {reqs}")
+    fwd.embed()
+    torch.cuda.synchronize()
+    cu = pl["cu_seqlens"]
+    worst = 0.0
+    for li in range(w.n_layers):
+        x_in = fwd.x.double().cpu().numpy()
+        fwd.layer(li)
+        torch.cuda.synchronize()
+        got = fwd.x.double().cpu().numpy()
+        res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_in, reqs)
+        for p in reqs:
+            worst = max(worst, O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]))
+    log(f"  per-layer max row rel err {worst:.3e}")
+    assert worst < tol(w)
+    fwd.head()
+    torch.cuda.synchronize()
+    out = fwd.out.cpu().numpy()
+    ref = oracle_heads(w, model, pl, fwd.x.double().cpu().numpy(), model.heads.n_out)
+    off = pl["logit_off"]
+    hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
+    log(f"  head max rel err {hw:.3e}")
+    assert hw < tol(w)
