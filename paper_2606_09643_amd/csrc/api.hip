@@ -65,7 +65,7 @@ LayerWs layer_ws(const vfm_cfg& c, const Plan& pl, const vfm_lora_table* l) {
   w.h = off;    off += align_up(T * c.d_model * es);
   w.big = off;  off += align_up(T * std::max<size_t>(3 * (size_t)c.d_model, c.d_ff) * es);
   w.attn = off; off += align_up(T * c.d_model * es);
-  w.u = off;    off += align_up(T * VFM_NPROJ * rpad_of(l) * es);
+  w.u = off;    off += align_up(T * 8 * rpad_of(l) * es);
   w.total = off;
   return w;
 }
@@ -185,7 +185,7 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
   void* attn = base + ws.attn;
   void* U = base + ws.u;
   const int rpad = rpad_of(lora);
-  const int ldu = VFM_NPROJ * rpad;
+  const int ldu = 8 * rpad;  // 7 projections + one spare slot
   const bool use_lora = lora && rpad > 0;
 
   auto has = [&](int p) { return use_lora && lora->A[p] != nullptr; };

@@ -194,6 +194,132 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Prefill attention for requests of at most 256 tokens (bf16, MFMA).
+// One block per (request, head): K and V^T of the whole request are staged in
+// LDS once (V^T through 8x8 register transposes), then each wave takes
+// 16-query groups; with all keys resident the softmax is one pass (max,
+// exp, sum) with no rescaling.  Keys are padded to a multiple of 32 with
+// zeros and masked.
+// ---------------------------------------------------------------------------
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
+                                                              int d, bf16* __restrict__ out,
+                                                              float scale_log2) {
+  constexpr int LMAX = 256;
+  constexpr int KP = DH + 8;      // K row stride (bf16)
+  constexpr int VP = LMAX + 8;    // V^T row stride (bf16)
+  __shared__ __attribute__((aligned(16))) bf16 Ks[LMAX * KP];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
+  const int p = blockIdx.x, h = blockIdx.y;
+  const int R = pl.cu_seqlens[p];
+  const int L = pl.cu_seqlens[p + 1] - R;
+  const int Lp = (L + 31) & ~31;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
+  const int64_t ld = 3 * (int64_t)d;
+  const bf16* base = qkv + (int64_t)R * ld + h * DH;
+  constexpr int CH = DH / 8;
+  for (int c = tid; c < Lp * CH; c += 256) {
+    const int key = c / CH, ch = c % CH;
+    bf16x8 v = {};
+    if (key < L) v = *reinterpret_cast<const bf16x8*>(base + (int64_t)key * ld + d + ch * 8);
+    *reinterpret_cast<bf16x8*>(&Ks[key * KP + ch * 8]) = v;
+  }
+  for (int tile = tid; tile < (Lp / 8) * CH; tile += 256) {
+    const int kb = (tile / CH) * 8, db = (tile % CH) * 8;
+    bf16x8 v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[e] = bf16x8{};
+      if (kb + e < L) v[e] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + e) * ld + 2 * d + db);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      bf16x8 col;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) col[e] = v[e][j];
+      *reinterpret_cast<bf16x8*>(&Vt[(db + j) * VP + kb]) = col;
+    }
+  }
+  __syncthreads();
+
+  const int nks = Lp / 16;  // 16-key sub-tiles (even)
+  for (int qg = wave; qg * 16 < L; qg += 4) {
+    const int qi = qg * 16 + (lane & 15);
+    bf16x8 qf[DH / 32];
+    {
+      const bf16* qrow = base + (int64_t)min(qi, L - 1) * ld + 8 * g;
+#pragma unroll
+      for (int s2 = 0; s2 < DH / 32; ++s2) qf[s2] = *reinterpret_cast<const bf16x8*>(qrow + s2 * 32);
+    }
+    f32x4 st[LMAX / 16];
+    float mx = NEG_BIG;
+#pragma unroll
+    for (int ks = 0; ks < LMAX / 16; ++ks) {
+      if (ks < nks) {
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s2 = 0; s2 < DH / 32; ++s2) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(ks * 16 + (lane & 15)) * KP + s2 * 32 + 8 * g]);
+          a = mfma16(kf, qf[s2], a);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = ks * 16 + 4 * g + i;
+          const bool masked = key >= L || (CAUSAL && key > qi);
+          a[i] = masked ? -INFINITY : a[i] * scale_log2;
+          mx = fmaxf(mx, a[i]);
+        }
+        st[ks] = a;
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float lsum = 0.f;
+    f32x4 o[DH / 16];
+#pragma unroll
+    for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < LMAX / 32; ++u) {
+      if (2 * u < nks) {
+        bf16x8 pf;
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float e = exp2f(st[2 * u + half][i] - mx);
+            lsum += e;
+            pf[half * 4 + i] = (bf16)e;
+          }
+#pragma unroll
+        for (int ds = 0; ds < DH / 16; ++ds) {
+          const bf16* vrow = &Vt[(ds * 16 + (lane & 15)) * VP + 32 * u + 4 * g];
+          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
+          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
+          bf16x8 vf;
+          vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
+          vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
+          o[ds] = mfma16(vf, pf, o[ds]);
+        }
+      }
+    }
+    lsum += __shfl_xor(lsum, 16, 64);
+    lsum += __shfl_xor(lsum, 32, 64);
+    if (qi < L) {
+      const float inv = 1.f / lsum;
+      bf16* orow = out + (int64_t)(R + qi) * d + h * DH + 4 * g;
+#pragma unroll
+      for (int ds = 0; ds < DH / 16; ++ds) {
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = (bf16)(o[ds][i] * inv);
+        *reinterpret_cast<bf16x4*>(orow + ds * 16) = v;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Prefill attention, generic SIMT (fp32 workloads): 64 queries per block,
 // 4 threads per query, each owning DH/4 dims; keys staged in LDS.
@@ -368,7 +494,15 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   }
   dim3 grid(pl.n_qblocks, H);
   const bool causal = c.attn == VFM_ATTN_CAUSAL;
-  if (dtype == VFM_BF16) {
+  if (dtype == VFM_BF16 && pl.max_seqlen <= 256) {
+    dim3 g2(pl.n_req, H);
+#define SHORT(D_, C_)                                                                            \
+  hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_>), g2, dim3(256), 0, s, pl, (const bf16*)qkv, d, \
+                     (bf16*)out, scale_log2)
+    if (DH == 64) { if (causal) SHORT(64, true); else SHORT(64, false); }
+    else { if (causal) SHORT(128, true); else SHORT(128, false); }
+#undef SHORT
+  } else if (dtype == VFM_BF16) {
 #define PRE(D_, C_)                                                                            \
   hipLaunchKernelGGL((attn_prefill_bf16_kernel<D_, C_>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
                      d, (bf16*)out, scale_log2)

@@ -34,12 +34,395 @@ __device__ __forceinline__ int swz(int row, int kc) { return kc ^ ((row & 7) ^ (
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.f + erff(v * 0.70710678118654752440f));
 }
+// GELU for bf16 outputs: erf from Abramowitz & Stegun, Handbook of
+// Mathematical Functions, formula 7.1.26 (|error| <= 1.5e-7, far below the
+// 2^-9 rounding of the bf16 result), about a third of the instructions of a
+// full-precision erff.
+__device__ __forceinline__ float gelu_erf_fast(float v) {
+  const float x = fabsf(v) * 0.70710678118654752440f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  const float e = poly * __expf(-x * x);          // 1 - erf(|v|/sqrt 2)
+  const float erf_abs = 1.f - e;
+  const float erf_v = v < 0.f ? -erf_abs : erf_abs;
+  return 0.5f * v * (1.f + erf_v);
+}
 __device__ __forceinline__ float silu_f(float v) { return v / (1.f + expf(-v)); }
 
 __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+typedef const void __attribute__((address_space(1)))* gptr_t;
+typedef void __attribute__((address_space(3)))* lptr_t;
+
+// Fused per-task LoRA expand for one wave's FM x FN fragment grid (shared by
+// both bf16 kernels).  wrow0 / wcol0: the wave's first row / first B-tile row.
+template <int FM, int FN, bool SWIGLU>
+__device__ __forceinline__ void lora_expand_frags(const GemmArgs& a, int m0, int BMrows, int wrow0,
+                                                  int n0, int wcol0, int lane,
+                                                  f32x4 (&acc)[FM][FN]) {
+  const GemmLora& L = a.lora;
+  const bf16* U = (const bf16*)L.U;
+  const int mlast = min(m0 + BMrows, a.M) - 1;
+  const int t0 = L.row_task[m0], t1 = L.row_task[mlast];
+  for (int t = t0; t <= t1; ++t) {
+    const int r = min(L.rank[t], L.max_rank) & ~7;
+    if (r <= 0) continue;
+    const int s0 = L.seg_row[t], s1 = L.seg_row[t + 1];
+    if (s1 <= wrow0 || s0 >= wrow0 + FM * 16) continue;
+    for (int kk = 0; kk < r; kk += 32) {
+      const int kof = kk + 8 * (lane >> 4);
+      const bool kin = kof < r;
+      bf16x8 xf[FM];
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi) xf[mi] = bf16x8{};
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        int slot, nrow, nlim;
+        if (SWIGLU) {
+          const int sub = wcol0 / 16 + ni;
+          slot = sub & 1;
+          const int jb = n0 + (sub >> 1) * 16;
+          if (jb >= a.N) continue;
+          nrow = jb + (lane & 15);
+          nlim = a.N;
+        } else {
+          const int nb = n0 + wcol0 + ni * 16;
+          if (nb >= a.N) continue;
+          slot = nb / L.slot_width;
+          nrow = nb - slot * L.slot_width + (lane & 15);
+          nlim = L.slot_width;
+        }
+        if (L.B[slot] == nullptr) continue;
+        const bf16* Bt = (const bf16*)L.B[slot][t];
+        bf16x8 wf = {};
+        if (kin && nrow < nlim) wf = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)nrow * r + kof);
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi) {
+          const int m = wrow0 + mi * 16 + (lane & 15);
+          bf16x8 x = {};
+          if (m >= s0 && m < s1 && m < a.M)
+            x = *reinterpret_cast<const bf16x8*>(U + (int64_t)m * L.ldu + L.ucol[slot] + kof);
+          acc[mi][ni] = mfma16(wf, x, acc[mi][ni]);
+        }
+      }
+    }
+  }
+}
+
+// Epilogue for one wave's FM x FN fragment grid; lane holds 4 consecutive
+// output columns of one row per fragment.  Bias is read once per column
+// group and the residual loads of a row group are issued together, so the
+// global-memory latency is paid FM times, not FM x FN times.
+template <int EPI, bool SWIGLU, int FM, int FN>
+__device__ __forceinline__ void epilogue_frags(const GemmArgs& a, int wrow0, int n0, int wcol0,
+                                               int lane, const f32x4 (&acc)[FM][FN]) {
+  if (SWIGLU) {
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi) {
+      const int m = wrow0 + mi * 16 + (lane & 15);
+      if (m >= a.M) continue;
+#pragma unroll
+      for (int ni = 0; ni < FN; ni += 2) {
+        const int sub = wcol0 / 16 + ni;
+        const int j = n0 + (sub >> 1) * 16 + 4 * (lane >> 4);
+        if (j >= a.N) continue;
+        bf16x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = (bf16)(silu_f(acc[mi][ni][r]) * acc[mi][ni + 1][r]);
+        *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + j) = o;
+      }
+    }
+    return;
+  }
+  const bf16* bias = (const bf16*)a.bias;
+  f32x4 bv[FN];
+#pragma unroll
+  for (int ni = 0; ni < FN; ++ni) {
+    bv[ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int n = n0 + wcol0 + ni * 16 + 4 * (lane >> 4);
+    if (bias && n < a.N) {
+      const bf16x4 bb = *reinterpret_cast<const bf16x4*>(bias + n);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bv[ni][r] = (float)bb[r];
+    }
+  }
+#pragma unroll
+  for (int mi = 0; mi < FM; ++mi) {
+    const int m = wrow0 + mi * 16 + (lane & 15);
+    if (m >= a.M) continue;
+    if (EPI == EPI_RESID) {
+      float* row = (float*)a.out + (int64_t)m * a.ldo;
+      float4 old[FN];
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int n = n0 + wcol0 + ni * 16 + 4 * (lane >> 4);
+        old[ni] = n < a.N ? *reinterpret_cast<const float4*>(row + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int n = n0 + wcol0 + ni * 16 + 4 * (lane >> 4);
+        if (n >= a.N) continue;
+        float4 o = old[ni];
+        o.x += acc[mi][ni][0] + bv[ni][0];
+        o.y += acc[mi][ni][1] + bv[ni][1];
+        o.z += acc[mi][ni][2] + bv[ni][2];
+        o.w += acc[mi][ni][3] + bv[ni][3];
+        *reinterpret_cast<float4*>(row + n) = o;
+      }
+    } else {
+      bf16* row = (bf16*)a.out + (int64_t)m * a.ldo;
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int n = n0 + wcol0 + ni * 16 + 4 * (lane >> 4);
+        if (n >= a.N) continue;
+        bf16x4 o;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float v = acc[mi][ni][r] + bv[ni][r];
+          o[r] = (bf16)(EPI == EPI_GELU ? gelu_erf_fast(v) : v);
+        }
+        *reinterpret_cast<bf16x4*>(row + n) = o;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Large-M bf16 GEMM: 256x256x64 block tile, 8 waves (4 along M x 2 along N)
+// of 64x128, operands streamed global -> LDS with global_load_lds_dwordx4
+// (no staging registers), two LDS stages (128 KB), and an XCD-aware tile
+// order: consecutive block ids land on different XCDs (each with its own
+// L2), so block b takes logical tile (b % 8) * per + b / 8 and logical tiles
+// run in groups of LGM row-tiles sweeping all column tiles, keeping each
+// XCD's X rows and W columns resident in its L2.
+//
+// The per-task LoRA expand runs as extra 64-wide K steps of the same
+// pipeline: for every task t with rows in the tile, the A tile holds the
+// shrink outputs U[m, slot cols] of t's rows (rows of other tasks come from a
+// zero page) and the B tile holds B_t[n, :r_t] (zero past the rank).  For a
+// SwiGLU block the A tile is [U_gate | U_up] and gate rows of B carry B_gate
+// in the low 32 columns, up rows carry B_up in the high 32.  The MFMA loop
+// cannot tell these steps from the backbone's.
+// ---------------------------------------------------------------------------
+constexpr int LBM = 256, LBN = 256, LGM = 4;
+
+__device__ __attribute__((aligned(16))) bf16 g_zero_page[8];  // zero-initialised at load
+
+template <int EPI, bool SWIGLU>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
+  constexpr int NW = 8, NTH = 512, WN = 2, TM = 64, TN = 128, FM = 4, FN = 8;
+  constexpr int ACH = LBM * 8 / NTH, BCH = LBN * 8 / NTH;  // 4, 4 chunks of 16 B
+  constexpr int SA = LBM * BK, SB = LBN * BK;
+  constexpr int RSTEP = NTH / 8;                             // 64 rows per chunk step
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (SA + SB)];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  constexpr int NTILE = SWIGLU ? LBN / 2 : LBN;  // output columns per block
+  const int MT = (a.M + LBM - 1) / LBM, NTn = (a.N + NTILE - 1) / NTILE, ntiles = MT * NTn;
+  const int per = gridDim.x / 8;
+  const int Lid = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (Lid >= ntiles) return;
+  int tm, tn;
+  {
+    const int gsz = LGM * NTn;
+    const int g = Lid / gsz, r = Lid % gsz;
+    const int fm = g * LGM;
+    const int gm = min(MT - fm, LGM);
+    tm = fm + r % gm;
+    tn = r / gm;
+  }
+  const int m0 = tm * LBM, n0 = tn * NTILE;
+  const bf16* X = (const bf16*)a.X;
+  const GemmLora& L = a.lora;
+
+  // Each wave fills whole 1 KB LDS slots (8 rows x 128 B); lane `lane` of
+  // chunk i writes LDS row (i*NW + wave)*8 + lane/8, physical 16-byte chunk
+  // lane%8, so it loads the logical chunk that the swizzle maps there.
+  const int row0 = wave * 8 + (lane >> 3);
+  const int kc0 = (lane & 7) ^ ((row0 & 7) ^ ((row0 >> 3) & 1));
+  const bf16* xsrc[ACH];
+#pragma unroll
+  for (int i = 0; i < ACH; ++i)
+    xsrc[i] = X + (int64_t)min(m0 + row0 + i * RSTEP, a.M - 1) * a.ldx + kc0 * 8;
+  const bf16* wsrc[BCH];
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) {
+    const int row = row0 + i * RSTEP;
+    int wrow;
+    const bf16* wb = (const bf16*)a.W;
+    if (SWIGLU) {
+      const int sub = row >> 4;
+      wb = (sub & 1) ? (const bf16*)a.W2 : (const bf16*)a.W;
+      wrow = n0 + (sub >> 1) * 16 + (row & 15);
+    } else {
+      wrow = n0 + row;
+    }
+    wsrc[i] = wb + (int64_t)min(wrow, a.N - 1) * a.K + kc0 * 8;
+  }
+
+  // The LoRA steps of this tile: every task t0..t1 with rows in
+  // [m0, m0 + LBM) (rows are sorted by task), `parts` steps each.  A task of
+  // rank 0 gets an all-zero B tile.  (Kept out of LDS on purpose: a second
+  // LDS object makes the compiler wait for the in-flight DMA before every
+  // fragment read.)
+  const int nk = a.K / BK;
+  int t0 = 0, nlora = 0;
+  const int parts = (SWIGLU && L.max_rank > 32) ? 2 : 1;
+  if (L.enabled) {
+    bool live;
+    if (SWIGLU) live = L.B[0] != nullptr || L.B[1] != nullptr;
+    else live = L.B[min(n0 / L.slot_width, 2)] != nullptr;
+    if (live) {
+      t0 = L.row_task[m0];
+      nlora = (L.row_task[min(m0 + LBM, a.M) - 1] - t0 + 1) * parts;
+    }
+  }
+  const int nsteps = nk + nlora;
+  // metadata of the first two tasks, loaded up front so the LoRA steps of a
+  // tile with one or two tasks issue their DMA without dependent loads
+  int c_r0 = 0, c_r1 = 0, c_a0 = 0, c_a1 = 0, c_e0 = 0, c_e1 = 0;
+  const bf16 *c_b00 = nullptr, *c_b01 = nullptr, *c_b10 = nullptr, *c_b11 = nullptr;
+  if (nlora > 0) {
+    const int slot = SWIGLU ? 0 : min(n0 / L.slot_width, 2);
+    c_r0 = min(L.rank[t0], L.max_rank) & ~7;
+    c_a0 = L.seg_row[t0];
+    c_e0 = L.seg_row[t0 + 1];
+    c_b00 = L.B[slot] ? (const bf16*)L.B[slot][t0] : nullptr;
+    if (SWIGLU) c_b01 = L.B[1] ? (const bf16*)L.B[1][t0] : nullptr;
+    if (nlora > parts) {
+      c_r1 = min(L.rank[t0 + 1], L.max_rank) & ~7;
+      c_a1 = c_e0;
+      c_e1 = L.seg_row[t0 + 2];
+      c_b10 = L.B[slot] ? (const bf16*)L.B[slot][t0 + 1] : nullptr;
+      if (SWIGLU) c_b11 = L.B[1] ? (const bf16*)L.B[1][t0 + 1] : nullptr;
+    }
+  }
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int mi = 0; mi < FM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto issue = [&](int e) {
+    bf16* As = smem + (e & 1) * (SA + SB);
+    bf16* Bs = As + SA;
+    if (e < nk) {
+      const int k0 = e * BK;
+#pragma unroll
+      for (int i = 0; i < ACH; ++i)
+        __builtin_amdgcn_global_load_lds((gptr_t)(xsrc[i] + k0), (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+#pragma unroll
+      for (int i = 0; i < BCH; ++i)
+        __builtin_amdgcn_global_load_lds((gptr_t)(wsrc[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16, 0, 0);
+      return;
+    }
+    const int t = t0 + (e - nk) / parts, part = (e - nk) % parts;
+    const int ci = t - t0;
+    const bool cached = ci < 2;
+    const int r = ci == 0 ? c_r0 : (ci == 1 ? c_r1 : (min(L.rank[t], L.max_rank) & ~7));
+    const int s0 = ci == 0 ? c_a0 : (ci == 1 ? c_a1 : L.seg_row[t]);
+    const int s1 = ci == 0 ? c_e0 : (ci == 1 ? c_e1 : L.seg_row[t + 1]);
+    const bf16* U = (const bf16*)L.U;
+    const bf16* zero = g_zero_page;
+    // A: the task's rows of U; 64 columns starting at the step's slot.  Only
+    // columns of slots the shrink wrote are read (the rest come from the zero
+    // page), so stale workspace bytes never meet a zero of B.
+    const int rpad = L.max_rank > 32 ? 64 : 32;
+    int ucolA;
+    bool colA;
+    if (SWIGLU && rpad == 32) {
+      ucolA = L.ucol[0];
+      colA = (kc0 < 4) ? (L.B[0] != nullptr) : (L.B[1] != nullptr);
+    } else if (SWIGLU) {
+      ucolA = L.ucol[part];
+      colA = L.B[part] != nullptr;
+    } else {
+      ucolA = L.ucol[min(n0 / L.slot_width, 2)];
+      colA = kc0 * 8 < rpad;
+    }
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) {
+      const int m = m0 + row0 + i * RSTEP;
+      const bf16* src = (colA && m >= s0 && m < s1 && m < a.M) ? U + (int64_t)m * L.ldu + ucolA + kc0 * 8 : zero;
+      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+    }
+    // B: B_t rows of this block's output columns, zero past the rank
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      const int row = row0 + i * RSTEP;
+      const bf16* src = zero;
+      if (SWIGLU) {
+        const int sub = row >> 4, which = sub & 1;
+        const int j = n0 + (sub >> 1) * 16 + (row & 15);
+        int kc = kc0;
+        bool on;
+        if (L.max_rank > 32) on = (which == part) && L.B[part] != nullptr;
+        else { on = which ? (kc0 >= 4) : (kc0 < 4); kc = which ? kc0 - 4 : kc0; }
+        if (on && kc * 8 < r && j < a.N && L.B[which] != nullptr) {
+          const bf16* Bt = cached ? (ci == 0 ? (which ? c_b01 : c_b00) : (which ? c_b11 : c_b10))
+                                  : (const bf16*)L.B[which][t];
+          src = Bt + (int64_t)j * r + kc * 8;
+        }
+      } else {
+        const int n = n0 + row;
+        const int slot = min(n / L.slot_width, 2);
+        const int nrow = n - slot * L.slot_width;
+        if (kc0 * 8 < r && n < a.N && nrow < L.slot_width && L.B[slot] != nullptr) {
+          const bf16* Bt = cached ? (ci == 0 ? c_b00 : c_b10) : (const bf16*)L.B[slot][t];
+          src = Bt + (int64_t)nrow * r + kc0 * 8;
+        }
+      }
+      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(Bs + (i * NW + wave) * 512), 16, 0, 0);
+    }
+  };
+  auto compute = [&](int e) {
+    const bf16* As = smem + (e & 1) * (SA + SB);
+    const bf16* Bs = As + SA;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int kc = kk * 4 + (lane >> 4);
+      bf16x8 wf[FN];
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int r = wn * TN + ni * 16 + (lane & 15);
+        wf[ni] = *reinterpret_cast<const bf16x8*>(Bs + r * BK + swz(r, kc) * 8);
+      }
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi) {
+        const int r = wm * TM + mi * 16 + (lane & 15);
+        const bf16x8 xf = *reinterpret_cast<const bf16x8*>(As + r * BK + swz(r, kc) * 8);
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = mfma16(wf[ni], xf, acc[mi][ni]);
+      }
+    }
+  };
+
+  // Waits are explicit: vmcnt(0) makes this wave's LDS-bound loads land, the
+  // raw s_barrier then makes every wave's loads visible.  (A full
+  // __syncthreads would add a fence the loop does not need.)
+  issue(0);
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  for (int e = 0; e < nsteps; ++e) {
+    if (e + 1 < nsteps) issue(e + 1);  // the other stage: every wave left it at the last barrier
+    compute(e);
+    __builtin_amdgcn_s_waitcnt(0xF70);
+    __builtin_amdgcn_s_barrier();
+  }
+  epilogue_frags<EPI, SWIGLU, FM, FN>(a, m0 + wm * TM, n0, wn * TN, lane, acc);
+}
+
+// ---------------------------------------------------------------------------
+// Small-M bf16 GEMM (decode-sized batches): 128x128x64, 4 waves of 64x64,
+// register-staged LDS double buffer, more blocks for few rows.
+// ---------------------------------------------------------------------------
 template <int EPI, bool SWIGLU>
 __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
@@ -134,96 +517,10 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs a) {
     __syncthreads();
   }
 
-  // ---- fused per-task LoRA expand ---------------------------------------
-  if (a.lora.enabled) {
-    const GemmLora& L = a.lora;
-    const bf16* U = (const bf16*)L.U;
-    const int wm0 = m0 + wm * 64;
-    const int mlast = min(m0 + BM, a.M) - 1;
-    const int t0 = L.row_task[m0], t1 = L.row_task[mlast];
-    for (int t = t0; t <= t1; ++t) {
-      const int r = min(L.rank[t], L.max_rank) & ~7;
-      if (r <= 0) continue;
-      const int s0 = L.seg_row[t], s1 = L.seg_row[t + 1];
-      if (s1 <= wm0 || s0 >= wm0 + 64) continue;
-      for (int kk = 0; kk < r; kk += 32) {
-        const int kof = kk + 8 * (lane >> 4);
-        const bool kin = kof < r;
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          int slot, nrow, nlim;
-          if (SWIGLU) {
-            const int s = wn * 4 + ni;
-            slot = s & 1;
-            nrow = n0 + (s >> 1) * 16 + (lane & 15);
-            nlim = a.N;
-            if (n0 + (s >> 1) * 16 >= a.N) continue;
-          } else {
-            const int nb = n0 + wn * 64 + ni * 16;
-            if (nb >= a.N) continue;
-            slot = nb / L.slot_width;
-            nrow = nb - slot * L.slot_width + (lane & 15);
-            nlim = L.slot_width;
-          }
-          if (L.B[slot] == nullptr) continue;
-          const bf16* Bt = (const bf16*)L.B[slot][t];
-          bf16x8 wf = {};
-          if (kin && nrow < nlim) wf = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)nrow * r + kof);
-#pragma unroll
-          for (int mi = 0; mi < 4; ++mi) {
-            const int m = wm0 + mi * 16 + (lane & 15);
-            bf16x8 xf = {};
-            if (m >= s0 && m < s1 && m < a.M)
-              xf = *reinterpret_cast<const bf16x8*>(U + (int64_t)m * L.ldu + L.ucol[slot] + kof);
-            acc[mi][ni] = mfma16(wf, xf, acc[mi][ni]);
-          }
-        }
-      }
-    }
-  }
-
-  // ---- epilogue -----------------------------------------------------------
-  const bf16* bias = (const bf16*)a.bias;
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
-    const int m = m0 + wm * 64 + mi * 16 + (lane & 15);
-    if (m >= a.M) continue;
-    if (SWIGLU) {
-#pragma unroll
-      for (int ni = 0; ni < 4; ni += 2) {
-        const int s = wn * 4 + ni;
-        const int j = n0 + (s >> 1) * 16 + 4 * (lane >> 4);
-        if (j >= a.N) continue;
-        bf16x4 o;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) o[r] = (bf16)(silu_f(acc[mi][ni][r]) * acc[mi][ni + 1][r]);
-        *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + j) = o;
-      }
-    } else {
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int n = n0 + wn * 64 + ni * 16 + 4 * (lane >> 4);
-        if (n >= a.N) continue;
-        f32x4 v = acc[mi][ni];
-        if (bias) {
-          const bf16x4 bb = *reinterpret_cast<const bf16x4*>(bias + n);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] += (float)bb[r];
-        }
-        if (EPI == EPI_RESID) {
-          float4* dst = reinterpret_cast<float4*>((float*)a.out + (int64_t)m * a.ldo + n);
-          float4 o = *dst;
-          o.x += v[0]; o.y += v[1]; o.z += v[2]; o.w += v[3];
-          *dst = o;
-        } else {
-          bf16x4 o;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) o[r] = (bf16)(EPI == EPI_GELU ? gelu_erf(v[r]) : v[r]);
-          *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + n) = o;
-        }
-      }
-    }
-  }
+  const int wrow0 = m0 + wm * 64;
+  if (a.lora.enabled)
+    lora_expand_frags<4, 4, SWIGLU>(a, m0, BM, wrow0, n0, wn * 64, lane, acc);
+  epilogue_frags<EPI, SWIGLU, 4, 4>(a, wrow0, n0, wn * 64, lane, acc);
 }
 
 // ---------------------------------------------------------------------------
@@ -342,7 +639,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 
 template <int EPI, bool SW>
 hipError_t launch_one(int dtype, const GemmArgs& a, hipStream_t s) {
-  if (dtype == VFM_BF16) {
+  const bool one_slot = !a.lora.enabled || SW || a.lora.slot_width % LBN == 0;
+  if (dtype == VFM_BF16 && a.M >= 1024 && one_slot) {
+    const int nt = SW ? LBN / 2 : LBN;
+    const int ntiles = ((a.M + LBM - 1) / LBM) * ((a.N + nt - 1) / nt);
+    const int grid = (ntiles + 7) / 8 * 8;
+    hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW>), dim3(grid), dim3(512), 0, s, a);
+  } else if (dtype == VFM_BF16) {
     const int nt = SW ? BN / 2 : BN;
     const int grid = ((a.M + BM - 1) / BM) * ((a.N + nt - 1) / nt);
     hipLaunchKernelGGL((gemm_bf16_kernel<EPI, SW>), dim3(grid), dim3(256), 0, s, a);

@@ -129,25 +129,18 @@ __global__ __launch_bounds__(256) void norm_pool_kernel(Plan pl, const float* __
   int first = r0, last = r1;
   if (pool == VFM_POOL_FIRST) last = r0 + 1;
   if (pool == VFM_POOL_LAST) first = r1 - 1;
-  float4 s[MAXI];
-#pragma unroll
-  for (int i = 0; i < MAXI; ++i) s[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int r = first + wave; r < last; r += 4) {
     float4 v[MAXI];
     norm_row_regs<T, MAXI>(x + (int64_t)r * d, d, g, b, kind, eps, v);
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
-      s[i].x += v[i].x; s[i].y += v[i].y; s[i].z += v[i].z; s[i].w += v[i].w;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < MAXI; ++i) {
-    const int c = lane + 64 * i;
-    if (c < (d >> 2)) {
-      atomicAdd(&acc[4 * c + 0], s[i].x);
-      atomicAdd(&acc[4 * c + 1], s[i].y);
-      atomicAdd(&acc[4 * c + 2], s[i].z);
-      atomicAdd(&acc[4 * c + 3], s[i].w);
+      const int c = lane + 64 * i;
+      if (c < (d >> 2)) {
+        atomicAdd(&acc[4 * c + 0], v[i].x);
+        atomicAdd(&acc[4 * c + 1], v[i].y);
+        atomicAdd(&acc[4 * c + 2], v[i].z);
+        atomicAdd(&acc[4 * c + 3], v[i].w);
+      }
     }
   }
   __syncthreads();

@@ -32,46 +32,59 @@ __device__ inline void tile_rows(const Plan& pl, int bid, int& t, int& r0, int& 
 // ---------------------------------------------------------------------------
 // shrink: U[m, ucol + j] = s_t * X[m, :] . A_t[j, :]   (j < rpad, zero past r_t)
 // ---------------------------------------------------------------------------
+template <int NP, int NSUB>
 __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
+  // One block per 64-row tile of one task; each wave owns 16 rows and every
+  // projection of the group, so the rows are read once for all of them.
   int t, r0, r1;
   tile_rows(pl, blockIdx.x, t, r0, r1);
-  const int p = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rank = min(a.rank[t], a.rpad) & ~7;
   const float sc = a.scale[t];
   const bf16* X = (const bf16*)a.X;
-  const bf16* At = rank > 0 ? (const bf16*)a.A[p][t] : nullptr;
   bf16* U = (bf16*)a.U;
-  const int mrow = r0 + wave * 16 + (lane & 15);
-  const int nsub = a.rpad >> 4;
-  f32x4 acc[4];
+  const int m = r0 + wave * 16 + (lane & 15);
+  f32x4 acc[NP][NSUB];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) acc[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+    for (int s2 = 0; s2 < NSUB; ++s2) acc[pp][s2] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (rank > 0 && r0 + wave * 16 < r1) {
-    const bf16* xrow = X + (int64_t)min(mrow, r1 - 1) * a.ldx + 8 * (lane >> 4);
-#pragma unroll 4
+    const bf16* xrow = X + (int64_t)min(m, r1 - 1) * a.ldx + 8 * (lane >> 4);
+    const bf16* arow[NP][NSUB];
+    bool aon[NSUB];
+#pragma unroll
+    for (int s2 = 0; s2 < NSUB; ++s2) aon[s2] = s2 * 16 + (lane & 15) < rank;
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp) {
+      const bf16* At = (const bf16*)a.A[pp][t];
+#pragma unroll
+      for (int s2 = 0; s2 < NSUB; ++s2)
+        arow[pp][s2] = At + (int64_t)min(s2 * 16 + (lane & 15), rank - 1) * a.K + 8 * (lane >> 4);
+    }
+#pragma unroll 2
     for (int k = 0; k < a.K; k += 32) {
       const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        if (s >= nsub) break;
-        const int j = s * 16 + (lane & 15);
-        bf16x8 af = {};
-        if (j < rank) af = *reinterpret_cast<const bf16x8*>(At + (int64_t)j * a.K + k + 8 * (lane >> 4));
-        acc[s] = mfma16(af, xf, acc[s]);
-      }
+      for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+        for (int s2 = 0; s2 < NSUB; ++s2) {
+          bf16x8 af = *reinterpret_cast<const bf16x8*>(arow[pp][s2] + k);
+          if (!aon[s2]) af = bf16x8{};
+          acc[pp][s2] = mfma16(af, xf, acc[pp][s2]);
+        }
     }
   }
-  const int m = r0 + wave * 16 + (lane & 15);
   if (m < r1) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s >= nsub) break;
-      bf16x4 o;
+    for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[s][i] * sc);
-      *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[p] + s * 16 + 4 * (lane >> 4)) = o;
-    }
+      for (int s2 = 0; s2 < NSUB; ++s2) {
+        bf16x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[pp][s2][i] * sc);
+        *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[pp] + s2 * 16 + 4 * (lane >> 4)) = o;
+      }
   }
 }
 
@@ -220,9 +233,19 @@ __global__ __launch_bounds__(256) void heads_f32_kernel(Plan pl, const float* __
 
 hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s) {
   if (pl.n_rtiles == 0 || a.n_proj == 0) return hipSuccess;
-  dim3 grid(pl.n_rtiles, a.n_proj);
-  if (dtype == VFM_BF16) hipLaunchKernelGGL(shrink_bf16_kernel, grid, dim3(256), 0, s, pl, a);
-  else hipLaunchKernelGGL(shrink_f32_kernel, grid, dim3(256), 0, s, pl, a);
+  if (dtype == VFM_BF16) {
+    dim3 grid(pl.n_rtiles);
+#define SHR(NP_, NS_) hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
+    if (a.rpad == 32) {
+      if (a.n_proj == 1) SHR(1, 2); else if (a.n_proj == 2) SHR(2, 2); else SHR(3, 2);
+    } else {
+      if (a.n_proj == 1) SHR(1, 4); else if (a.n_proj == 2) SHR(2, 4); else SHR(3, 4);
+    }
+#undef SHR
+  } else {
+    dim3 grid(pl.n_rtiles, a.n_proj);
+    hipLaunchKernelGGL(shrink_f32_kernel, grid, dim3(256), 0, s, pl, a);
+  }
   return hipGetLastError();
 }
 

@@ -306,3 +306,22 @@ def test_bench_workload_full_size_sampled():
     hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
     log(f"  head max rel err {hw:.3e}")
     assert hw < tol(w)
+
+
+def test_layer_parity_long_prompts():
+    """Causal prompts longer than 256 tokens take the flash (online-softmax)
+    attention kernel: ragged 300 / 1 / 513-token prompts, 0.1 adapters."""
+    case = dict(task_id=[3, 0, 63], seq_len=[300, 1, 513])
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(4, n_layers=1, b_std=0.1, case=case)
+    log(f"layer workload 4 long prompts T={pb.T}")
+    fwd.embed()
+    x_in = fwd.x.double().cpu().numpy()
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    res = oracle_layer_rows(w, oracle_weights(model.layers[0]), model.adapters[0], pl, x_in,
+                            range(batch.n_req))
+    cu = pl["cu_seqlens"]
+    worst = max(O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]) for p in range(batch.n_req))
+    log(f"  max row rel err {worst:.3e}")
+    assert worst < tol(w)
