@@ -81,8 +81,15 @@ def algorithmic_work(w, batch, ranks, heads_n_out):
 # --------------------------------------------------------------------------
 # CPU baseline: the fp64 oracle on a bounded sample of the same batch
 # --------------------------------------------------------------------------
-def cpu_baseline(w, batch, model, inp, budget_s=15.0):
-    import torch
+def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
+    """The fp64 oracle on whole requests of the same batch, layer by layer.
+
+    Requests are taken in original order until the oracle time estimated
+    from their first layer reaches about `budget_s`; then every layer and the
+    final norm / head run for those requests.  Each layer's bf16 weights
+    (and, when decoding, the requests' KV slices) are converted to fp64
+    outside the timed region.
+    """
     from oracle import vfm_oracle as O
     from tests.gpu_common import expected_embed, oracle_plan
     from tests.helpers import np64, oracle_adapter, oracle_weights, spec_of
@@ -93,31 +100,57 @@ def cpu_baseline(w, batch, model, inp, budget_s=15.0):
         cores = os.cpu_count()
     pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
     x_all = expected_embed(w, batch, inp, pl)
-    Ws = [oracle_weights(model.layers[i]) for i in range(w.n_layers)]   # bf16 -> fp64 outside timing
     spec = spec_of(w)
     cu = pl["cu_seqlens"]
     inv = np.argsort(pl["order"])
-    done_tokens, done_req = 0, 0
-    t0 = time.perf_counter()
-    for i in range(batch.n_req):                 # original request order, whole requests only
+    xs = {}
+
+    def kv_of(li, i):
+        if kv is None:
+            return None
+        c, s0 = int(batch.ctx[i]), int(kv.kv_start[i])
+        return (np64(kv.k[li][s0:s0 + c]), np64(kv.v[li][s0:s0 + c]))
+
+    def run_layer(Wn, li, i, kvp):
         p = int(inv[i])
         t = int(pl["task"][p])
-        x = x_all[int(cu[p]):int(cu[p + 1])]
-        pos = pl["pos"][int(cu[p]):int(cu[p + 1])]
-        for li in range(w.n_layers):
-            x = O.layer(spec, Ws[li], oracle_adapter(model.adapters[li], t), x, pos=pos)[0]
-        if model.heads is not None:
-            xn = O.final(spec, np64(model.final["w"]), np64(model.final["b"]), x)
-            O.head(O.pool(xn, w.pool), np64(model.heads.W[t]), np64(model.heads.b[t]))
-        done_tokens += x.shape[0]
-        done_req += 1
-        if time.perf_counter() - t0 > budget_s:
+        sl = slice(int(cu[p]), int(cu[p + 1]))
+        return O.layer(spec, Wn, oracle_adapter(model.adapters[li], t), xs[i], pos=pl["pos"][sl],
+                       kv=kvp)[0]
+
+    W0 = oracle_weights(model.layers[0])
+    sample, est = [], 0.0
+    for i in range(batch.n_req):
+        p = int(inv[i])
+        xs[i] = x_all[int(cu[p]):int(cu[p + 1])]
+        kvp = kv_of(0, i)
+        t0 = time.perf_counter()
+        run_layer(W0, 0, i, kvp)
+        est += (time.perf_counter() - t0) * w.n_layers
+        sample.append(i)
+        if est > budget_s:
             break
-    dt = time.perf_counter() - t0
-    return {"value": done_tokens / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {done_req} of {batch.n_req} requests (original order), "
-                      f"{done_tokens} tokens, all {w.n_layers} layers + head, fp64 numpy, "
-                      f"{dt:.1f} s"}
+    elapsed = 0.0
+    for li in range(w.n_layers):
+        Wn = W0 if li == 0 else oracle_weights(model.layers[li])
+        kvs = {i: kv_of(li, i) for i in sample}
+        t0 = time.perf_counter()
+        for i in sample:
+            xs[i] = run_layer(Wn, li, i, kvs[i])
+        elapsed += time.perf_counter() - t0
+    fw, fb = np64(model.final["w"]), np64(model.final["b"])
+    t0 = time.perf_counter()
+    for i in sample:
+        t = int(pl["task"][int(inv[i])])
+        xn = O.final(spec, fw, fb, xs[i])
+        if model.heads is not None:
+            O.head(O.pool(xn, w.pool), np64(model.heads.W[t]), np64(model.heads.b[t]))
+    elapsed += time.perf_counter() - t0
+    tokens = int(sum(xs[i].shape[0] for i in sample))
+    return {"value": tokens / elapsed, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {len(sample)} of {batch.n_req} requests (original order), "
+                      f"{tokens} tokens, all {w.n_layers} layers + final norm/head, fp64 numpy, "
+                      f"{elapsed:.1f} s"}
 
 
 def main():
@@ -149,6 +182,14 @@ def main():
     ranks = wl.task_ranks(w)
     work = algorithmic_work(w, batch, ranks, model.heads.n_out if model.heads is not None else None)
     stream = torch.cuda.current_stream()
+
+    # Calibration for HBM-traffic counters: one plain device copy of a known
+    # size (256 MiB read + 256 MiB written), outside the timed region.
+    cal_src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+    cal_dst = torch.empty_like(cal_src)
+    cal_dst.copy_(cal_src)
+    torch.cuda.synchronize()
+    del cal_src, cal_dst
 
     for _ in range(args.warmup):
         fwd(stream)
@@ -204,7 +245,7 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, batch, model, inp)
+        out["cpu_baseline"] = cpu_baseline(w, batch, model, inp, kv)
     print(json.dumps(out), flush=True)
 
 

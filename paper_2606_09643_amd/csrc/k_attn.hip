@@ -27,6 +27,23 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
 }
 
 constexpr float LOG2E = 1.4426950408889634f;
+
+// 2^x for the softmax, where x <= 0 after the max subtraction: the hardware
+// v_exp_f32 directly (no range reduction needed; -inf gives 0).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// eight floats -> one bf16x8 MFMA operand with four packed conversions
+__device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
+  const bf16x2 p0 = __builtin_convertvector(f32x2{a[0], a[1]}, bf16x2);
+  const bf16x2 p1 = __builtin_convertvector(f32x2{a[2], a[3]}, bf16x2);
+  const bf16x2 p2 = __builtin_convertvector(f32x2{b[0], b[1]}, bf16x2);
+  const bf16x2 p3 = __builtin_convertvector(f32x2{b[2], b[3]}, bf16x2);
+  const bf16x4 lo = __builtin_shufflevector(p0, p1, 0, 1, 2, 3);
+  const bf16x4 hi = __builtin_shufflevector(p2, p3, 0, 1, 2, 3);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
 constexpr float NEG_BIG = -1e30f;
 
 // ---------------------------------------------------------------------------
@@ -72,6 +89,14 @@ __global__ __launch_bounds__(256) void kv_write_kernel(Plan pl, const T* __restr
   }
 }
 
+// K is stored unpadded with an XOR chunk swizzle (16-byte chunk kc of key r
+// at kc ^ ((r >> 1) & 7) for 128-byte rows, kc ^ (r & 15) for 256-byte rows),
+// which makes the 16-row fragment reads bank-conflict free on gfx950.
+template <int DH>
+__device__ __forceinline__ int kswz(int r, int kc) {
+  return DH == 64 ? (kc ^ ((r >> 1) & 7)) : (kc ^ (r & 15));
+}
+
 // ---------------------------------------------------------------------------
 // Prefill attention, bf16, MFMA.
 // ---------------------------------------------------------------------------
@@ -79,9 +104,8 @@ template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                                 int d, bf16* __restrict__ out,
                                                                 float scale_log2) {
-  constexpr int KP = DH + 8;   // padded LDS row of K (bf16)
   constexpr int VP = 64 + 8;   // padded LDS row of V^T
-  __shared__ __attribute__((aligned(16))) bf16 Ks[64 * KP];
+  __shared__ __attribute__((aligned(16))) bf16 Ks[64 * DH];   // swizzled rows (kswz)
   __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
   const int b = blockIdx.x, h = blockIdx.y;
   const int p = upper_index(pl.qblk_off, pl.n_req + 1, b);
@@ -106,19 +130,28 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
 
   const int kend = CAUSAL ? min(L, q0 + 64) : L;
   for (int kb = 0; kb < kend; kb += 64) {
-    // stage K (row-major) and V^T into LDS; rows past the request are zero
-    constexpr int CH = DH / 8;  // 16-byte chunks per key row
-    for (int c = tid; c < 64 * CH; c += 256) {
-      const int key = c / CH, ch = c % CH;
-      bf16x8 kv = {}, vv = {};
+    // stage K (swizzled rows) and V^T into LDS; rows past the request are
+    // zero.  All of a thread's loads are issued before its first store.
+    constexpr int CH = DH / 8;            // 16-byte chunks per key row
+    constexpr int PT = 64 * CH / 256;     // chunks per thread (2 or 4)
+    bf16x8 kv[PT], vv[PT];
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      kv[i] = bf16x8{};
+      vv[i] = bf16x8{};
       if (kb + key < L) {
         const bf16* src = qkv + (int64_t)(R + kb + key) * ld + h * DH + ch * 8;
-        kv = *reinterpret_cast<const bf16x8*>(src + d);
-        vv = *reinterpret_cast<const bf16x8*>(src + 2 * d);
+        kv[i] = *reinterpret_cast<const bf16x8*>(src + d);
+        vv[i] = *reinterpret_cast<const bf16x8*>(src + 2 * d);
       }
-      *reinterpret_cast<bf16x8*>(&Ks[key * KP + ch * 8]) = kv;
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(ch * 8 + e) * VP + key] = vv[e];
+    for (int i = 0; i < PT; ++i) {
+      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      *reinterpret_cast<bf16x8*>(&Ks[key * DH + kswz<DH>(key, ch) * 8]) = kv[i];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(ch * 8 + e) * VP + key] = vv[i][e];
     }
     __syncthreads();
 
@@ -128,7 +161,8 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
       st[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < DH / 32; ++s) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(ks * 16 + (lane & 15)) * KP + s * 32 + 8 * g]);
+        const int r = ks * 16 + (lane & 15);
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[r * DH + kswz<DH>(r, s * 4 + g) * 8]);
         st[ks] = mfma16(kf, qf[s], st[ks]);
       }
     }
@@ -148,7 +182,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
     mb = fmaxf(mb, __shfl_xor(mb, 16, 64));
     mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
     const float m_new = fmaxf(m_run, mb);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = fast_exp2(m_run - m_new);
     m_run = m_new;
     float lsum = 0.f;
     bf16x8 pf[2];
@@ -156,7 +190,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float e = exp2f(st[ks][i] - m_new);
+        const float e = fast_exp2(st[ks][i] - m_new);
         lsum += e;
         pf[ks >> 1][(ks & 1) * 4 + i] = (bf16)e;
       }
@@ -171,10 +205,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
         const bf16* vrow = &Vt[(ds * 16 + (lane & 15)) * VP + 32 * u + 4 * g];
         const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
         const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-        bf16x8 vf;
-        vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
-        vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
-        o[ds] = mfma16(vf, pf[u], o[ds]);
+        o[ds] = mfma16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pf[u], o[ds]);
       }
     }
     __syncthreads();
@@ -203,76 +234,107 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
 // exp, sum) with no rescaling.  Keys are padded to a multiple of 32 with
 // zeros and masked.
 // ---------------------------------------------------------------------------
-template <int DH, bool CAUSAL>
+template <int DH, bool CAUSAL, int NKS>
 __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                               int d, bf16* __restrict__ out,
                                                               float scale_log2) {
-  constexpr int LMAX = 256;
-  constexpr int KP = DH + 8;      // K row stride (bf16)
+  // NKS 16-key sub-tiles cover every request of the batch (NKS * 16 >= L)
+  constexpr int LMAX = NKS * 16;
+  constexpr int CH = DH / 8;      // 16-byte chunks per key row
   constexpr int VP = LMAX + 8;    // V^T row stride (bf16)
-  __shared__ __attribute__((aligned(16))) bf16 Ks[LMAX * KP];
+  __shared__ __attribute__((aligned(16))) bf16 Ks[LMAX * DH];
   __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
   const int p = blockIdx.x, h = blockIdx.y;
   const int R = pl.cu_seqlens[p];
   const int L = pl.cu_seqlens[p + 1] - R;
-  const int Lp = (L + 31) & ~31;
+  constexpr int Lp = LMAX;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
   const int64_t ld = 3 * (int64_t)d;
   const bf16* base = qkv + (int64_t)R * ld + h * DH;
-  constexpr int CH = DH / 8;
-  for (int c = tid; c < Lp * CH; c += 256) {
-    const int key = c / CH, ch = c % CH;
-    bf16x8 v = {};
-    if (key < L) v = *reinterpret_cast<const bf16x8*>(base + (int64_t)key * ld + d + ch * 8);
-    *reinterpret_cast<bf16x8*>(&Ks[key * KP + ch * 8]) = v;
-  }
-  for (int tile = tid; tile < (Lp / 8) * CH; tile += 256) {
-    const int kb = (tile / CH) * 8, db = (tile % CH) * 8;
-    bf16x8 v[8];
+
+  // Stage K and V^T.  Every global load of a thread is issued before its
+  // first LDS store, so the block pays the load latency once.
+  {
+    constexpr int KPT = (LMAX * CH + 255) / 256;  // K chunks per thread
+    bf16x8 kr[KPT];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      v[e] = bf16x8{};
-      if (kb + e < L) v[e] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + e) * ld + 2 * d + db);
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      kr[i] = bf16x8{};
+      if (key < L && c < LMAX * CH) kr[i] = *reinterpret_cast<const bf16x8*>(base + (int64_t)key * ld + d + ch * 8);
+    }
+    constexpr int VPT = ((LMAX / 8) * CH + 255) / 256;  // 8x8 V tiles per thread
+    bf16x8 vr[VPT][8];
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int tile = tid + 256 * i, kb = (tile / CH) * 8, db = (tile % CH) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        vr[i][e] = bf16x8{};
+        if (kb + e < L && tile < (LMAX / 8) * CH)
+          vr[i][e] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + e) * ld + 2 * d + db);
+      }
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      bf16x8 col;
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      if (c < LMAX * CH) *reinterpret_cast<bf16x8*>(&Ks[key * DH + kswz<DH>(key, ch) * 8]) = kr[i];
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) col[e] = v[e][j];
-      *reinterpret_cast<bf16x8*>(&Vt[(db + j) * VP + kb]) = col;
+    for (int i = 0; i < VPT; ++i) {
+      const int tile = tid + 256 * i, kb = (tile / CH) * 8, db = (tile % CH) * 8;
+      if (tile < (LMAX / 8) * CH) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          bf16x8 col;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) col[e] = vr[i][e][j];
+          *reinterpret_cast<bf16x8*>(&Vt[(db + j) * VP + kb]) = col;
+        }
+      }
     }
   }
   __syncthreads();
 
-  const int nks = Lp / 16;  // 16-key sub-tiles (even)
+  auto load_q = [&](int qg, bf16x8 (&qf)[DH / 32]) {
+    const int qi = qg * 16 + (lane & 15);
+    const bf16* qrow = base + (int64_t)min(qi, L - 1) * ld + 8 * g;
+#pragma unroll
+    for (int s2 = 0; s2 < DH / 32; ++s2) qf[s2] = *reinterpret_cast<const bf16x8*>(qrow + s2 * 32);
+  };
+  bf16x8 qnext[DH / 32];
+  if (wave * 16 < L) load_q(wave, qnext);
   for (int qg = wave; qg * 16 < L; qg += 4) {
     const int qi = qg * 16 + (lane & 15);
     bf16x8 qf[DH / 32];
-    {
-      const bf16* qrow = base + (int64_t)min(qi, L - 1) * ld + 8 * g;
 #pragma unroll
-      for (int s2 = 0; s2 < DH / 32; ++s2) qf[s2] = *reinterpret_cast<const bf16x8*>(qrow + s2 * 32);
-    }
-    f32x4 st[LMAX / 16];
+    for (int s2 = 0; s2 < DH / 32; ++s2) qf[s2] = qnext[s2];
+    if ((qg + 4) * 16 < L) load_q(qg + 4, qnext);   // in flight during this group
+    f32x4 st[NKS];
     float mx = NEG_BIG;
+    // The key swizzle of row 16*ks + (lane & 15) does not depend on ks, so
+    // every fragment address is a per-lane base plus a constant offset.
+    const bf16* kbase = &Ks[(lane & 15) * DH];
+    // keep the fragment reads inside this loop: hoisting all of them out
+    // (they do not depend on the query group) needs ~2x the registers
+    asm volatile("" : "+v"(kbase));
 #pragma unroll
-    for (int ks = 0; ks < LMAX / 16; ++ks) {
-      if (ks < nks) {
-        f32x4 a = {0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < NKS; ++ks) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s2 = 0; s2 < DH / 32; ++s2) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(ks * 16 + (lane & 15)) * KP + s2 * 32 + 8 * g]);
-          a = mfma16(kf, qf[s2], a);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = ks * 16 + 4 * g + i;
-          const bool masked = key >= L || (CAUSAL && key > qi);
-          a[i] = masked ? -INFINITY : a[i] * scale_log2;
-          mx = fmaxf(mx, a[i]);
-        }
-        st[ks] = a;
+      for (int s2 = 0; s2 < DH / 32; ++s2) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+            kbase + ks * 16 * DH + kswz<DH>(lane & 15, s2 * 4 + g) * 8);
+        a = mfma16(kf, qf[s2], a);
       }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = ks * 16 + 4 * g + i;
+        const bool masked = key >= L || (CAUSAL && key > qi);
+        a[i] = masked ? -INFINITY : a[i] * scale_log2;
+        mx = fmaxf(mx, a[i]);
+      }
+      st[ks] = a;
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -280,28 +342,24 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     f32x4 o[DH / 16];
 #pragma unroll
     for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const bf16* vbase = &Vt[(lane & 15) * VP + 4 * g];
+    asm volatile("" : "+v"(vbase));
 #pragma unroll
-    for (int u = 0; u < LMAX / 32; ++u) {
-      if (2 * u < nks) {
-        bf16x8 pf;
+    for (int u = 0; u < NKS / 2; ++u) {
+      f32x4 e0, e1;
 #pragma unroll
-        for (int half = 0; half < 2; ++half)
+      for (int i = 0; i < 4; ++i) {
+        e0[i] = fast_exp2(st[2 * u][i] - mx);
+        e1[i] = fast_exp2(st[2 * u + 1][i] - mx);
+        lsum += e0[i] + e1[i];
+      }
+      const bf16x8 pf = pack8(e0, e1);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float e = exp2f(st[2 * u + half][i] - mx);
-            lsum += e;
-            pf[half * 4 + i] = (bf16)e;
-          }
-#pragma unroll
-        for (int ds = 0; ds < DH / 16; ++ds) {
-          const bf16* vrow = &Vt[(ds * 16 + (lane & 15)) * VP + 32 * u + 4 * g];
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-          bf16x8 vf;
-          vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
-          vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
-          o[ds] = mfma16(vf, pf, o[ds]);
-        }
+      for (int ds = 0; ds < DH / 16; ++ds) {
+        const bf16* vrow = vbase + ds * 16 * VP + 32 * u;
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
+        o[ds] = mfma16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pf, o[ds]);
       }
     }
     lsum += __shfl_xor(lsum, 16, 64);
@@ -496,11 +554,20 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   const bool causal = c.attn == VFM_ATTN_CAUSAL;
   if (dtype == VFM_BF16 && pl.max_seqlen <= 256) {
     dim3 g2(pl.n_req, H);
-#define SHORT(D_, C_)                                                                            \
-  hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_>), g2, dim3(256), 0, s, pl, (const bf16*)qkv, d, \
-                     (bf16*)out, scale_log2)
-    if (DH == 64) { if (causal) SHORT(64, true); else SHORT(64, false); }
-    else { if (causal) SHORT(128, true); else SHORT(128, false); }
+    const int nks = ((pl.max_seqlen + 31) / 32) * 2;   // 16-key sub-tiles, even
+#define SHORT(D_, C_, N_)                                                                           \
+  hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_, N_>), g2, dim3(256), 0, s, pl, (const bf16*)qkv, \
+                     d, (bf16*)out, scale_log2)
+#define SHORT_N(D_, C_)                                            \
+  switch (nks) {                                                   \
+    case 2: SHORT(D_, C_, 2); break;   case 4: SHORT(D_, C_, 4); break;   \
+    case 6: SHORT(D_, C_, 6); break;   case 8: SHORT(D_, C_, 8); break;   \
+    case 10: SHORT(D_, C_, 10); break; case 12: SHORT(D_, C_, 12); break; \
+    case 14: SHORT(D_, C_, 14); break; default: SHORT(D_, C_, 16); break; \
+  }
+    if (DH == 64) { if (causal) { SHORT_N(64, true); } else { SHORT_N(64, false); } }
+    else { if (causal) { SHORT_N(128, true); } else { SHORT_N(128, false); } }
+#undef SHORT_N
 #undef SHORT
   } else if (dtype == VFM_BF16) {
 #define PRE(D_, C_)                                                                            \

@@ -29,7 +29,13 @@ namespace {
 
 constexpr int BM = 128, BN = 128, BK = 64;
 
-__device__ __forceinline__ int swz(int row, int kc) { return kc ^ ((row & 7) ^ ((row >> 3) & 1)); }
+// LDS chunk swizzle of a [rows][64 bf16] tile (128-byte rows, eight 16-byte
+// chunks): logical chunk kc of row r lives at physical chunk kc ^ ((r >> 1) & 7).
+// Measured on gfx950 with the LDS bank-conflict counter: zero conflicts for
+// the ds_read_b128 fragment reads of both the 16x16 and the 32x32 MFMA
+// operand layouts (rows r..r+15 at one logical chunk).
+__device__ __forceinline__ int swz_bits(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int swz(int row, int kc) { return kc ^ swz_bits(row); }
 
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.f + erff(v * 0.70710678118654752440f));
@@ -245,7 +251,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // chunk i writes LDS row (i*NW + wave)*8 + lane/8, physical 16-byte chunk
   // lane%8, so it loads the logical chunk that the swizzle maps there.
   const int row0 = wave * 8 + (lane >> 3);
-  const int kc0 = (lane & 7) ^ ((row0 & 7) ^ ((row0 >> 3) & 1));
+  const int kc0 = (lane & 7) ^ swz_bits(row0);  // same for row0 + i * RSTEP
   const bf16* xsrc[ACH];
 #pragma unroll
   for (int i = 0; i < ACH; ++i)
