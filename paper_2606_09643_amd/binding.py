@@ -28,6 +28,7 @@ VFM_EMBED_ROWS, VFM_EMBED_TOKENS, VFM_EMBED_PATCHES = 0, 1, 2
 VFM_NPROJ = 7
 VFM_PLAN_HEADER = 16
 VFM_ROW_TILE = 64
+VFM_SMALL_BATCH_ROWS = 1024
 PROJ = ("q", "k", "v", "o", "gate", "up", "down")
 
 EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size",

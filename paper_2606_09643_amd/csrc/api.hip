@@ -1,6 +1,7 @@
 // C ABI entry points: argument validation, workspace carving and the launch
 // sequence of one backbone layer over a mixed-task batch.
 #include <algorithm>
+#include <initializer_list>
 
 #include "vfm_internal.h"
 
@@ -53,19 +54,53 @@ inline int rpad_of(const vfm_lora_table* l) {
   return l->max_rank <= 32 ? 32 : 64;
 }
 
+// Small bf16 batches take the split-K GEMM + separate shrink + finalize path.
+inline bool use_skinny(const vfm_cfg& c, const Plan& pl) {
+  return c.dtype == VFM_BF16 && pl.T < VFM_SMALL_BATCH_ROWS;
+}
+
+// Largest number of keys one request attends to (ctx + its rows), from the
+// host copy of the plan.
+int max_keys_of(const vfm_batch* b, const Plan& pl) {
+  const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
+  const int32_t* ctx = b->plan_host + po.ctx;
+  const int32_t* cu = b->plan_host + po.cu_seqlens;
+  int mk = 0;
+  for (int p = 0; p < pl.n_req; ++p) mk = std::max(mk, ctx[p] + cu[p + 1] - cu[p]);
+  return mk;
+}
+
 struct LayerWs {
-  size_t h, big, attn, u, total;
+  size_t h, big, attn, u, z, p, aws, total;
+  int kchunks;
 };
 
-LayerWs layer_ws(const vfm_cfg& c, const Plan& pl, const vfm_lora_table* l) {
+LayerWs layer_ws(const vfm_cfg& c, const Plan& pl, const vfm_lora_table* l, int max_keys) {
   const size_t es = elem_size(c.dtype);
   const size_t T = (size_t)pl.T;
+  const int d = c.d_model, f = c.d_ff, rpad = rpad_of(l);
   LayerWs w;
   size_t off = 0;
-  w.h = off;    off += align_up(T * c.d_model * es);
-  w.big = off;  off += align_up(T * std::max<size_t>(3 * (size_t)c.d_model, c.d_ff) * es);
-  w.attn = off; off += align_up(T * c.d_model * es);
-  w.u = off;    off += align_up(T * 8 * rpad_of(l) * es);
+  w.h = off;    off += align_up(T * d * es);
+  w.big = off;  off += align_up(T * std::max<size_t>(3 * (size_t)d, f) * es);
+  w.attn = off; off += align_up(T * d * es);
+  w.u = off;    off += align_up(T * 8 * rpad * es);
+  w.aws = off; off += align_up(attention_workspace(c, pl, max_keys));
+  w.z = w.p = off;
+  w.kchunks = 0;
+  if (use_skinny(c, pl)) {
+    // fp32 split partials of the largest projection group
+    // (the LoRA expand adds one more slice)
+    auto zbytes = [&](int N, int K) { return (size_t)(skinny_splits(N, K) + 1) * T * N * 4; };
+    const int n_up = c.mlp == VFM_MLP_SWIGLU ? 2 * f : f;
+    const size_t zmax = std::max(std::max(zbytes(3 * d, d), zbytes(d, d)),
+                                 std::max(zbytes(n_up, d), zbytes(d, f)));
+    w.z = off; off += align_up(zmax);
+    if (rpad > 0) {
+      w.kchunks = std::max(shrink_chunks(d), shrink_chunks(f));
+      w.p = off; off += align_up((size_t)w.kchunks * T * 8 * rpad * 4);
+    }
+  }
   w.total = off;
   return w;
 }
@@ -117,7 +152,7 @@ extern "C" int vfm_workspace_size(const vfm_cfg* cfg, const vfm_batch* batch,
   Plan pl;
   VFM_TRY(check_batch(batch, &pl));
   VFM_TRY(check_lora(lora, pl));
-  size_t need = layer_ws(*cfg, pl, lora).total;
+  size_t need = layer_ws(*cfg, pl, lora, max_keys_of(batch, pl)).total;
   need = std::max(need, head_ws(*cfg, pl));
   *bytes = need;
   return VFM_OK;
@@ -174,7 +209,8 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
       if (end > kv_slots) return VFM_ERR_SHAPE;
     }
   }
-  const LayerWs ws = layer_ws(c, pl, lora);
+  const int max_keys = max_keys_of(batch, pl);
+  const LayerWs ws = layer_ws(c, pl, lora, max_keys);
   if (!workspace || ws_bytes < ws.total || ((uintptr_t)workspace % ALIGN)) return VFM_ERR_WORKSPACE;
 
   hipStream_t s = (hipStream_t)stream;
@@ -184,95 +220,129 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
   void* act = base + ws.big;  // the MLP activation reuses the qkv region
   void* attn = base + ws.attn;
   void* U = base + ws.u;
+  float* Z = (float*)(base + ws.z);
+  float* P = (float*)(base + ws.p);
   const int rpad = rpad_of(lora);
   const int ldu = 8 * rpad;  // 7 projections + one spare slot
   const bool use_lora = lora && rpad > 0;
 
+  const bool skinny = use_skinny(c, pl);
+
   auto has = [&](int p) { return use_lora && lora->A[p] != nullptr; };
-  auto shrink = [&](const void* X, int K, std::initializer_list<int> projs) -> hipError_t {
-    ShrinkArgs a = {};
-    a.X = X; a.ldx = K; a.K = K; a.U = U; a.ldu = ldu; a.rpad = rpad;
-    a.rank = lora->rank; a.scale = lora->scale;
-    for (int p : projs) {
-      if (!has(p)) continue;
-      a.A[a.n_proj] = lora->A[p];
-      a.ucol[a.n_proj] = p * rpad;
-      a.n_proj++;
-    }
-    return launch_lora_shrink(c.dtype, pl, a, s);
-  };
-  auto gl = [&](std::initializer_list<int> projs, int slot_width) {
-    GemmLora L = {};
-    int i = 0;
+  // One projection group: X [T, K] times the stacked weights (W, then W2
+  // for SwiGLU), the per-task LoRA of `projs` (column slots of slot_width),
+  // and the epilogue.
+  auto project = [&](int cls, const void* X, int K, const void* W, const void* W2,
+                     const void* bias, int N, int epi, void* out, int ldo,
+                     std::initializer_list<int> projs, int slot_width) -> int {
     bool any = false;
-    for (int p : projs) {
-      if (has(p)) {
-        L.B[i] = lora->B[p];
-        any = true;
+    for (int p : projs) any = any || has(p);
+    if (!skinny) {
+      if (any) {
+        ShrinkArgs a = {};
+        a.X = X; a.ldx = K; a.K = K; a.U = U; a.ldu = ldu; a.rpad = rpad;
+        a.rank = lora->rank; a.scale = lora->scale;
+        for (int p : projs) {
+          if (!has(p)) continue;
+          a.A[a.n_proj] = lora->A[p];
+          a.ucol[a.n_proj] = p * rpad;
+          a.n_proj++;
+        }
+        VFM_TIMED(VFM_PROF_SHRINK, launch_lora_shrink(c.dtype, pl, a, s));
       }
-      L.ucol[i] = p * rpad;
-      ++i;
+      GemmArgs g = {};
+      g.X = X; g.ldx = K; g.W = W; g.W2 = W2; g.bias = bias;
+      g.M = T; g.N = N; g.K = K; g.epi = epi; g.out = out; g.ldo = ldo;
+      if (any) {
+        GemmLora& L = g.lora;
+        int i = 0;
+        for (int p : projs) {
+          if (has(p)) L.B[i] = lora->B[p];
+          L.ucol[i] = p * rpad;
+          ++i;
+        }
+        L.enabled = 1;
+        L.U = U; L.ldu = ldu; L.slot_width = slot_width;
+        L.rank = lora->rank; L.row_task = pl.row_task; L.seg_row = pl.seg_row;
+        L.max_rank = lora->max_rank;
+      }
+      VFM_TIMED(cls, launch_gemm(c.dtype, g, s));
+      return VFM_OK;
     }
-    if (!any) return L;
-    L.enabled = 1;
-    L.U = U; L.ldu = ldu; L.slot_width = slot_width;
-    L.rank = lora->rank; L.row_task = pl.row_task; L.seg_row = pl.seg_row;
-    L.max_rank = lora->max_rank;
-    return L;
+    // small batch: split-K shrink + reduce, split-K GEMM into partial
+    // slices, the LoRA expand as one more slice, then the streaming sum
+    const bool sw = epi == EPI_SWIGLU;
+    const int nz = sw ? 2 * N : N;
+    SkinnyArgs k = {};
+    k.X = X; k.ldx = K; k.W = W; k.W2 = W2; k.n_half = N;
+    k.M = T; k.N = nz; k.K = K; k.Z = Z;
+    k.nsplit = skinny_splits(nz, K);
+    FinalizeArgs fa = {};
+    fa.Z = Z; fa.nslices = k.nsplit; fa.M = T; fa.N = N; fa.epi = epi; fa.bias = bias;
+    fa.out = out; fa.ldo = ldo;
+    if (any) {
+      ShrinkSplitArgs a = {};
+      a.X = X; a.ldx = K; a.K = K; a.P = P; a.ldp = ldu; a.rpad = rpad;
+      a.kchunks = shrink_chunks(K); a.rank = lora->rank;
+      LoraReduceArgs ra = {};
+      ra.P = P; ra.ldp = ldu; ra.kchunks = a.kchunks; ra.U = (bf16*)U; ra.ldu = ldu;
+      ra.rpad = rpad; ra.scale = lora->scale;
+      for (int p : projs) {
+        if (!has(p)) continue;
+        a.A[a.n_proj] = lora->A[p];
+        a.ucol[a.n_proj] = p * rpad;
+        ra.ucol[a.n_proj] = p * rpad;
+        a.n_proj++;
+      }
+      ra.n_slots = a.n_proj;
+      VFM_TIMED(VFM_PROF_SHRINK, launch_shrink_split(pl, a, s));
+      VFM_TIMED(VFM_PROF_SHRINK, launch_lora_reduce(pl, ra, s));
+      ExpandZArgs ea = {};
+      ea.U = (const bf16*)U; ea.ldu = ldu;
+      int i = 0;
+      for (int p : projs) {
+        if (has(p)) ea.B[i] = lora->B[p];
+        ea.ucol[i] = p * rpad;
+        ++i;
+      }
+      ea.slot_width = sw ? N : slot_width;
+      ea.rank = lora->rank; ea.max_rank = lora->max_rank;
+      ea.L = Z + (size_t)k.nsplit * T * nz; ea.NZ = nz;
+      VFM_TIMED(VFM_PROF_SHRINK, launch_lora_expand_z(pl, ea, s));
+      fa.nslices = k.nsplit + 1;
+    }
+    const int pi = prof_begin(cls, s);
+    hipError_t e = launch_gemm_skinny(k, s);
+    if (e == hipSuccess) e = launch_finalize(fa, s);
+    prof_end(pi, s);
+    return hip_status(e);
   };
 
   // a2: pre-norm 1
   VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm1_w, w->norm1_b, c.norm, c.norm_eps, h, s));
   // a3 + a4: shared QKV projection with the per-task LoRA of q, k, v
-  if (has(VFM_Q) || has(VFM_K) || has(VFM_V)) VFM_TIMED(VFM_PROF_SHRINK, shrink(h, d, {VFM_Q, VFM_K, VFM_V}));
-  {
-    GemmArgs g = {};
-    g.X = h; g.ldx = d; g.W = w->w_qkv; g.bias = w->b_qkv;
-    g.M = T; g.N = 3 * d; g.K = d; g.epi = EPI_STORE; g.out = qkv; g.ldo = 3 * d;
-    g.lora = gl({VFM_Q, VFM_K, VFM_V}, d);
-    VFM_TIMED(VFM_PROF_GEMM_QKV, launch_gemm(c.dtype, g, s));
-  }
+  VFM_TRY(project(VFM_PROF_GEMM_QKV, h, d, w->w_qkv, nullptr, w->b_qkv, 3 * d, EPI_STORE, qkv,
+                  3 * d, {VFM_Q, VFM_K, VFM_V}, d));
   // a5: rotary embedding of q and k
   if (c.rope_theta > 0.f)
     VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta, s));
   // a6: attention per request (and the KV-cache write)
-  VFM_TIMED(VFM_PROF_ATTN, launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, nullptr, 0, s));
+  VFM_TIMED(VFM_PROF_ATTN, launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, base + ws.aws,
+                                            ws.z - ws.aws, max_keys, s));
   // a7: output projection + LoRA_o + residual
-  if (has(VFM_O)) VFM_TIMED(VFM_PROF_SHRINK, shrink(attn, d, {VFM_O}));
-  {
-    GemmArgs g = {};
-    g.X = attn; g.ldx = d; g.W = w->w_o; g.bias = w->b_o;
-    g.M = T; g.N = d; g.K = d; g.epi = EPI_RESID; g.out = x; g.ldo = d;
-    g.lora = gl({VFM_O}, d);
-    VFM_TIMED(VFM_PROF_GEMM_O, launch_gemm(c.dtype, g, s));
-  }
+  VFM_TRY(project(VFM_PROF_GEMM_O, attn, d, w->w_o, nullptr, w->b_o, d, EPI_RESID, x, d, {VFM_O}, d));
   // a8: pre-norm 2
   VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm2_w, w->norm2_b, c.norm, c.norm_eps, h, s));
   // a9: MLP up (+ gate) with LoRA and the activation fused
-  if (c.mlp == VFM_MLP_SWIGLU) {
-    if (has(VFM_GATE) || has(VFM_UP)) VFM_TIMED(VFM_PROF_SHRINK, shrink(h, d, {VFM_GATE, VFM_UP}));
-    GemmArgs g = {};
-    g.X = h; g.ldx = d; g.W = w->w_gate; g.W2 = w->w_up;
-    g.M = T; g.N = f; g.K = d; g.epi = EPI_SWIGLU; g.out = act; g.ldo = f;
-    g.lora = gl({VFM_GATE, VFM_UP}, f);
-    VFM_TIMED(VFM_PROF_GEMM_UP, launch_gemm(c.dtype, g, s));
-  } else {
-    if (has(VFM_UP)) VFM_TIMED(VFM_PROF_SHRINK, shrink(h, d, {VFM_UP}));
-    GemmArgs g = {};
-    g.X = h; g.ldx = d; g.W = w->w_up; g.bias = w->b_up;
-    g.M = T; g.N = f; g.K = d; g.epi = EPI_GELU; g.out = act; g.ldo = f;
-    g.lora = gl({VFM_UP}, f);
-    VFM_TIMED(VFM_PROF_GEMM_UP, launch_gemm(c.dtype, g, s));
-  }
+  if (c.mlp == VFM_MLP_SWIGLU)
+    VFM_TRY(project(VFM_PROF_GEMM_UP, h, d, w->w_gate, w->w_up, nullptr, f, EPI_SWIGLU, act, f,
+                    {VFM_GATE, VFM_UP}, f));
+  else
+    VFM_TRY(project(VFM_PROF_GEMM_UP, h, d, w->w_up, nullptr, w->b_up, f, EPI_GELU, act, f,
+                    {VFM_UP}, f));
   // a10: down projection + LoRA_down + residual
-  if (has(VFM_DOWN)) VFM_TIMED(VFM_PROF_SHRINK, shrink(act, f, {VFM_DOWN}));
-  {
-    GemmArgs g = {};
-    g.X = act; g.ldx = f; g.W = w->w_down; g.bias = w->b_down;
-    g.M = T; g.N = d; g.K = f; g.epi = EPI_RESID; g.out = x; g.ldo = d;
-    g.lora = gl({VFM_DOWN}, d);
-    VFM_TIMED(VFM_PROF_GEMM_DOWN, launch_gemm(c.dtype, g, s));
-  }
+  VFM_TRY(project(VFM_PROF_GEMM_DOWN, act, f, w->w_down, nullptr, w->b_down, d, EPI_RESID, x, d,
+                  {VFM_DOWN}, d));
   return VFM_OK;
 }
 

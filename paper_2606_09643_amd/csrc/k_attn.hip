@@ -459,40 +459,74 @@ __device__ inline void load8<float>(const float* p, float (&v)[8]) {
   v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-template <typename T, int DH>
+// The keys of a request are cut into DEC_CHUNK-key chunks, one block per
+// (request, head, chunk), so long contexts spread over many CUs instead of
+// finishing as a long tail; each block leaves its chunk's running max m,
+// sum l and unnormalised output o, and a merge kernel combines the chunks
+// (the usual rescaling of partial softmax sums by 2^(m_c - m)).
+// Inside a block, each group of LPK lanes walks one key stream; every step
+// issues the K and V loads of UNR keys of the stream before any is used.
+constexpr int DEC_CHUNK = 256;
+
+template <typename T, int DH, int UNR>
 __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __restrict__ qkv, int d,
                                                           const T* __restrict__ kc,
                                                           const T* __restrict__ vc,
-                                                          T* __restrict__ out, float scale_log2) {
+                                                          float* __restrict__ part, int nchunk,
+                                                          float scale_log2) {
   constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
   constexpr int NG = 256 / LPK;        // key streams per block
   __shared__ float sm[NG], sl[NG];
   __shared__ float so[NG][DH + 1];
-  const int p = blockIdx.x, h = blockIdx.y;
+  // heads vary fastest across consecutive blocks, so the blocks in flight
+  // read whole cache rows (all heads of a key) rather than one head's slice
+  // of many rows
+  const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
   const int tid = threadIdx.x;
   const int grp = tid / LPK, sub = tid % LPK;
   const int R = pl.cu_seqlens[p];            // the request's (single) query row
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
+  const int kbeg = c * DEC_CHUNK;
+  if (kbeg >= nkeys) return;                 // block-uniform
+  const int kend = min(kbeg + DEC_CHUNK, nkeys);
   const int64_t base = (int64_t)pl.kv_start[p];
   float q[8];
   load8<T>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8, q);
   float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
-  for (int k = grp; k < nkeys; k += NG) {
-    float kv[8], vv[8];
-    const int64_t off = (base + k) * d + h * DH + sub * 8;
-    load8<T>(kc + off, kv);
-    load8<T>(vc + off, vv);
-    float s = 0.f;
+  const T* kp = kc + base * d + h * DH + sub * 8;
+  const T* vp = vc + base * d + h * DH + sub * 8;
+  for (int k0 = kbeg + grp; k0 < kend; k0 += UNR * NG) {
+    float kv[UNR][8], vv[UNR][8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) s += q[i] * kv[i];
+    for (int u = 0; u < UNR; ++u) {
+      const int k = min(k0 + u * NG, kend - 1);   // clamped: masked below
+      load8<T>(kp + (int64_t)k * d, kv[u]);
+      load8<T>(vp + (int64_t)k * d, vv[u]);
+    }
+    float sc[UNR];
+    float smax = NEG_BIG;
 #pragma unroll
-    for (int w = LPK / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
-    s *= scale_log2;
-    const float m_new = fmaxf(m_run, s);
-    const float alpha = exp2f(m_run - m_new), e = exp2f(s - m_new);
-    l_run = l_run * alpha + e;
+    for (int u = 0; u < UNR; ++u) {
+      float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] = o[i] * alpha + e * vv[i];
+      for (int i = 0; i < 8; ++i) s += q[i] * kv[u][i];
+#pragma unroll
+      for (int w = LPK / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+      sc[u] = k0 + u * NG < kend ? s * scale_log2 : NEG_BIG;
+      smax = fmaxf(smax, sc[u]);
+    }
+    const float m_new = fmaxf(m_run, smax);
+    const float alpha = exp2f(m_run - m_new);
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] *= alpha;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const float e = k0 + u * NG < kend ? exp2f(sc[u] - m_new) : 0.f;
+      l_run += e;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] += e * vv[u][i];
+    }
     m_run = m_new;
   }
   if (sub == 0) { sm[grp] = m_run; sl[grp] = l_run; }
@@ -508,8 +542,30 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
       lsum += sl[gq] * w;
       acc += so[gq][tid] * w;
     }
-    out[(int64_t)R * d + h * DH + tid] = from_f32<T>(acc / lsum);
+    // partial record of (p, h, c): [m, l, o[0..DH)]
+    float* rec = part + (((int64_t)p * gridDim.x + h) * nchunk + c) * (DH + 2);
+    rec[2 + tid] = acc;
+    if (tid == 0) { rec[0] = M; rec[1] = lsum; }
   }
+}
+
+template <typename T, int DH>
+__global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const float* __restrict__ part,
+                                                               int nchunk, int d, T* __restrict__ out) {
+  const int p = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const int R = pl.cu_seqlens[p];
+  const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
+  const int nc = min((nkeys + DEC_CHUNK - 1) / DEC_CHUNK, nchunk);
+  const float* rec = part + ((int64_t)p * gridDim.y + h) * nchunk * (DH + 2);
+  float M = NEG_BIG;
+  for (int c = 0; c < nc; ++c) M = fmaxf(M, rec[c * (DH + 2)]);
+  float lsum = 0.f, acc = 0.f;
+  for (int c = 0; c < nc; ++c) {
+    const float w = exp2f(rec[c * (DH + 2)] - M);
+    lsum += rec[c * (DH + 2) + 1] * w;
+    acc += rec[c * (DH + 2) + 2 + tid] * w;
+  }
+  out[(int64_t)R * d + h * DH + tid] = from_f32<T>(acc / lsum);
 }
 
 }  // namespace
@@ -526,10 +582,15 @@ hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads,
   return hipGetLastError();
 }
 
-size_t attention_workspace(const vfm_cfg&, const Plan&) { return 0; }
+size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys) {
+  if (c.attn != VFM_ATTN_DECODE) return 0;
+  const int nchunk = (max_keys + DEC_CHUNK - 1) / DEC_CHUNK;
+  return (size_t)pl.n_req * c.n_heads * nchunk * (c.head_dim + 2) * sizeof(float);
+}
 
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv, void* out,
-                            void* k_cache, void* v_cache, void*, size_t, hipStream_t s) {
+                            void* k_cache, void* v_cache, void* ws, size_t ws_bytes, int max_keys,
+                            hipStream_t s) {
   const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
   if (k_cache && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
@@ -541,12 +602,20 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
                          (float*)k_cache, (float*)v_cache);
   }
   if (c.attn == VFM_ATTN_DECODE) {
-    dim3 grid(pl.n_req, H);
-#define DEC(TT, D_)                                                                          \
-  hipLaunchKernelGGL((attn_decode_kernel<TT, D_>), grid, dim3(256), 0, s, pl, (const TT*)qkv, d, \
-                     (const TT*)k_cache, (const TT*)v_cache, (TT*)out, scale_log2)
-    if (dtype == VFM_BF16) { if (DH == 64) DEC(bf16, 64); else DEC(bf16, 128); }
-    else { if (DH == 64) DEC(float, 64); else DEC(float, 128); }
+    if (ws_bytes < attention_workspace(c, pl, max_keys)) return hipErrorInvalidValue;
+    const int nchunk = (max_keys + DEC_CHUNK - 1) / DEC_CHUNK;
+    float* part = (float*)ws;
+    dim3 grid(H, pl.n_req, nchunk), gm(pl.n_req, H);
+#define DEC(TT, D_)                                                                                    \
+  hipLaunchKernelGGL((attn_decode_kernel<TT, D_, 4>), grid, dim3(256), 0, s, pl, (const TT*)qkv, d,   \
+                     (const TT*)k_cache, (const TT*)v_cache, part, nchunk, scale_log2);               \
+  hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
+                     nchunk, d, (TT*)out)
+    if (dtype == VFM_BF16) {
+      if (DH == 64) { DEC(bf16, 64); } else { DEC(bf16, 128); }
+    } else {
+      if (DH == 64) { DEC(float, 64); } else { DEC(float, 128); }
+    }
 #undef DEC
     return hipGetLastError();
   }

@@ -1,0 +1,448 @@
+// Shared projections for small batches (decode: one token per request).
+//
+// With a few hundred rows every weight element is used by few rows, so the
+// shared projections stream the weights from HBM, and the per-task LoRA work
+// is a gather of each task's factors for the handful of rows it owns
+// (Section 4.2 adapter handling, applied per task on the shared batch).
+// Three kernels per projection group replace the large-tile GEMM:
+//
+//   gemm_skinny    Z[s, m, n] = sum over K range s of X[m, k] W[n, k]:
+//                  256-row x BN-column tiles, two LDS stages fed by
+//                  global_load_lds, K split so the grid covers the chip.
+//                  Partials stay per split (fp32, no atomics), so results
+//                  do not depend on scheduling.
+//   shrink_split   P[c, m, slot + j] = sum over K chunk c of X[m, k] A_t[j, k]:
+//                  one block per (task row tile, K chunk), so a task's A
+//                  factors are read once, by many blocks at a time.
+//   lora_reduce    U = bf16(s_t * sum_c P), one pass over the partials
+//   lora_expand_z  one more partial slice Z[ns] = U B_t^T: one block per
+//                  (task row tile, 256 columns) on the MFMA, so B_t is read
+//                  once per column for all of the task's rows in the tile
+//   finalize       y = sum of the slices + bias, then the activation or
+//                  residual epilogue, streamed one thread per 4 outputs.
+#include <algorithm>
+
+#include "vfm_internal.h"
+
+namespace {
+
+typedef const void __attribute__((address_space(1)))* gptr_t;
+typedef void __attribute__((address_space(3)))* lptr_t;
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+// 128-byte LDS rows: logical 16-byte chunk kc of row r sits at chunk
+// kc ^ ((r >> 1) & 7), which spreads the 16-row fragment reads over all banks.
+__device__ __forceinline__ int swz(int row, int kc) { return kc ^ ((row >> 1) & 7); }
+
+constexpr int SBM = 256, SBK = 64;
+
+// ---------------------------------------------------------------------------
+// Split-K GEMM, BN = 64 * NWN columns per block, 4 x NWN waves of 64 x 64.
+// ---------------------------------------------------------------------------
+template <int NWN>
+__global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
+  constexpr int BN = 64 * NWN, NW = 4 * NWN;
+  constexpr int SA = SBM * SBK, SB = BN * SBK;
+  constexpr int ARND = SBM / (8 * NW), BRND = BN / (8 * NW);
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (SA + SB)];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave & 3, wn = wave >> 2;
+  const int ntn = (a.N + BN - 1) / BN;
+  const int tn = blockIdx.x % ntn, split = blockIdx.x / ntn;
+  const int m0 = blockIdx.y * SBM, n0 = tn * BN;
+  const int nkt = a.K / SBK;
+  const int kt0 = (int)((int64_t)split * nkt / a.nsplit);
+  const int kt1 = (int)((int64_t)(split + 1) * nkt / a.nsplit);
+  const bf16* X = (const bf16*)a.X;
+
+  // each wave fills 8 rows x 128 B (1 KB) of LDS per round; the swizzle is
+  // applied on the global side, so lane l writes chunk (l & 7) of its row
+  const int row0 = wave * 8 + (lane >> 3);
+  const int kc0 = (lane & 7) ^ ((row0 >> 1) & 7);  // same for row0 + 8 * NW * i
+  const bf16* xsrc[ARND];
+#pragma unroll
+  for (int i = 0; i < ARND; ++i)
+    xsrc[i] = X + (int64_t)min(m0 + row0 + i * 8 * NW, a.M - 1) * a.ldx + kc0 * 8;
+  const bf16* wsrc[BRND];
+#pragma unroll
+  for (int i = 0; i < BRND; ++i) {
+    const int n = min(n0 + row0 + i * 8 * NW, a.N - 1);
+    const bool hi = a.W2 != nullptr && n >= a.n_half;
+    wsrc[i] = (const bf16*)(hi ? a.W2 : a.W) + (int64_t)(hi ? n - a.n_half : n) * a.K + kc0 * 8;
+  }
+  auto issue = [&](int kt, int st) {
+    bf16* As = smem + st * (SA + SB);
+    bf16* Bs = As + SA;
+    const int k0 = kt * SBK;
+#pragma unroll
+    for (int i = 0; i < ARND; ++i)
+      __builtin_amdgcn_global_load_lds((gptr_t)(xsrc[i] + k0), (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < BRND; ++i)
+      __builtin_amdgcn_global_load_lds((gptr_t)(wsrc[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16, 0, 0);
+  };
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (kt0 < kt1) {
+    issue(kt0, 0);
+    __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): the stage has landed in LDS
+    __builtin_amdgcn_s_barrier();
+    for (int kt = kt0; kt < kt1; ++kt) {
+      const int st = (kt - kt0) & 1;
+      if (kt + 1 < kt1) issue(kt + 1, st ^ 1);
+      const bf16* As = smem + st * (SA + SB);
+      const bf16* Bs = As + SA;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int kc = kk * 4 + (lane >> 4);
+        bf16x8 wf[4], xf[4];
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int r = wn * 64 + ni * 16 + (lane & 15);
+          wf[ni] = *reinterpret_cast<const bf16x8*>(Bs + r * SBK + swz(r, kc) * 8);
+        }
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi) {
+          const int r = wm * 64 + mi * 16 + (lane & 15);
+          xf[mi] = *reinterpret_cast<const bf16x8*>(As + r * SBK + swz(r, kc) * 8);
+        }
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = mfma16(wf[ni], xf[mi], acc[mi][ni]);
+      }
+      __builtin_amdgcn_s_waitcnt(0xF70);
+      __builtin_amdgcn_s_barrier();
+    }
+  }
+  // lane holds D[n = 4 * (lane >> 4) + i][m = lane & 15] of each 16 x 16 block
+  float* Zs = a.Z + (int64_t)split * a.M * a.N;
+#pragma unroll
+  for (int mi = 0; mi < 4; ++mi) {
+    const int m = m0 + wm * 64 + mi * 16 + (lane & 15);
+    if (m >= a.M) continue;
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      const int n = n0 + wn * 64 + ni * 16 + 4 * (lane >> 4);
+      if (n >= a.N) continue;
+      *reinterpret_cast<float4*>(Zs + (int64_t)m * a.N + n) =
+          make_float4(acc[mi][ni][0], acc[mi][ni][1], acc[mi][ni][2], acc[mi][ni][3]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Split-K segmented shrink.  Each wave owns 16 rows of the tile and every
+// projection of the group; A rows feed the MFMA A slot, X rows the B slot.
+// ---------------------------------------------------------------------------
+template <int NP, int NSUB>
+__global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitArgs a) {
+  const int tile = blockIdx.x, c = blockIdx.y;
+  const int t = upper_index(pl.rtile_off, pl.n_tasks + 1, tile);
+  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
+  const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rank = min(a.rank[t], a.rpad);
+  const int m = r0 + wave * 16 + (lane & 15);
+  const int k0 = c * a.kchunk, k1 = min(k0 + a.kchunk, a.K);
+  const bf16* X = (const bf16*)a.X;
+  f32x4 acc[NP][NSUB];
+#pragma unroll
+  for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) acc[pp][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (rank > 0 && r0 + wave * 16 < r1) {
+    const bf16* xrow = X + (int64_t)min(m, r1 - 1) * a.ldx + 8 * (lane >> 4);
+    const bf16* arow[NP][NSUB];
+    bool on[NSUB];
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) on[s] = s * 16 + (lane & 15) < rank;
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp) {
+      const bf16* At = (const bf16*)a.A[pp][t];
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s)
+        arow[pp][s] = At + (int64_t)min(s * 16 + (lane & 15), rank - 1) * a.K + 8 * (lane >> 4);
+    }
+#pragma unroll 4
+    for (int k = k0; k < k1; k += 32) {
+      const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
+#pragma unroll
+      for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+          bf16x8 af = *reinterpret_cast<const bf16x8*>(arow[pp][s] + k);
+          if (!on[s]) af = bf16x8{};
+          acc[pp][s] = mfma16(af, xf, acc[pp][s]);
+        }
+    }
+  }
+  if (m < r1) {
+    float* P = a.P + ((int64_t)c * pl.T + m) * a.ldp;
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s)
+        *reinterpret_cast<float4*>(P + a.ucol[pp] + s * 16 + 4 * (lane >> 4)) =
+            make_float4(acc[pp][s][0], acc[pp][s][1], acc[pp][s][2], acc[pp][s][3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LoRA reduce: U[m, ucol[q] + j] = bf16(s_t * sum_c P[c, m, ucol[q] + j])
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void lora_reduce_kernel(Plan pl, LoraReduceArgs a) {
+  const int per_row = a.n_slots * a.rpad / 4;  // 4-column groups per row
+  const int g = blockIdx.x * 256 + threadIdx.x;
+  if (g >= pl.T * per_row) return;
+  const int m = g / per_row, e = g % per_row;
+  const int q = e / (a.rpad / 4), j = (e % (a.rpad / 4)) * 4;
+  const float sc = a.scale[pl.row_task[m]];
+  const float* P = a.P + (int64_t)m * a.ldp + a.ucol[q] + j;
+  const int64_t cs = (int64_t)pl.T * a.ldp;
+  float4 s4[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) s4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  int c = 0;
+  for (; c + 4 <= a.kchunks; c += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = *reinterpret_cast<const float4*>(P + (c + i) * cs);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      s4[i].x += v[i].x; s4[i].y += v[i].y; s4[i].z += v[i].z; s4[i].w += v[i].w;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {  // the last kchunks mod 4 chunks
+    if (c + i >= a.kchunks) break;
+    const float4 v = *reinterpret_cast<const float4*>(P + (c + i) * cs);
+    s4[i].x += v.x; s4[i].y += v.y; s4[i].z += v.z; s4[i].w += v.w;
+  }
+  const float r4[4] = {(s4[0].x + s4[1].x) + (s4[2].x + s4[3].x), (s4[0].y + s4[1].y) + (s4[2].y + s4[3].y),
+                       (s4[0].z + s4[1].z) + (s4[2].z + s4[3].z), (s4[0].w + s4[1].w) + (s4[2].w + s4[3].w)};
+  bf16x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = (bf16)(r4[i] * sc);
+  *reinterpret_cast<bf16x4*>(a.U + (int64_t)m * a.ldu + a.ucol[q] + j) = o;
+}
+
+// ---------------------------------------------------------------------------
+// LoRA expand into one more partial slice: L[m, n] = U[m, slot(n)] . B_t[n', :r]
+// for every column n of Z (SwiGLU: gate columns [0, N), up [N, 2N)); zero
+// where the task has no adapter for the slot.  Block = one task row tile
+// (<= 64 rows) x 256 columns; wave w owns 64 columns as four 16-column
+// blocks.  B_t rows feed the MFMA A slot, U rows the B slot, so each lane
+// ends with 4 consecutive columns of one row.  B_t is read once per (tile,
+// column): the per-task adapter gather.
+// ---------------------------------------------------------------------------
+constexpr int EXP_COLS = 256;
+
+__global__ __launch_bounds__(256) void lora_expand_z_kernel(Plan pl, ExpandZArgs a) {
+  const int tile = blockIdx.x;
+  const int t = upper_index(pl.rtile_off, pl.n_tasks + 1, tile);
+  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
+  const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
+  const int nrb = (r1 - r0 + 15) / 16;       // 16-row blocks of the tile
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int cw = blockIdx.y * EXP_COLS + wave * 64;   // the wave's first Z column
+  if (cw >= a.NZ) return;
+  const int slot = min(cw / a.slot_width, 2);
+  const int brow0 = cw - slot * a.slot_width;
+  const int r = min(a.rank[t], a.max_rank);
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (r > 0 && a.B[slot] != nullptr) {
+    const bf16* Bt = (const bf16*)a.B[slot][t];
+    for (int k0 = 0; k0 < r; k0 += 32) {
+      const int kof = k0 + 8 * (lane >> 4);
+      const bool kon = kof < r;
+      bf16x8 bf[4], uf[4];
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        bf[cb] = bf16x8{};
+        if (kon) bf[cb] = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)(brow0 + cb * 16 + (lane & 15)) * r + kof);
+      }
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        uf[rb] = bf16x8{};
+        const int m = r0 + rb * 16 + (lane & 15);
+        if (rb < nrb && kon && m < r1)
+          uf[rb] = *reinterpret_cast<const bf16x8*>(a.U + (int64_t)m * a.ldu + a.ucol[slot] + kof);
+      }
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        if (rb >= nrb) continue;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = mfma16(bf[cb], uf[rb], acc[rb][cb]);
+      }
+    }
+  }
+#pragma unroll
+  for (int rb = 0; rb < 4; ++rb) {
+    const int m = r0 + rb * 16 + (lane & 15);
+    if (rb >= nrb || m >= r1) continue;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+      *reinterpret_cast<float4*>(a.L + (int64_t)m * a.NZ + cw + cb * 16 + 4 * (lane >> 4)) =
+          make_float4(acc[rb][cb][0], acc[rb][cb][1], acc[rb][cb][2], acc[rb][cb][3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Finalize: sum of the partial slices (fixed order) + bias + epilogue, one
+// thread per row and 4 output columns; every load is independent of the
+// others, so the kernel streams the partials.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void add4(float4& a, const float4& b) {
+  a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+}
+
+__device__ __forceinline__ float4 sum_slices(const float* z, int64_t zs, int ns) {
+  float4 s4[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s4[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+  int sp = 0;
+  for (; sp + 4 <= ns; sp += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4*>(z + (sp + j) * zs);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) add4(s4[j], v[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < 3; ++j)  // the last ns mod 4 slices
+    if (sp + j < ns) add4(s4[j], *reinterpret_cast<const float4*>(z + (sp + j) * zs));
+  add4(s4[0], s4[1]);
+  add4(s4[2], s4[3]);
+  add4(s4[0], s4[2]);
+  return s4[0];
+}
+
+__global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
+  const int per_row = a.N / 4;
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (g >= (int64_t)a.M * per_row) return;
+  const int m = (int)(g / per_row), n = (int)(g % per_row) * 4;
+  const bool swiglu = a.epi == EPI_SWIGLU;
+  const int nz = swiglu ? 2 * a.N : a.N;   // columns of Z
+  const int64_t zs = (int64_t)a.M * nz;
+  const float* z = a.Z + (int64_t)m * nz + n;
+  float4 v = sum_slices(z, zs, a.nslices);
+  if (a.bias && !swiglu) {
+    const bf16x4 bv = *reinterpret_cast<const bf16x4*>((const bf16*)a.bias + n);
+    v.x += (float)bv[0]; v.y += (float)bv[1]; v.z += (float)bv[2]; v.w += (float)bv[3];
+  }
+  if (a.epi == EPI_RESID) {
+    float4* xo = reinterpret_cast<float4*>((float*)a.out + (int64_t)m * a.ldo + n);
+    float4 xv = *xo;
+    add4(xv, v);
+    *xo = xv;
+    return;
+  }
+  const float g4[4] = {v.x, v.y, v.z, v.w};
+  float u4[4] = {0.f, 0.f, 0.f, 0.f};
+  if (swiglu) {
+    const float4 u = sum_slices(z + a.N, zs, a.nslices);
+    u4[0] = u.x; u4[1] = u.y; u4[2] = u.z; u4[3] = u.w;
+  }
+  bf16x4 o;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    float y = g4[c];
+    if (swiglu) y = y / (1.f + __expf(-y)) * u4[c];
+    else if (a.epi == EPI_GELU) y = gelu_erf_fast(y);
+    o[c] = (bf16)y;
+  }
+  *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + n) = o;
+}
+
+// Column-tile width and K split of the small-batch GEMM for an N x K
+// weight, from a sweep of 256-row products on MI355X: wide weights (N >=
+// 8192) take 256-column tiles, narrow ones 64-column tiles (two blocks per
+// CU), and K is split until one row tile fills the chip once (256 or 512
+// blocks), at most 4 ways for wide weights so the fp32 partials stay below
+// the weight bytes.  The split depends on the weight shape only, never on
+// the batch, so a row's result does not depend on the other rows.
+void skinny_shape(int N, int K, int* bn, int* nsplit) {
+  const int nkt = K / SBK;
+  const bool wide = N >= 8192;
+  const int b = wide ? 256 : 64;
+  const int slots = wide ? 256 : 512;
+  const int tiles = (N + b - 1) / b;
+  const int cap = wide ? 4 : 16;
+  *bn = b;
+  *nsplit = std::max(1, std::min(std::min(slots / tiles, cap), nkt));
+}
+
+}  // namespace
+
+int skinny_splits(int N, int K) {
+  int bn, ns;
+  skinny_shape(N, K, &bn, &ns);
+  return ns;
+}
+
+hipError_t launch_gemm_skinny(const SkinnyArgs& a0, hipStream_t s) {
+  if (a0.M == 0) return hipSuccess;
+  SkinnyArgs a = a0;
+  int bn;
+  skinny_shape(a.N, a.K, &bn, &a.nsplit);
+  const int ntn = (a.N + bn - 1) / bn;
+  dim3 grid(ntn * a.nsplit, (a.M + SBM - 1) / SBM);
+  switch (bn) {
+    case 64: hipLaunchKernelGGL(gemm_skinny_kernel<1>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(gemm_skinny_kernel<2>, grid, dim3(512), 0, s, a); break;
+    default: hipLaunchKernelGGL(gemm_skinny_kernel<4>, grid, dim3(1024), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+// K chunks of the split shrink: fixed 256-column chunks (the last one
+// ragged), independent of the batch for the same reason as the GEMM split.
+int shrink_chunks(int K) { return (K + 255) / 256; }
+
+hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a0, hipStream_t s) {
+  if (pl.n_rtiles == 0 || a0.n_proj == 0) return hipSuccess;
+  ShrinkSplitArgs a = a0;
+  a.kchunk = 256;
+  dim3 grid(pl.n_rtiles, a.kchunks);
+#define VFM_SS(NP_, NS_) hipLaunchKernelGGL((shrink_split_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
+  if (a.rpad == 32) {
+    if (a.n_proj == 1) VFM_SS(1, 2); else if (a.n_proj == 2) VFM_SS(2, 2); else VFM_SS(3, 2);
+  } else {
+    if (a.n_proj == 1) VFM_SS(1, 4); else if (a.n_proj == 2) VFM_SS(2, 4); else VFM_SS(3, 4);
+  }
+#undef VFM_SS
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_reduce(const Plan& pl, const LoraReduceArgs& a, hipStream_t s) {
+  const int64_t n = (int64_t)pl.T * a.n_slots * a.rpad / 4;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(lora_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pl, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_expand_z(const Plan& pl, const ExpandZArgs& a, hipStream_t s) {
+  if (pl.n_rtiles == 0) return hipSuccess;
+  dim3 grid(pl.n_rtiles, (a.NZ + EXP_COLS - 1) / EXP_COLS);
+  hipLaunchKernelGGL(lora_expand_z_kernel, grid, dim3(256), 0, s, pl, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s) {
+  const int64_t n = (int64_t)a.M * (a.N / 4);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}

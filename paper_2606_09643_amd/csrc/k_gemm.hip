@@ -40,23 +40,6 @@ __device__ __forceinline__ int swz(int row, int kc) { return kc ^ swz_bits(row);
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.f + erff(v * 0.70710678118654752440f));
 }
-// GELU for bf16 outputs: erf from Abramowitz & Stegun, Handbook of
-// Mathematical Functions, formula 7.1.26 (|error| <= 1.5e-7, far below the
-// 2^-9 rounding of the bf16 result), about a third of the instructions of a
-// full-precision erff.
-__device__ __forceinline__ float gelu_erf_fast(float v) {
-  const float x = fabsf(v) * 0.70710678118654752440f;
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.f));
-  float poly = fmaf(1.061405429f, t, -1.453152027f);
-  poly = fmaf(poly, t, 1.421413741f);
-  poly = fmaf(poly, t, -0.284496736f);
-  poly = fmaf(poly, t, 0.254829592f);
-  poly *= t;
-  const float e = poly * __expf(-x * x);          // 1 - erf(|v|/sqrt 2)
-  const float erf_abs = 1.f - e;
-  const float erf_v = v < 0.f ? -erf_abs : erf_abs;
-  return 0.5f * v * (1.f + erf_v);
-}
 __device__ __forceinline__ float silu_f(float v) { return v / (1.f + expf(-v)); }
 
 __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {

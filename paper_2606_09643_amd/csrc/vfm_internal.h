@@ -92,6 +92,24 @@ template <typename T> __device__ inline T from_f32(float v);
 template <> __device__ inline float from_f32<float>(float v) { return v; }
 template <> __device__ inline bf16 from_f32<bf16>(float v) { return (bf16)v; }
 
+// GELU for bf16 outputs: erf from Abramowitz & Stegun, Handbook of
+// Mathematical Functions, formula 7.1.26 (|error| <= 1.5e-7, far below the
+// 2^-9 rounding of the bf16 result), about a third of the instructions of a
+// full-precision erff.
+__device__ inline float gelu_erf_fast(float v) {
+  const float x = fabsf(v) * 0.70710678118654752440f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.f));
+  float poly = fmaf(1.061405429f, t, -1.453152027f);
+  poly = fmaf(poly, t, 1.421413741f);
+  poly = fmaf(poly, t, -0.284496736f);
+  poly = fmaf(poly, t, 0.254829592f);
+  poly *= t;
+  const float e = poly * __expf(-x * x);          // 1 - erf(|v|/sqrt 2)
+  const float erf_abs = 1.f - e;
+  const float erf_v = v < 0.f ? -erf_abs : erf_abs;
+  return 0.5f * v * (1.f + erf_v);
+}
+
 // Benchmark timing hooks (profile.hip): bracket one launch of class `cls`.
 int prof_begin(int cls, hipStream_t s);
 void prof_end(int idx, hipStream_t s);
@@ -152,15 +170,73 @@ struct GemmArgs {
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 
+// ---- small-batch (decode) projections, bf16 only -------------------------
+// Split-K shared GEMM into fp32 partials: Z[s, m, n] = sum over the s-th
+// K range of X[m, k] W[n, k]; rows n >= n_half of the stacked weight come
+// from W2 (SwiGLU: gate columns then up columns).
+struct SkinnyArgs {
+  const void* X; int ldx;
+  const void* W; const void* W2; int n_half;
+  int M, N, K;
+  int nsplit;
+  float* Z;
+};
+hipError_t launch_gemm_skinny(const SkinnyArgs& a, hipStream_t s);
+int skinny_splits(int N, int K);
+
+// Split-K segmented LoRA shrink into fp32 partials:
+// P[c, m, ucol[p] + j] = sum over K chunk c of X[m, k] A_{t,p}[j, k] for
+// j < rpad (zero past rank_t); kchunks chunks of kchunk columns.
+struct ShrinkSplitArgs {
+  const void* X; int ldx; int K;
+  const void* const* A[3]; int ucol[3]; int n_proj;
+  float* P; int ldp; int rpad; int kchunk; int kchunks;
+  const int32_t* rank;
+};
+hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a, hipStream_t s);
+int shrink_chunks(int K);
+
+// U[m, ucol[q] + j] = bf16(scale_t * sum_c P[c, m, ucol[q] + j]), q < n_slots, j < rpad.
+struct LoraReduceArgs {
+  const float* P; int ldp; int kchunks;
+  bf16* U; int ldu;
+  int ucol[3]; int n_slots; int rpad;
+  const float* scale;
+};
+hipError_t launch_lora_reduce(const Plan& pl, const LoraReduceArgs& a, hipStream_t s);
+
+// Per-task LoRA expand into a partial slice L [M, NZ] (fp32, every entry
+// written): L[m, n] = U[m, ucol[slot] ..] . B_{t,slot}[n - slot * slot_width, :r_t]
+// with slot = n / slot_width (a multiple of 64; SwiGLU: slot_width = N, so
+// gate columns are slot 0 and up columns slot 1).
+struct ExpandZArgs {
+  const bf16* U; int ldu; int ucol[3];
+  const void* const* B[3]; int slot_width;
+  const int32_t* rank; int max_rank;
+  float* L; int NZ;
+};
+hipError_t launch_lora_expand_z(const Plan& pl, const ExpandZArgs& a, hipStream_t s);
+
+// Sum of nslices partial slices Z[s] ([M, N], SwiGLU [M, 2N]: gate then up
+// columns) in a fixed order, plus bias, and the epilogue of GemmEpi.
+struct FinalizeArgs {
+  const float* Z; int nslices; int M; int N; int epi;   // epi: GemmEpi
+  const void* bias;
+  void* out; int ldo;
+};
+hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
+
 // In-place rotary embedding of the q and k parts of qkv [T, 3d].
 hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
                        float theta, hipStream_t s);
 
 // Attention per request over qkv [T, 3d] (plan order) into out [T, d].
+// Decode needs attention_workspace() bytes of ws; max_keys = the largest
+// ctx + length over the batch's requests.
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv,
                             void* out, void* k_cache, void* v_cache, void* ws, size_t ws_bytes,
-                            hipStream_t s);
-size_t attention_workspace(const vfm_cfg& c, const Plan& pl);
+                            int max_keys, hipStream_t s);
+size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys);
 
 // Input rows into the fp32 residual stream (plan order).
 hipError_t launch_embed(int dtype, const Plan& pl, int mode, const void* src, int width,

@@ -133,3 +133,11 @@ def test_validation_rejects_before_launch():
     sw = B.make_cfg(B.VFM_BF16, 768, 12, 64, 3072, 1, 1, 1, 1, 1e-6, 1e4)
     assert lib.vfm_workspace_size(C.byref(sw), C.byref(bc), None, C.byref(n)) == B.VFM_ERR_UNSUPPORTED
     assert B.vfm_status_string(B.VFM_ERR_TASK) == "task id out of range"
+
+
+def test_binding_constants_match_header():
+    """The binding's copies of the header's #define constants agree with it."""
+    src = open(os.path.join(ROOT, "include", "vfm.h")).read()
+    defs = dict(re.findall(r"#define\s+(VFM_\w+)\s+(\d+)", src))
+    for name in ("VFM_PLAN_HEADER", "VFM_ROW_TILE", "VFM_SMALL_BATCH_ROWS"):
+        assert int(defs[name]) == getattr(B, name), name

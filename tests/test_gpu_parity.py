@@ -178,15 +178,26 @@ def test_lora_apply(dtype, idx):
         assert worst < (2e-2 if dtype == "bf16" else 1e-5)
 
 
+# Batch-invariance cases: workload 2 with every task alone still above the
+# small-batch threshold (large-tile kernels), workload 4 below it (split-K).
+INVARIANCE = {
+    2: dict(task_id=[5, 0, 2, 0, 5, 2, 2, 5, 0, 5, 0, 2, 0, 2, 5, 5, 2, 0], seq_len=[197] * 18),
+    4: SMALL[4],
+}
+
+
 @pytest.mark.parametrize("idx", [2, 4])
 def test_batch_invariance_and_zero_rank_bit_exact(idx):
     """A task's rows are bit-identical whether co-batched with other tasks or
-    run alone, and a rank-0 task equals the bare backbone bit for bit."""
+    run alone (both batches on one side of the small-batch threshold), and a
+    rank-0 task equals the bare backbone bit for bit."""
     w = wl.WORKLOADS[idx]
     ranks = np.full(w.n_tasks, w.rank, np.int32)
     ranks[0] = 0
-    case = SMALL[idx]
-    w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, ranks=ranks, b_std=0.1)
+    case = INVARIANCE[idx]
+    w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, ranks=ranks, b_std=0.1,
+                                                    case=case)
+    small = pb.T < B.VFM_SMALL_BATCH_ROWS
     fwd.embed()
     fwd.layer(0)
     torch.cuda.synchronize()
@@ -196,6 +207,7 @@ def test_batch_invariance_and_zero_rank_bit_exact(idx):
         keep = [i for i, tt in enumerate(case["task_id"]) if tt == t]
         sub = _batch(w, [case["task_id"][i] for i in keep], [case["seq_len"][i] for i in keep])
         pbs = R.make_batch(w, sub, model.heads)
+        assert (pbs.T < B.VFM_SMALL_BATCH_ROWS) == small
         inps = R.Inputs(w, sub)
         # the same input rows as in the mixed batch
         cu_o = pl["cu_orig"]
