@@ -552,18 +552,40 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
 template <typename T, int DH>
 __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const float* __restrict__ part,
                                                                int nchunk, int d, T* __restrict__ out) {
+  constexpr int MAXC = 64;                   // chunks merged per pass through LDS
+  __shared__ float sw[MAXC];
   const int p = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
   const int R = pl.cu_seqlens[p];
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int nc = min((nkeys + DEC_CHUNK - 1) / DEC_CHUNK, nchunk);
   const float* rec = part + ((int64_t)p * gridDim.y + h) * nchunk * (DH + 2);
+  // global max of the chunk maxima (all threads read the same few values)
   float M = NEG_BIG;
   for (int c = 0; c < nc; ++c) M = fmaxf(M, rec[c * (DH + 2)]);
   float lsum = 0.f, acc = 0.f;
-  for (int c = 0; c < nc; ++c) {
-    const float w = exp2f(rec[c * (DH + 2)] - M);
-    lsum += rec[c * (DH + 2) + 1] * w;
-    acc += rec[c * (DH + 2) + 2 + tid] * w;
+  for (int c0 = 0; c0 < nc; c0 += MAXC) {
+    const int cn = min(MAXC, nc - c0);
+    __syncthreads();
+    if (tid < cn) sw[tid] = exp2f(rec[(c0 + tid) * (DH + 2)] - M);   // chunk weights, in parallel
+    __syncthreads();
+    int c = 0;
+    for (; c + 4 <= cn; c += 4) {
+      float o4[4], l4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        o4[j] = rec[(c0 + c + j) * (DH + 2) + 2 + tid];
+        l4[j] = rec[(c0 + c + j) * (DH + 2) + 1];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        lsum += l4[j] * sw[c + j];
+        acc += o4[j] * sw[c + j];
+      }
+    }
+    for (; c < cn; ++c) {
+      lsum += rec[(c0 + c) * (DH + 2) + 1] * sw[c];
+      acc += rec[(c0 + c) * (DH + 2) + 2 + tid] * sw[c];
+    }
   }
   out[(int64_t)R * d + h * DH + tid] = from_f32<T>(acc / lsum);
 }

@@ -143,8 +143,9 @@ __global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
 // ---------------------------------------------------------------------------
 template <int NP, int NSUB>
 __global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitArgs a) {
+  __shared__ int s_task;
   const int tile = blockIdx.x, c = blockIdx.y;
-  const int t = upper_index(pl.rtile_off, pl.n_tasks + 1, tile);
+  const int t = block_tile_task(pl, tile, &s_task);
   const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
   const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -245,56 +246,55 @@ __global__ __launch_bounds__(256) void lora_reduce_kernel(Plan pl, LoraReduceArg
 constexpr int EXP_COLS = 256;
 
 __global__ __launch_bounds__(256) void lora_expand_z_kernel(Plan pl, ExpandZArgs a) {
+  __shared__ int s_task;
   const int tile = blockIdx.x;
-  const int t = upper_index(pl.rtile_off, pl.n_tasks + 1, tile);
+  const int t = block_tile_task(pl, tile, &s_task);
   const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
   const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
-  const int nrb = (r1 - r0 + 15) / 16;       // 16-row blocks of the tile
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int cw = blockIdx.y * EXP_COLS + wave * 64;   // the wave's first Z column
   if (cw >= a.NZ) return;
   const int slot = min(cw / a.slot_width, 2);
   const int brow0 = cw - slot * a.slot_width;
   const int r = min(a.rank[t], a.max_rank);
-  f32x4 acc[4][4];
+  const bool on = r > 0 && a.B[slot] != nullptr;
+  // the task's B rows of the wave's 64 columns, all of the rank (<= 64)
+  bf16x8 bf[2][4];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb)
+  for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (r > 0 && a.B[slot] != nullptr) {
-    const bf16* Bt = (const bf16*)a.B[slot][t];
-    for (int k0 = 0; k0 < r; k0 += 32) {
-      const int kof = k0 + 8 * (lane >> 4);
-      const bool kon = kof < r;
-      bf16x8 bf[4], uf[4];
+    for (int cb = 0; cb < 4; ++cb) bf[kk][cb] = bf16x8{};
+  const bf16* Bt = on ? (const bf16*)a.B[slot][t] : nullptr;
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
-        bf[cb] = bf16x8{};
-        if (kon) bf[cb] = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)(brow0 + cb * 16 + (lane & 15)) * r + kof);
-      }
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        uf[rb] = bf16x8{};
-        const int m = r0 + rb * 16 + (lane & 15);
-        if (rb < nrb && kon && m < r1)
-          uf[rb] = *reinterpret_cast<const bf16x8*>(a.U + (int64_t)m * a.ldu + a.ucol[slot] + kof);
-      }
-#pragma unroll
-      for (int rb = 0; rb < 4; ++rb) {
-        if (rb >= nrb) continue;
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = mfma16(bf[cb], uf[rb], acc[rb][cb]);
-      }
-    }
-  }
-#pragma unroll
-  for (int rb = 0; rb < 4; ++rb) {
-    const int m = r0 + rb * 16 + (lane & 15);
-    if (rb >= nrb || m >= r1) continue;
+  for (int kk = 0; kk < 2; ++kk) {
+    const int kof = kk * 32 + 8 * (lane >> 4);
+    if (!on || kof >= r) continue;
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
-      *reinterpret_cast<float4*>(a.L + (int64_t)m * a.NZ + cw + cb * 16 + 4 * (lane >> 4)) =
-          make_float4(acc[rb][cb][0], acc[rb][cb][1], acc[rb][cb][2], acc[rb][cb][3]);
+      bf[kk][cb] = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)(brow0 + cb * 16 + (lane & 15)) * r + kof);
+  }
+  for (int rb = r0; rb < r1; rb += 16) {
+    const int m = rb + (lane & 15);
+    f32x4 acc[4];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (on) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        if (kk * 32 >= r) break;
+        const int kof = kk * 32 + 8 * (lane >> 4);
+        bf16x8 uf = bf16x8{};
+        if (kof < r && m < r1) uf = *reinterpret_cast<const bf16x8*>(a.U + (int64_t)m * a.ldu + a.ucol[slot] + kof);
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[cb] = mfma16(bf[kk][cb], uf, acc[cb]);
+      }
+    }
+    if (m < r1) {
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        *reinterpret_cast<float4*>(a.L + (int64_t)m * a.NZ + cw + cb * 16 + 4 * (lane >> 4)) =
+            make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
+    }
   }
 }
 

@@ -75,6 +75,65 @@ __device__ inline void norm_row_regs(const float* xr, int d, const TW* g, const 
   }
 }
 
+// Few rows (decode): one 256-thread block per row, MAXC float4 chunks per
+// thread, block reductions through LDS, so a small batch still keeps every
+// CU busy.
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void norm_rows_block_kernel(const float* __restrict__ x, int d,
+                                                              const T* __restrict__ g,
+                                                              const T* __restrict__ b, int kind,
+                                                              float eps, T* __restrict__ out) {
+  __shared__ float red[2][4];
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = d >> 2;
+  const float* xr = x + (int64_t)row * d;
+  float4 v[MAXC], gg[MAXC], bb[MAXC];
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = tid + 256 * i;
+    if (c < nch) {
+      v[i] = *reinterpret_cast<const float4*>(xr + 4 * c);
+      gg[i] = load4<T>(g + 4 * c);
+      bb[i] = b ? load4<T>(b + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+  }
+  float mean = 0.f;
+  if (kind == VFM_NORM_LAYER) {
+    sum = wave_sum(sum);
+    if (lane == 0) red[0][wave] = sum;
+    __syncthreads();
+    mean = ((red[0][0] + red[0][1]) + (red[0][2] + red[0][3])) / (float)d;
+  }
+  float sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = tid + 256 * i;
+    if (c < nch) {
+      const float a = v[i].x - mean, b2 = v[i].y - mean, cc = v[i].z - mean, dd = v[i].w - mean;
+      sq += (a * a + b2 * b2) + (cc * cc + dd * dd);
+    }
+  }
+  sq = wave_sum(sq);
+  if (lane == 0) red[1][wave] = sq;
+  __syncthreads();
+  const float rstd = rsqrtf(((red[1][0] + red[1][1]) + (red[1][2] + red[1][3])) / (float)d + eps);
+  T* o = out + (int64_t)row * d;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = tid + 256 * i;
+    if (c < nch) {
+      float4 y;
+      y.x = (v[i].x - mean) * rstd * gg[i].x + bb[i].x;
+      y.y = (v[i].y - mean) * rstd * gg[i].y + bb[i].y;
+      y.z = (v[i].z - mean) * rstd * gg[i].z + bb[i].z;
+      y.w = (v[i].w - mean) * rstd * gg[i].w + bb[i].w;
+      store4<T>(o + 4 * c, y);
+    }
+  }
+}
+
 template <typename T, int MAXI>
 __global__ __launch_bounds__(256) void norm_rows_kernel(const float* __restrict__ x, int n_rows,
                                                         int d, const T* __restrict__ g,
@@ -210,6 +269,14 @@ inline int maxi_for(int d) { return d <= 1024 ? 4 : (d <= 4096 ? 16 : 32); }
 hipError_t launch_norm(int dtype, const float* x, int T, int d, const void* g, const void* b,
                        int kind, float eps, void* out, hipStream_t s) {
   if (T == 0) return hipSuccess;
+  if (T < 2048 && d >= 1024) {   // few rows: a block per row (d <= 8192: <= 8 chunks per thread)
+#define NORM_BLOCK(TT)                                                                           \
+  hipLaunchKernelGGL((norm_rows_block_kernel<TT, 8>), dim3(T), dim3(256), 0, s, x, d, (const TT*)g, \
+                     (const TT*)b, kind, eps, (TT*)out)
+    if (dtype == VFM_BF16) NORM_BLOCK(bf16); else NORM_BLOCK(float);
+#undef NORM_BLOCK
+    return hipGetLastError();
+  }
   dim3 grid((T + 3) / 4), block(256);
   const int mi = maxi_for(d);
 #define NORM_LAUNCH(TT, MI)                                                                   \

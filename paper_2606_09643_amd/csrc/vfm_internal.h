@@ -86,6 +86,19 @@ __device__ inline int upper_index(const int32_t* arr, int n, int v) {
   return lo;
 }
 
+// The task owning segmented row tile `tile` (rtile_off[t] <= tile <
+// rtile_off[t + 1]; tasks without rows own no tile), found by the whole
+// block in one round of parallel loads instead of a chain of dependent ones.
+// Every thread of the block must call it: it ends with a barrier.
+__device__ inline int block_tile_task(const Plan& pl, int tile, int* slot) {
+  if (threadIdx.x == 0) *slot = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < pl.n_tasks; i += blockDim.x)
+    if (pl.rtile_off[i] <= tile && tile < pl.rtile_off[i + 1]) *slot = i;
+  __syncthreads();
+  return *slot;
+}
+
 __device__ inline float to_f32(float v) { return v; }
 __device__ inline float to_f32(bf16 v) { return (float)v; }
 template <typename T> __device__ inline T from_f32(float v);
