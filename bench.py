@@ -79,6 +79,33 @@ def algorithmic_work(w, batch, ranks, heads_n_out):
 
 
 # --------------------------------------------------------------------------
+# HBM traffic of the dominant kernel, from the committed counter summary
+# --------------------------------------------------------------------------
+def hbm_traffic(workload_name, cls):
+    """Bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each
+    scaled by the same counter's reading for a device copy of known size
+    (profiles/hbm_traffic.json); None when there is no record for this
+    kernel or its sources have changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        rec = json.load(open(path)).get(workload_name)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("class") != cls:
+        return None
+    h = hashlib.sha256()
+    for src in rec["source"]:
+        try:
+            h.update(open(os.path.join(ROOT, src), "rb").read())
+        except OSError:
+            return None
+    if h.hexdigest() != rec["source_sha256"]:
+        return None
+    return float(rec["traffic_bytes_per_launch"])
+
+
+# --------------------------------------------------------------------------
 # CPU baseline: the fp64 oracle on a bounded sample of the same batch
 # --------------------------------------------------------------------------
 def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
@@ -225,7 +252,16 @@ def main():
         achieved = per_launch / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                 "frac": achieved / peak, "traffic": None}
-    roof.update({"kernel": f"{dom} GEMM" if dom.startswith("gemm") else dom,
+    roof["traffic"] = hbm_traffic(w.name, dom)
+    if dom == "attn":
+        kname = "attn_decode_kernel (KV-cache attention)"
+    elif w.dtype != "bf16":
+        kname = "gemm_f32_kernel (MLP up projection + GELU)"
+    elif w.family == "decoder":
+        kname = "gemm_bf16_large_kernel (gate/up projections + SwiGLU, LoRA fused)"
+    else:
+        kname = "gemm_bf16_large_kernel (MLP up projection + GELU, LoRA fused)"
+    roof.update({"kernel": kname,
                  "avg_launch_ms": avg_ms, "launches": dom_n, "per_launch": per_launch})
 
     step_tflops = work["step_flops"] / (ms_step * 1e-3) / 1e12

@@ -615,13 +615,18 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
                             hipStream_t s) {
   const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
+  // timing classes: the attention kernel itself is VFM_PROF_ATTN, the cache
+  // write and the decode merge VFM_PROF_OTHER
+  int pi = -1;
   if (k_cache && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
+    pi = prof_begin(VFM_PROF_OTHER, s);
     if (dtype == VFM_BF16)
       hipLaunchKernelGGL(kv_write_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (const bf16*)qkv, d,
                          (bf16*)k_cache, (bf16*)v_cache);
     else
       hipLaunchKernelGGL(kv_write_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (const float*)qkv, d,
                          (float*)k_cache, (float*)v_cache);
+    prof_end(pi, s);
   }
   if (c.attn == VFM_ATTN_DECODE) {
     if (ws_bytes < attention_workspace(c, pl, max_keys)) return hipErrorInvalidValue;
@@ -629,10 +634,14 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
     float* part = (float*)ws;
     dim3 grid(H, pl.n_req, nchunk), gm(pl.n_req, H);
 #define DEC(TT, D_)                                                                                    \
+  pi = prof_begin(VFM_PROF_ATTN, s);                                                                   \
   hipLaunchKernelGGL((attn_decode_kernel<TT, D_, 4>), grid, dim3(256), 0, s, pl, (const TT*)qkv, d,   \
                      (const TT*)k_cache, (const TT*)v_cache, part, nchunk, scale_log2);               \
+  prof_end(pi, s);                                                                                     \
+  pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
   hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
-                     nchunk, d, (TT*)out)
+                     nchunk, d, (TT*)out);                                                             \
+  prof_end(pi, s)
     if (dtype == VFM_BF16) {
       if (DH == 64) { DEC(bf16, 64); } else { DEC(bf16, 128); }
     } else {
@@ -641,6 +650,7 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
 #undef DEC
     return hipGetLastError();
   }
+  pi = prof_begin(VFM_PROF_ATTN, s);
   dim3 grid(pl.n_qblocks, H);
   const bool causal = c.attn == VFM_ATTN_CAUSAL;
   if (dtype == VFM_BF16 && pl.max_seqlen <= 256) {
@@ -675,5 +685,6 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
       hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 128>), grid, dim3(256), 0, s, pl,
                          (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
   }
+  prof_end(pi, s);
   return hipGetLastError();
 }
