@@ -183,13 +183,15 @@ __device__ __forceinline__ void epilogue_frags(const GemmArgs& a, int wrow0, int
 }
 
 // ---------------------------------------------------------------------------
-// Large-M bf16 GEMM: 256x256x64 block tile, 8 waves (4 along M x 2 along N)
-// of 64x128, operands streamed global -> LDS with global_load_lds_dwordx4
-// (no staging registers), two LDS stages (128 KB), and an XCD-aware tile
-// order: consecutive block ids land on different XCDs (each with its own
-// L2), so block b takes logical tile (b % 8) * per + b / 8 and logical tiles
-// run in groups of LGM row-tiles sweeping all column tiles, keeping each
-// XCD's X rows and W columns resident in its L2.
+// Large-M bf16 GEMM: BMT x BNT x 64 block tile (256 rows, 128 / 192 / 256
+// columns), 8 waves (4 along M x 2 along N) of (BMT/4) x (BNT/2), operands
+// streamed global -> LDS with global_load_lds_dwordx4 (no staging registers),
+// two LDS stages (up to 128 KB), and an XCD-aware tile order: consecutive
+// block ids land on different XCDs (each with its own L2), so block b takes
+// logical tile (b % 8) * per + b / 8 and logical tiles run in groups of LGM
+// row-tiles sweeping all column tiles, keeping each XCD's X rows and W
+// columns resident in its L2.  The launcher picks the tile shape per GEMM
+// so that the last round of tiles fills the 256 CUs as far as possible.
 //
 // The per-task LoRA expand runs as extra 64-wide K steps of the same
 // pipeline: for every task t with rows in the tile, the A tile holds the
@@ -199,21 +201,22 @@ __device__ __forceinline__ void epilogue_frags(const GemmArgs& a, int wrow0, int
 // in the low 32 columns, up rows carry B_up in the high 32.  The MFMA loop
 // cannot tell these steps from the backbone's.
 // ---------------------------------------------------------------------------
-constexpr int LBM = 256, LBN = 256, LGM = 4;
+constexpr int LGM = 4;
 
 __device__ __attribute__((aligned(16))) bf16 g_zero_page[8];  // zero-initialised at load
 
-template <int EPI, bool SWIGLU>
+template <int EPI, bool SWIGLU, int BMT, int BNT>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
-  constexpr int NW = 8, NTH = 512, WN = 2, TM = 64, TN = 128, FM = 4, FN = 8;
-  constexpr int ACH = LBM * 8 / NTH, BCH = LBN * 8 / NTH;  // 4, 4 chunks of 16 B
-  constexpr int SA = LBM * BK, SB = LBN * BK;
+  constexpr int NW = 8, NTH = 512, WN = 2, TM = BMT / 4, TN = BNT / 2, FM = TM / 16, FN = TN / 16;
+  constexpr int ACH = BMT * 8 / NTH, BCH = BNT * 8 / NTH;  // 16-byte chunks per lane and stage
+  constexpr int SA = BMT * BK, SB = BNT * BK;
+  static_assert(BMT % 64 == 0 && BNT % 64 == 0 && FN % 2 == 0, "tile shape");
   constexpr int RSTEP = NTH / 8;                             // 64 rows per chunk step
   __shared__ __attribute__((aligned(16))) bf16 smem[2 * (SA + SB)];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  constexpr int NTILE = SWIGLU ? LBN / 2 : LBN;  // output columns per block
-  const int MT = (a.M + LBM - 1) / LBM, NTn = (a.N + NTILE - 1) / NTILE, ntiles = MT * NTn;
+  constexpr int NTILE = SWIGLU ? BNT / 2 : BNT;  // output columns per block
+  const int MT = (a.M + BMT - 1) / BMT, NTn = (a.N + NTILE - 1) / NTILE, ntiles = MT * NTn;
   const int per = gridDim.x / 8;
   const int Lid = (blockIdx.x % 8) * per + blockIdx.x / 8;
   if (Lid >= ntiles) return;
@@ -226,7 +229,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     tm = fm + r % gm;
     tn = r / gm;
   }
-  const int m0 = tm * LBM, n0 = tn * NTILE;
+  const int m0 = tm * BMT, n0 = tn * NTILE;
   const bf16* X = (const bf16*)a.X;
   const GemmLora& L = a.lora;
 
@@ -235,28 +238,32 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // lane%8, so it loads the logical chunk that the swizzle maps there.
   const int row0 = wave * 8 + (lane >> 3);
   const int kc0 = (lane & 7) ^ swz_bits(row0);  // same for row0 + i * RSTEP
-  const bf16* xsrc[ACH];
+  // element offsets (32-bit: the launcher keeps M * ldx and N * K below 2^31)
+  // of each chunk's row, to keep the 64-bit pointer pairs out of registers
+  int xoff[ACH];
 #pragma unroll
-  for (int i = 0; i < ACH; ++i)
-    xsrc[i] = X + (int64_t)min(m0 + row0 + i * RSTEP, a.M - 1) * a.ldx + kc0 * 8;
-  const bf16* wsrc[BCH];
+  for (int i = 0; i < ACH; ++i) xoff[i] = min(m0 + row0 + i * RSTEP, a.M - 1) * a.ldx + kc0 * 8;
+  int woff[BCH];
 #pragma unroll
   for (int i = 0; i < BCH; ++i) {
     const int row = row0 + i * RSTEP;
     int wrow;
-    const bf16* wb = (const bf16*)a.W;
     if (SWIGLU) {
       const int sub = row >> 4;
-      wb = (sub & 1) ? (const bf16*)a.W2 : (const bf16*)a.W;
       wrow = n0 + (sub >> 1) * 16 + (row & 15);
     } else {
       wrow = n0 + row;
     }
-    wsrc[i] = wb + (int64_t)min(wrow, a.N - 1) * a.K + kc0 * 8;
+    woff[i] = min(wrow, a.N - 1) * a.K + kc0 * 8;
   }
+  // SwiGLU: 16-row groups of the B tile alternate gate (W) and up (W2) rows
+  auto wbase = [&](int i) -> const bf16* {
+    if (SWIGLU && (((row0 + i * RSTEP) >> 4) & 1)) return (const bf16*)a.W2;
+    return (const bf16*)a.W;
+  };
 
   // The LoRA steps of this tile: every task t0..t1 with rows in
-  // [m0, m0 + LBM) (rows are sorted by task), `parts` steps each.  A task of
+  // [m0, m0 + BMT) (rows are sorted by task), `parts` steps each.  A task of
   // rank 0 gets an all-zero B tile.  (Kept out of LDS on purpose: a second
   // LDS object makes the compiler wait for the in-flight DMA before every
   // fragment read.)
@@ -269,7 +276,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     else live = L.B[min(n0 / L.slot_width, 2)] != nullptr;
     if (live) {
       t0 = L.row_task[m0];
-      nlora = (L.row_task[min(m0 + LBM, a.M) - 1] - t0 + 1) * parts;
+      nlora = (L.row_task[min(m0 + BMT, a.M) - 1] - t0 + 1) * parts;
     }
   }
   const int nsteps = nk + nlora;
@@ -306,10 +313,11 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       const int k0 = e * BK;
 #pragma unroll
       for (int i = 0; i < ACH; ++i)
-        __builtin_amdgcn_global_load_lds((gptr_t)(xsrc[i] + k0), (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((gptr_t)(X + xoff[i] + k0), (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
 #pragma unroll
       for (int i = 0; i < BCH; ++i)
-        __builtin_amdgcn_global_load_lds((gptr_t)(wsrc[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((gptr_t)(wbase(i) + woff[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16,
+                                         0, 0);
       return;
     }
     const int t = t0 + (e - nk) / parts, part = (e - nk) % parts;
@@ -626,14 +634,42 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   }
 }
 
+// Tile shape of the large GEMM for an M x N product: the candidate with the
+// least estimated time, rounds of 256 concurrent tiles times the bytes a tile
+// moves per K step (BMT + BNT rows of 128 B; the loop is bound by that
+// stream), among shapes whose column tiles do not straddle a LoRA slot.
+struct LargeShape { int bm, bn; };
+inline LargeShape large_shape(int M, int N, bool sw, int lora_slot_width) {
+  const LargeShape cand[3] = {{256, 256}, {256, 192}, {256, 128}};
+  LargeShape best = {0, 0};
+  double best_cost = 0.0;
+  for (const LargeShape& c : cand) {
+    if (lora_slot_width > 0 && !sw && lora_slot_width % c.bn) continue;
+    const int nt = sw ? c.bn / 2 : c.bn;
+    const long tiles = (long)((M + c.bm - 1) / c.bm) * ((N + nt - 1) / nt);
+    const long rounds = (tiles + 255) / 256;
+    const double cost = (double)rounds * (c.bm + c.bn) * (sw ? 2.0 * nt / c.bn : 1.0);
+    if (best.bm == 0 || cost < best_cost * 0.97) { best = c; best_cost = cost; }
+  }
+  return best;
+}
+
+template <int EPI, bool SW, int BMT, int BNT>
+void launch_large(const GemmArgs& a, hipStream_t s) {
+  const int nt = SW ? BNT / 2 : BNT;
+  const int ntiles = ((a.M + BMT - 1) / BMT) * ((a.N + nt - 1) / nt);
+  const int grid = (ntiles + 7) / 8 * 8;
+  hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW, BMT, BNT>), dim3(grid), dim3(512), 0, s, a);
+}
+
 template <int EPI, bool SW>
 hipError_t launch_one(int dtype, const GemmArgs& a, hipStream_t s) {
-  const bool one_slot = !a.lora.enabled || SW || a.lora.slot_width % LBN == 0;
-  if (dtype == VFM_BF16 && a.M >= 1024 && one_slot) {
-    const int nt = SW ? LBN / 2 : LBN;
-    const int ntiles = ((a.M + LBM - 1) / LBM) * ((a.N + nt - 1) / nt);
-    const int grid = (ntiles + 7) / 8 * 8;
-    hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW>), dim3(grid), dim3(512), 0, s, a);
+  const LargeShape sh = large_shape(a.M, a.N, SW, a.lora.enabled ? a.lora.slot_width : 0);
+  const bool fits32 = (int64_t)a.M * a.ldx < ((int64_t)1 << 31) && (int64_t)a.N * a.K < ((int64_t)1 << 31);
+  if (dtype == VFM_BF16 && a.M >= 1024 && sh.bm > 0 && fits32) {
+    if (sh.bn == 256) launch_large<EPI, SW, 256, 256>(a, s);
+    else if (sh.bn == 192) launch_large<EPI, SW, 256, 192>(a, s);
+    else launch_large<EPI, SW, 256, 128>(a, s);
   } else if (dtype == VFM_BF16) {
     const int nt = SW ? BN / 2 : BN;
     const int grid = ((a.M + BM - 1) / BM) * ((a.N + nt - 1) / nt);
