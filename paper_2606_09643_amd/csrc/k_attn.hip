@@ -314,10 +314,13 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     float mx = NEG_BIG;
     // The key swizzle of row 16*ks + (lane & 15) does not depend on ks, so
     // every fragment address is a per-lane base plus a constant offset.
-    const bf16* kbase = &Ks[(lane & 15) * DH];
     // keep the fragment reads inside this loop: hoisting all of them out
-    // (they do not depend on the query group) needs ~2x the registers
-    asm volatile("" : "+v"(kbase));
+    // (they do not depend on the query group) needs ~2x the registers.  The
+    // offset, not the pointer, goes through the empty asm, so the compiler
+    // still knows the reads are LDS reads (ds_read, not flat loads).
+    int koff = (lane & 15) * DH;
+    asm volatile("" : "+v"(koff));
+    const bf16* kbase = Ks + koff;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       f32x4 a = {0.f, 0.f, 0.f, 0.f};
@@ -342,8 +345,9 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     f32x4 o[DH / 16];
 #pragma unroll
     for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const bf16* vbase = &Vt[(lane & 15) * VP + 4 * g];
-    asm volatile("" : "+v"(vbase));
+    int voff = (lane & 15) * VP + 4 * g;
+    asm volatile("" : "+v"(voff));
+    const bf16* vbase = Vt + voff;
 #pragma unroll
     for (int u = 0; u < NKS / 2; ++u) {
       f32x4 e0, e1;

@@ -65,3 +65,16 @@ def test_large_gemm_keeps_lds_dma_in_flight(all_asm):
 def test_no_packed_fp32(all_asm):
     for f, asm in all_asm.items():
         assert not re.search(r"\bv_pk_(add|mul|fma)_f32\b", asm), f
+
+
+def test_lds_reads_stay_lds(all_asm):
+    """LDS tiles are read with ds_* instructions: a pointer into LDS that the
+    compiler loses track of (e.g. passed through an asm statement) becomes a
+    generic pointer and every fragment read turns into a flat load through the
+    vector-memory pipeline."""
+    for f in ("k_attn.hip", "k_decode.hip", "k_segmented.hip", "k_rows.hip"):
+        for name, body in _kernels(all_asm[f]).items():
+            assert not re.search(r"^\s+flat_(load|store)", body, re.M), f"{f}: {name} uses flat memory ops"
+    for name, body in _kernels(all_asm["k_gemm.hip"]).items():
+        if "gemm_bf16_large_kernel" in name:
+            assert not re.search(r"^\s+flat_(load|store)", body, re.M), name
