@@ -34,22 +34,32 @@ __device__ inline void tile_rows(const Plan& pl, int bid, int& t, int& r0, int& 
 // ---------------------------------------------------------------------------
 template <int NP, int NSUB>
 __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
-  // One block per 64-row tile of one task; each wave owns 16 rows and every
-  // projection of the group, so the rows are read once for all of them.
-  int t, r0, r1;
-  tile_rows(pl, blockIdx.x, t, r0, r1);
+  // Two blocks per 64-row tile of one task, 32 rows each.  Wave w owns 16
+  // rows (w & 1) and half of K (w >> 1) for every projection of the group,
+  // so each row is read once for all of them; the two K halves are summed
+  // through LDS in a fixed order.
+  __shared__ f32x4 part[2][NP][NSUB][64];
+  __shared__ int s_task;
+  const int tile = blockIdx.x >> 1, half = blockIdx.x & 1;
+  const int t = block_tile_task(pl, tile, &s_task);
+  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE + half * 32;
+  const int r1 = min(pl.seg_row[t] + (tile - pl.rtile_off[t] + 1) * VFM_ROW_TILE, pl.seg_row[t + 1]);
+  if (r0 >= r1) return;                       // block-uniform: the tile's second half is empty
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rg = wave & 1, kh = wave >> 1;
   const int rank = min(a.rank[t], a.rpad) & ~7;
   const float sc = a.scale[t];
   const bf16* X = (const bf16*)a.X;
   bf16* U = (bf16*)a.U;
-  const int m = r0 + wave * 16 + (lane & 15);
+  const int m = r0 + rg * 16 + (lane & 15);
+  const int kmid = (a.K / 64) * 32;           // K halves on 32-column boundaries
+  const int kb = kh ? kmid : 0, ke = kh ? a.K : kmid;
   f32x4 acc[NP][NSUB];
 #pragma unroll
   for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
     for (int s2 = 0; s2 < NSUB; ++s2) acc[pp][s2] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (rank > 0 && r0 + wave * 16 < r1) {
+  if (rank > 0 && r0 + rg * 16 < r1) {
     const bf16* xrow = X + (int64_t)min(m, r1 - 1) * a.ldx + 8 * (lane >> 4);
     const bf16* arow[NP][NSUB];
     bool aon[NSUB];
@@ -63,7 +73,7 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
         arow[pp][s2] = At + (int64_t)min(s2 * 16 + (lane & 15), rank - 1) * a.K + 8 * (lane >> 4);
     }
 #pragma unroll 2
-    for (int k = 0; k < a.K; k += 32) {
+    for (int k = kb; k < ke; k += 32) {
       const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
 #pragma unroll
       for (int pp = 0; pp < NP; ++pp)
@@ -75,20 +85,34 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
         }
     }
   }
-  if (m < r1) {
+  if (kh == 1) {
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+      for (int s2 = 0; s2 < NSUB; ++s2) part[rg][pp][s2][lane] = acc[pp][s2];
+  }
+  __syncthreads();
+  if (kh == 0 && m < r1) {
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
       for (int s2 = 0; s2 < NSUB; ++s2) {
+        const f32x4 o2 = part[rg][pp][s2][lane];
         bf16x4 o;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[pp][s2][i] * sc);
+        for (int i = 0; i < 4; ++i) o[i] = (bf16)((acc[pp][s2][i] + o2[i]) * sc);
         *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[pp] + s2 * 16 + 4 * (lane >> 4)) = o;
       }
   }
 }
 
 __global__ __launch_bounds__(256) void shrink_f32_kernel(Plan pl, ShrinkArgs a) {
+  // One block per (row tile, projection).  K is walked in 32-column chunks
+  // staged in LDS (the tile's rows and the task's A rows); thread (row i,
+  // group g) accumulates rpad/4 outputs of row i from LDS.
+  constexpr int KC = 32;
+  __shared__ float xs[VFM_ROW_TILE][KC + 1];
+  __shared__ float as[VFM_MAX_RANK][KC + 1];
   int t, r0, r1;
   tile_rows(pl, blockIdx.x, t, r0, r1);
   const int p = blockIdx.y;
@@ -98,15 +122,36 @@ __global__ __launch_bounds__(256) void shrink_f32_kernel(Plan pl, ShrinkArgs a) 
   const float* At = rank > 0 ? (const float*)a.A[p][t] : nullptr;
   float* U = (float*)a.U;
   const int rows = r1 - r0;
-  for (int e = threadIdx.x; e < rows * a.rpad; e += 256) {
-    const int m = r0 + e / a.rpad, j = e % a.rpad;
-    float s = 0.f;
-    if (j < rank) {
-      const float* x = X + (int64_t)m * a.ldx;
-      const float* w = At + (int64_t)j * a.K;
-      for (int k = 0; k < a.K; ++k) s += x[k] * w[k];
+  const int i = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int jn = a.rpad / 4;                  // outputs per thread (8 or 16)
+  float acc[VFM_MAX_RANK / 4];
+#pragma unroll
+  for (int q = 0; q < VFM_MAX_RANK / 4; ++q) acc[q] = 0.f;
+  if (rank > 0) {
+    for (int k0 = 0; k0 < a.K; k0 += KC) {
+      for (int e = threadIdx.x; e < VFM_ROW_TILE * KC; e += 256) {
+        const int r = e / KC, k = e % KC;
+        xs[r][k] = r < rows ? X[(int64_t)(r0 + r) * a.ldx + k0 + k] : 0.f;
+      }
+      for (int e = threadIdx.x; e < a.rpad * KC; e += 256) {
+        const int j = e / KC, k = e % KC;
+        as[j][k] = j < rank ? At[(int64_t)j * a.K + k0 + k] : 0.f;
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int k = 0; k < KC; ++k) {
+        const float xv = xs[i][k];
+#pragma unroll
+        for (int q = 0; q < VFM_MAX_RANK / 4; ++q)
+          if (q < jn) acc[q] = fmaf(xv, as[g * jn + q][k], acc[q]);
+      }
+      __syncthreads();
     }
-    U[(int64_t)m * a.ldu + a.ucol[p] + j] = s * sc;
+  }
+  if (i < rows) {
+#pragma unroll
+    for (int q = 0; q < VFM_MAX_RANK / 4; ++q)
+      if (q < jn) U[(int64_t)(r0 + i) * a.ldu + a.ucol[p] + g * jn + q] = acc[q] * sc;
   }
 }
 
@@ -234,7 +279,7 @@ __global__ __launch_bounds__(256) void heads_f32_kernel(Plan pl, const float* __
 hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s) {
   if (pl.n_rtiles == 0 || a.n_proj == 0) return hipSuccess;
   if (dtype == VFM_BF16) {
-    dim3 grid(pl.n_rtiles);
+    dim3 grid(2 * pl.n_rtiles);
 #define SHR(NP_, NS_) hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
     if (a.rpad == 32) {
       if (a.n_proj == 1) SHR(1, 2); else if (a.n_proj == 2) SHR(2, 2); else SHR(3, 2);
