@@ -87,4 +87,4 @@ def pick_requests(pl, k=6):
     for c in cand:
         if int(c) not in out:
             out.append(int(c))
-    return out[:max(k, 6)]
+    return out[:k]

@@ -337,3 +337,54 @@ def test_layer_parity_long_prompts():
     worst = max(O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]) for p in range(batch.n_req))
     log(f"  max row rel err {worst:.3e}")
     assert worst < tol(w)
+
+
+@pytest.mark.parametrize("idx", [1, 3, 4, 5])
+def test_full_size_sampled(idx):
+    """Each remaining workload at its full batch, in the bench's launch
+    configuration: every layer's output on sampled requests against the
+    oracle run on that layer's GPU input, and, when every layer runs, every
+    request's head outputs.  The decoder workloads run their first two layers
+    (the kernels and launch shapes of all 32 are the same); decode also
+    checks the new K / V rows written to the cache."""
+    w = wl.WORKLOADS[idx]
+    n_layers = w.n_layers if w.family != "decoder" else 2
+    batch = wl.draw_batch(w)
+    model = R.Model(w, n_layers=n_layers)
+    inp = R.Inputs(w, batch)
+    kv = R.KVCache(w, batch, n_layers) if w.mode == "decode" else None
+    pb = R.make_batch(w, batch, model.heads, kv)
+    fwd = R.Forward(model, pb, inp, kv)
+    pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
+    reqs = pick_requests(pl, k=4 if idx == 4 else 6)
+    log(f"full-size workload {idx}: T={pb.T}, {n_layers} layers, sampled plan positions {reqs}")
+    fwd.embed()
+    torch.cuda.synchronize()
+    cu = pl["cu_seqlens"]
+    worst = 0.0
+    for li in range(n_layers):
+        x_in = fwd.x.double().cpu().numpy()
+        fwd.layer(li)
+        torch.cuda.synchronize()
+        got = fwd.x.double().cpu().numpy()
+        kvc = (kv.k[li], kv.v[li]) if kv is not None else None
+        res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_in, reqs,
+                                kv=kvc, kv_start=kv.kv_start if kv is not None else None)
+        for p in reqs:
+            worst = max(worst, O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]))
+            if kv is not None:
+                i = int(pl["order"][p])
+                slot = int(kv.kv_start[i] + batch.ctx[i])
+                assert O.row_rel_error(kv.k[li][slot].double().cpu().numpy()[None], res[p][1]) < tol(w)
+                assert O.row_rel_error(kv.v[li][slot].double().cpu().numpy()[None], res[p][2]) < tol(w)
+        log(f"  layer {li}: max row rel err so far {worst:.3e}")
+    assert worst < tol(w)
+    if model.heads is not None and n_layers == w.n_layers:
+        fwd.head()
+        torch.cuda.synchronize()
+        out = fwd.out.cpu().numpy()
+        ref = oracle_heads(w, model, pl, fwd.x.double().cpu().numpy(), model.heads.n_out)
+        off = pl["logit_off"]
+        hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
+        log(f"  head max rel err {hw:.3e}")
+        assert hw < tol(w)
