@@ -223,6 +223,9 @@ int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_
  * a4. Segmented LoRA on one projection: for every plan-order row m of task
  * t with rank_t > 0,  y[m, :] += scale_t * (x[m, :] A_{t,proj}^T) B_{t,proj}^T.
  *   x: device [T, d_in] (dtype), plan order.  y: device float32 [T, d_out].
+ *   d_in a multiple of 64, d_out a multiple of 4 (else VFM_ERR_SHAPE).
+ *   workspace: device, >= T * rpad * sizeof(dtype) bytes (rpad = 32 if
+ *   max_rank <= 32, else 64), 256-byte aligned.
  * ---------------------------------------------------------------------- */
 int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t d_out,
                    const vfm_lora_table* lora, const vfm_batch* batch, const void* x, float* y,

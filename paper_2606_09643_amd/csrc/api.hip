@@ -357,7 +357,7 @@ extern "C" int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t
   VFM_TRY(check_batch(batch, &pl));
   VFM_TRY(check_lora(lora, pl));
   if (!lora->A[proj]) return VFM_ERR_ARG;
-  if (d_in < 32 || d_in % 32 || d_out < 4 || d_out % 4) return VFM_ERR_SHAPE;
+  if (d_in < 64 || d_in % 64 || d_out < 4 || d_out % 4) return VFM_ERR_SHAPE;
   const int rpad = rpad_of(lora);
   if (rpad == 0) return VFM_OK;
   const size_t need = align_up((size_t)pl.T * rpad * elem_size(dtype));

@@ -32,75 +32,112 @@ __device__ inline void tile_rows(const Plan& pl, int bid, int& t, int& r0, int& 
 // ---------------------------------------------------------------------------
 // shrink: U[m, ucol + j] = s_t * X[m, :] . A_t[j, :]   (j < rpad, zero past r_t)
 // ---------------------------------------------------------------------------
+typedef const void __attribute__((address_space(1)))* gptr_t;
+typedef void __attribute__((address_space(3)))* lptr_t;
+__device__ __attribute__((aligned(16))) bf16 g_seg_zero[8];  // zero-initialised at load
+
+// A 16-byte global load the compiler does not track; the kernel's own vmcnt
+// waits cover it (loads complete in issue order).  Without this the
+// compiler waits for every outstanding load at the loop's back-edge.
+__device__ __forceinline__ void gload16_untracked(bf16x8& dst, const bf16* p) {
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
+}
+
 template <int NP, int NSUB>
 __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
-  // Two blocks per 64-row tile of one task, 32 rows each.  Wave w owns 16
-  // rows (w & 1) and half of K (w >> 1) for every projection of the group,
-  // so each row is read once for all of them; the two K halves are summed
-  // through LDS in a fixed order.
-  __shared__ f32x4 part[2][NP][NSUB][64];
-  __shared__ int s_task;
-  const int tile = blockIdx.x >> 1, half = blockIdx.x & 1;
-  const int t = block_tile_task(pl, tile, &s_task);
-  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE + half * 32;
-  const int r1 = min(pl.seg_row[t] + (tile - pl.rtile_off[t] + 1) * VFM_ROW_TILE, pl.seg_row[t + 1]);
-  if (r0 >= r1) return;                       // block-uniform: the tile's second half is empty
+  // One block per 64-row tile of one task; wave w owns 16 rows and every
+  // projection of the group, so each row is read once for all of them.  The
+  // task's A rows (shared by the 4 waves) go through an LDS ring of NST
+  // 64-column chunks fed by global_load_lds (rows past the rank come from a
+  // zero page); each wave's activation rows go through a register ring of
+  // the same depth, so NST - 1 chunks are in flight while one is consumed.
+  // LDS rows are 128 B with chunk swizzle kc ^ ((row >> 1) & 7).
+  constexpr int NST = 4;
+  constexpr int AR = NP * NSUB * 16;            // A rows per chunk
+  constexpr int ARND = AR * 8 / 256;            // 16-byte pieces per thread and chunk
+  constexpr int GRP = ARND + 2;                 // loads per lane and chunk
+  // one LDS object (the task slot sits past the ring): with a second one the
+  // compiler would wait for the ring's DMA before every fragment read
+  __shared__ __attribute__((aligned(16))) bf16 As[NST][AR * 64 + 8];
+  const int tile = blockIdx.x;
+  const int t = block_tile_task(pl, tile, reinterpret_cast<int*>(&As[NST - 1][AR * 64]));
+  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
+  const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rg = wave & 1, kh = wave >> 1;
   const int rank = min(a.rank[t], a.rpad) & ~7;
   const float sc = a.scale[t];
   const bf16* X = (const bf16*)a.X;
   bf16* U = (bf16*)a.U;
-  const int m = r0 + rg * 16 + (lane & 15);
-  const int kmid = (a.K / 64) * 32;           // K halves on 32-column boundaries
-  const int kb = kh ? kmid : 0, ke = kh ? a.K : kmid;
+  const int m = r0 + wave * 16 + (lane & 15);
   f32x4 acc[NP][NSUB];
 #pragma unroll
   for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
     for (int s2 = 0; s2 < NSUB; ++s2) acc[pp][s2] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (rank > 0 && r0 + rg * 16 < r1) {
+  if (rank > 0) {   // block-uniform
+    const bf16* asrc[ARND];
+    const int prow0 = wave * 8 + (lane >> 3);
+    const int kcl = (lane & 7) ^ ((prow0 >> 1) & 7);   // same for prow0 + 32 i
+#pragma unroll
+    for (int i = 0; i < ARND; ++i) {
+      const int row = prow0 + i * 32;                     // row = (pp*NSUB + s2)*16 + j
+      const int pp = row / (NSUB * 16), j = row % (NSUB * 16);
+      asrc[i] = j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
+    }
+    // rows past the tile's end read its last row (results discarded)
     const bf16* xrow = X + (int64_t)min(m, r1 - 1) * a.ldx + 8 * (lane >> 4);
-    const bf16* arow[NP][NSUB];
-    bool aon[NSUB];
+    const int nc = a.K / 64;
+    bf16x8 xr[NST][2];
+    // every chunk index past the end re-reads the last chunk, so each step
+    // issues the same GRP loads and one wait count holds throughout
+    auto issue = [&](int c, int st) {
+      const int cc = min(c, nc - 1);
 #pragma unroll
-    for (int s2 = 0; s2 < NSUB; ++s2) aon[s2] = s2 * 16 + (lane & 15) < rank;
+      for (int i = 0; i < ARND; ++i) {
+        const bf16* src = asrc[i] ? asrc[i] + cc * 64 : g_seg_zero;
+        __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(&As[st][(i * 4 + wave) * 512]), 16, 0, 0);
+      }
+      gload16_untracked(xr[st][0], xrow + cc * 64);
+      gload16_untracked(xr[st][1], xrow + cc * 64 + 32);
+    };
 #pragma unroll
-    for (int pp = 0; pp < NP; ++pp) {
-      const bf16* At = (const bf16*)a.A[pp][t];
+    for (int i = 0; i < NST - 1; ++i) issue(i, i);
+    for (int c0 = 0; c0 < nc; c0 += NST) {
 #pragma unroll
-      for (int s2 = 0; s2 < NSUB; ++s2)
-        arow[pp][s2] = At + (int64_t)min(s2 * 16 + (lane & 15), rank - 1) * a.K + 8 * (lane >> 4);
-    }
-#pragma unroll 2
-    for (int k = kb; k < ke; k += 32) {
-      const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
+      for (int j = 0; j < NST; ++j) {
+        const int c = c0 + j;
+        if (c >= nc) break;
+        // chunk c landed once at most (NST - 2) later groups are outstanding
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * GRP) : "memory");
+        asm volatile("" : "+v"(xr[j][0]), "+v"(xr[j][1]));   // uses stay below the wait
+        __builtin_amdgcn_s_barrier();     // every wave's part is in LDS; stage (c-1) is free
+        issue(c + NST - 1, (j + NST - 1) % NST);
+        const bf16* Ab = As[j];
+        const bf16x8 x0 = xr[j][0], x1 = xr[j][1];
 #pragma unroll
-      for (int pp = 0; pp < NP; ++pp)
+        for (int kk = 0; kk < 2; ++kk) {
+          const int kc = kk * 4 + (lane >> 4);
 #pragma unroll
-        for (int s2 = 0; s2 < NSUB; ++s2) {
-          bf16x8 af = *reinterpret_cast<const bf16x8*>(arow[pp][s2] + k);
-          if (!aon[s2]) af = bf16x8{};
-          acc[pp][s2] = mfma16(af, xf, acc[pp][s2]);
+          for (int pp = 0; pp < NP; ++pp)
+#pragma unroll
+            for (int s2 = 0; s2 < NSUB; ++s2) {
+              const int r = (pp * NSUB + s2) * 16 + (lane & 15);
+              const bf16x8 af = *reinterpret_cast<const bf16x8*>(Ab + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8));
+              acc[pp][s2] = mfma16(af, kk ? x1 : x0, acc[pp][s2]);
+            }
         }
+      }
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // nothing lands after the block ends
   }
-  if (kh == 1) {
-#pragma unroll
-    for (int pp = 0; pp < NP; ++pp)
-#pragma unroll
-      for (int s2 = 0; s2 < NSUB; ++s2) part[rg][pp][s2][lane] = acc[pp][s2];
-  }
-  __syncthreads();
-  if (kh == 0 && m < r1) {
+  if (m < r1) {
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
       for (int s2 = 0; s2 < NSUB; ++s2) {
-        const f32x4 o2 = part[rg][pp][s2][lane];
         bf16x4 o;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (bf16)((acc[pp][s2][i] + o2[i]) * sc);
+        for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[pp][s2][i] * sc);
         *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[pp] + s2 * 16 + 4 * (lane >> 4)) = o;
       }
   }
@@ -279,7 +316,7 @@ __global__ __launch_bounds__(256) void heads_f32_kernel(Plan pl, const float* __
 hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s) {
   if (pl.n_rtiles == 0 || a.n_proj == 0) return hipSuccess;
   if (dtype == VFM_BF16) {
-    dim3 grid(2 * pl.n_rtiles);
+    dim3 grid(pl.n_rtiles);
 #define SHR(NP_, NS_) hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
     if (a.rpad == 32) {
       if (a.n_proj == 1) SHR(1, 2); else if (a.n_proj == 2) SHR(2, 2); else SHR(3, 2);
