@@ -553,6 +553,118 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
   }
 }
 
+// bf16 variant with the next step's K / V loads in flight while the current
+// step is computed: a two-slot register ring filled by loads the compiler
+// does not track (so it does not wait for every load at the loop back-edge);
+// the kernel's own waits cover them, as loads complete in issue order.
+__device__ __forceinline__ void gload16_untracked(bf16x8& dst, const bf16* p) {
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
+}
+
+template <int DH, int UNR>
+__global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf16* __restrict__ qkv, int d,
+                                                               const bf16* __restrict__ kc,
+                                                               const bf16* __restrict__ vc,
+                                                               float* __restrict__ part, int nchunk,
+                                                               float scale_log2) {
+  constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
+  constexpr int NG = 256 / LPK;        // key streams per block
+  constexpr int STEP = UNR * NG;       // keys per step of the block
+  __shared__ float sm[NG], sl[NG];
+  __shared__ float so[NG][DH + 1];
+  const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int grp = tid / LPK, sub = tid % LPK;
+  const int R = pl.cu_seqlens[p];
+  const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
+  const int kbeg = c * DEC_CHUNK;
+  if (kbeg >= nkeys) return;                 // block-uniform
+  const int kend = min(kbeg + DEC_CHUNK, nkeys);
+  const int64_t base = (int64_t)pl.kv_start[p];
+  float q[8];
+  load8<bf16>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8, q);
+  float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
+  const bf16* kp = kc + base * d + h * DH + sub * 8;
+  const bf16* vp = vc + base * d + h * DH + sub * 8;
+  bf16x8 kb[2][UNR], vb[2][UNR];
+  // keys past the chunk re-read its last key (masked), so every step issues
+  // 2 * UNR loads and one wait count holds throughout
+  auto issue = [&](int slot, int k0) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int k = min(k0 + u * NG, kend - 1);
+      gload16_untracked(kb[slot][u], kp + (int64_t)k * d);
+      gload16_untracked(vb[slot][u], vp + (int64_t)k * d);
+    }
+  };
+  auto step = [&](int slot, int k0) {
+    float sc[UNR];
+    float smax = NEG_BIG;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += q[i] * (float)kb[slot][u][i];
+#pragma unroll
+      for (int w = LPK / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+      sc[u] = k0 + u * NG < kend ? s * scale_log2 : NEG_BIG;
+      smax = fmaxf(smax, sc[u]);
+    }
+    const float m_new = fmaxf(m_run, smax);
+    const float alpha = exp2f(m_run - m_new);
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] *= alpha;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const float e = k0 + u * NG < kend ? exp2f(sc[u] - m_new) : 0.f;
+      l_run += e;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] += e * (float)vb[slot][u][i];
+    }
+    m_run = m_new;
+  };
+  const int first = kbeg + grp;
+  // q is needed by the first step: take its (tracked) load's wait here,
+  // before the untracked K / V loads are in flight behind it
+#pragma unroll
+  for (int i = 0; i < 8; ++i) asm volatile("" ::"v"(q[i]));
+  if (first < kend) {
+    issue(0, first);
+    for (int k0 = first; k0 < kend; k0 += 2 * STEP) {
+      issue(1, k0 + STEP);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * UNR) : "memory");   // slot 0 has landed
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) asm volatile("" : "+v"(kb[0][u]), "+v"(vb[0][u]));
+      step(0, k0);
+      if (k0 + STEP >= kend) break;
+      issue(0, k0 + 2 * STEP);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * UNR) : "memory");   // slot 1 has landed
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) asm volatile("" : "+v"(kb[1][u]), "+v"(vb[1][u]));
+      step(1, k0 + STEP);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  if (sub == 0) { sm[grp] = m_run; sl[grp] = l_run; }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) so[grp][sub * 8 + i] = o[i];
+  __syncthreads();
+  if (tid < DH) {
+    float M = NEG_BIG;
+    for (int gq = 0; gq < NG; ++gq) M = fmaxf(M, sm[gq]);
+    float lsum = 0.f, acc = 0.f;
+    for (int gq = 0; gq < NG; ++gq) {
+      const float w = exp2f(sm[gq] - M);
+      lsum += sl[gq] * w;
+      acc += so[gq][tid] * w;
+    }
+    float* rec = part + (((int64_t)p * gridDim.x + h) * nchunk + c) * (DH + 2);
+    rec[2 + tid] = acc;
+    if (tid == 0) { rec[0] = M; rec[1] = lsum; }
+  }
+}
+
 template <typename T, int DH>
 __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const float* __restrict__ part,
                                                                int nchunk, int d, T* __restrict__ out) {
@@ -639,8 +751,12 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
     dim3 grid(H, pl.n_req, nchunk), gm(pl.n_req, H);
 #define DEC(TT, D_)                                                                                    \
   pi = prof_begin(VFM_PROF_ATTN, s);                                                                   \
-  hipLaunchKernelGGL((attn_decode_kernel<TT, D_, 4>), grid, dim3(256), 0, s, pl, (const TT*)qkv, d,   \
-                     (const TT*)k_cache, (const TT*)v_cache, part, nchunk, scale_log2);               \
+  if (dtype == VFM_BF16)                                                                               \
+    hipLaunchKernelGGL((attn_decode_bf16_kernel<D_, 4>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
+                       d, (const bf16*)k_cache, (const bf16*)v_cache, part, nchunk, scale_log2);     \
+  else                                                                                                 \
+    hipLaunchKernelGGL((attn_decode_kernel<float, D_, 4>), grid, dim3(256), 0, s, pl, (const float*)qkv, \
+                       d, (const float*)k_cache, (const float*)v_cache, part, nchunk, scale_log2);   \
   prof_end(pi, s);                                                                                     \
   pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
   hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
