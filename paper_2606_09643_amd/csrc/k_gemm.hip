@@ -182,6 +182,129 @@ __device__ __forceinline__ void epilogue_frags(const GemmArgs& a, int wrow0, int
   }
 }
 
+// Epilogue of the large-M kernel through LDS.  The MFMA fragments leave each
+// lane with 4 consecutive columns of 16 different rows, so direct stores are
+// 16 row pieces of 32 B (bf16) or 64 B (fp32) per instruction.  Here the
+// finished values (bias, activation applied) go into the idle operand LDS as
+// a row-major tile first, and the block then writes whole rows, 16 B per lane
+// with consecutive lanes on consecutive addresses.  16-byte chunk q of tile
+// row r sits at chunk q ^ (r & S), S + 1 the largest power of two (at most 8)
+// dividing the row's chunk count, which spreads the fragment writes of
+// consecutive rows over distinct banks.  The fp32 residual tile (4 B per
+// value) is done in two halves of rows.
+template <int QR>
+__device__ __forceinline__ int lds_chunk(int r, int q) {
+  constexpr int LOW = QR & -QR, S = (LOW < 8 ? LOW : 8) - 1;
+  return q ^ (r & S);
+}
+
+template <int EPI, bool SWIGLU, int BMT, int BNT, int FM, int FN>
+__device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m0, int n0, int wm, int wn,
+                                             int lane, int tid, const f32x4 (&acc)[FM][FN]) {
+  constexpr int NTH = 512, TM = BMT / 4, TN = BNT / 2;
+  constexpr int NC = SWIGLU ? BNT / 2 : BNT;        // output columns of the tile
+  const int g = lane >> 4;
+  __syncthreads();                                  // every wave is done with the operand stages
+  if (EPI != EPI_RESID) {
+    constexpr int QR = NC / 8;                      // 16-byte chunks per row (bf16)
+    static_assert(QR % 4 == 0, "row chunks");
+    static_assert(BMT * NC * 2 <= 2 * (BMT + BNT) * BK * 2, "tile fits the operand LDS");
+    bf16* T = reinterpret_cast<bf16*>(lds);
+    if (SWIGLU) {
+#pragma unroll
+      for (int mi = 0; mi < FM; ++mi) {
+        const int r = wm * TM + mi * 16 + (lane & 15);
+#pragma unroll
+        for (int ni = 0; ni < FN; ni += 2) {
+          const int sub = wn * TN / 16 + ni;
+          const int j = (sub >> 1) * 16 + 4 * g;     // tile column of the lane's 4 values
+          bf16x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = (bf16)(silu_f(acc[mi][ni][e]) * acc[mi][ni + 1][e]);
+          *reinterpret_cast<bf16x4*>(T + r * NC + lds_chunk<QR>(r, j >> 3) * 8 + (j & 4)) = o;
+        }
+      }
+    } else {
+      const bf16* bias = (const bf16*)a.bias;
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int j = wn * TN + ni * 16 + 4 * g;
+        float bv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bias && n0 + j < a.N) {
+          const bf16x4 bb = *reinterpret_cast<const bf16x4*>(bias + n0 + j);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) bv[e] = (float)bb[e];
+        }
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi) {
+          const int r = wm * TM + mi * 16 + (lane & 15);
+          bf16x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float v = acc[mi][ni][e] + bv[e];
+            o[e] = (bf16)(EPI == EPI_GELU ? gelu_erf_fast(v) : v);
+          }
+          *reinterpret_cast<bf16x4*>(T + r * NC + lds_chunk<QR>(r, j >> 3) * 8 + (j & 4)) = o;
+        }
+      }
+    }
+    __syncthreads();
+    bf16* out = (bf16*)a.out;
+#pragma unroll 4
+    for (int e = tid; e < BMT * QR; e += NTH) {
+      const int r = e / QR, q = e % QR;
+      const int m = m0 + r, n = n0 + q * 8;
+      const bf16x8 v = *reinterpret_cast<const bf16x8*>(T + r * NC + lds_chunk<QR>(r, q) * 8);
+      if (m < a.M && n < a.N) *reinterpret_cast<bf16x8*>(out + (int64_t)m * a.ldo + n) = v;
+    }
+    return;
+  }
+  // fp32 residual: x[m, n] += acc + bias, rows of each half staged as fp32
+  constexpr int HR = BMT / 2;                       // rows per half
+  constexpr int QR = NC / 4;                        // 16-byte chunks per row (fp32)
+  static_assert(QR % 4 == 0, "row chunks");
+  static_assert(HR * NC * 4 <= 2 * (BMT + BNT) * BK * 2, "half tile fits the operand LDS");
+  float* T = reinterpret_cast<float*>(lds);
+  const bf16* bias = (const bf16*)a.bias;
+  float* x = (float*)a.out;
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    if ((wm >> 1) == half) {                        // waves wm = 2 half, 2 half + 1 own these rows
+#pragma unroll
+      for (int ni = 0; ni < FN; ++ni) {
+        const int j = wn * TN + ni * 16 + 4 * g;
+        float bv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bias && n0 + j < a.N) {
+          const bf16x4 bb = *reinterpret_cast<const bf16x4*>(bias + n0 + j);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) bv[e] = (float)bb[e];
+        }
+#pragma unroll
+        for (int mi = 0; mi < FM; ++mi) {
+          const int r = (wm & 1) * TM + mi * 16 + (lane & 15);   // row within the half
+          const float4 o = make_float4(acc[mi][ni][0] + bv[0], acc[mi][ni][1] + bv[1],
+                                       acc[mi][ni][2] + bv[2], acc[mi][ni][3] + bv[3]);
+          *reinterpret_cast<float4*>(T + r * NC + lds_chunk<QR>(r, j >> 2) * 4) = o;
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int e = tid; e < HR * QR; e += NTH) {
+      const int r = e / QR, q = e % QR;
+      const int m = m0 + half * HR + r, n = n0 + q * 4;
+      if (m < a.M && n < a.N) {
+        const float4 v = *reinterpret_cast<const float4*>(T + r * NC + lds_chunk<QR>(r, q) * 4);
+        float4* dst = reinterpret_cast<float4*>(x + (int64_t)m * a.ldo + n);
+        float4 o = *dst;
+        o.x += v.x; o.y += v.y; o.z += v.z; o.w += v.w;
+        *dst = o;
+      }
+    }
+    if (half == 0) __syncthreads();                 // the second half reuses the buffer
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Large-M bf16 GEMM: BMT x BNT x 64 block tile (256 rows, 128 / 192 / 256
 // columns), 8 waves (4 along M x 2 along N) of (BMT/4) x (BNT/2), operands
@@ -306,6 +429,18 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
 #pragma unroll
     for (int ni = 0; ni < FN; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  auto issue_bb = [&](int e) {
+    bf16* As = smem + (e & 1) * (SA + SB);
+    bf16* Bs = As + SA;
+    const int k0 = e * BK;
+#pragma unroll
+    for (int i = 0; i < ACH; ++i)
+      __builtin_amdgcn_global_load_lds((gptr_t)(X + xoff[i] + k0), (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < BCH; ++i)
+      __builtin_amdgcn_global_load_lds((gptr_t)(wbase(i) + woff[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16,
+                                       0, 0);
+  };
   auto issue = [&](int e) {
     bf16* As = smem + (e & 1) * (SA + SB);
     bf16* Bs = As + SA;
@@ -404,16 +539,29 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // Waits are explicit: vmcnt(0) makes this wave's LDS-bound loads land, the
   // raw s_barrier then makes every wave's loads visible.  (A full
   // __syncthreads would add a fence the loop does not need.)
+  // The backbone K steps run in a loop of their own (its loads are plain
+  // strided tiles), then the LoRA steps; the loop that mixes both kinds of
+  // issue costs the backbone loop about a tenth of its speed.
   issue(0);
   __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0)
   __builtin_amdgcn_s_barrier();
-  for (int e = 0; e < nsteps; ++e) {
-    if (e + 1 < nsteps) issue(e + 1);  // the other stage: every wave left it at the last barrier
+  for (int e = 0; e + 1 < nk; ++e) {
+    issue_bb(e + 1);                   // the other stage: every wave left it at the last barrier
     compute(e);
     __builtin_amdgcn_s_waitcnt(0xF70);
     __builtin_amdgcn_s_barrier();
   }
-  epilogue_frags<EPI, SWIGLU, FM, FN>(a, m0 + wm * TM, n0, wn * TN, lane, acc);
+  for (int e = nk - 1; e < nsteps; ++e) {
+    if (e + 1 < nsteps) issue(e + 1);
+    compute(e);
+    __builtin_amdgcn_s_waitcnt(0xF70);
+    __builtin_amdgcn_s_barrier();
+  }
+  if (EPI == EPI_STORE)
+    epilogue_lds<EPI, SWIGLU, BMT, BNT, FM, FN>(a, reinterpret_cast<char*>(smem), m0, n0, wm, wn, lane, tid,
+                                                 acc);
+  else
+    epilogue_frags<EPI, SWIGLU, FM, FN>(a, m0 + wm * TM, n0, wn * TN, lane, acc);
 }
 
 // ---------------------------------------------------------------------------
