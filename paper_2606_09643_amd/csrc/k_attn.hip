@@ -321,6 +321,10 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     int koff = (lane & 15) * DH;
     asm volatile("" : "+v"(koff));
     const bf16* kbase = Ks + koff;
+    // Scores stay unscaled here (the scale is positive, so the max commutes
+    // with it); only sub-tiles that can hold a masked key pay for the mask:
+    // the padded tail past L, and for causal rows the sub-tiles that reach
+    // past the group's first query.
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
       f32x4 a = {0.f, 0.f, 0.f, 0.f};
@@ -330,17 +334,24 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
             kbase + ks * 16 * DH + kswz<DH>(lane & 15, s2 * 4 + g) * 8);
         a = mfma16(kf, qf[s2], a);
       }
+      const bool full = (ks + 1) * 16 <= L && (!CAUSAL || (ks + 1) * 16 <= qg * 16 + 1);
+      if (full) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = ks * 16 + 4 * g + i;
-        const bool masked = key >= L || (CAUSAL && key > qi);
-        a[i] = masked ? -INFINITY : a[i] * scale_log2;
-        mx = fmaxf(mx, a[i]);
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, a[i]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = ks * 16 + 4 * g + i;
+          const bool masked = key >= L || (CAUSAL && key > qi);
+          a[i] = masked ? -INFINITY : a[i];
+          mx = fmaxf(mx, a[i]);
+        }
       }
       st[ks] = a;
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mxs = -mx * scale_log2;   // exp2(s * scale - max * scale), one fma per score
     float lsum = 0.f;
     f32x4 o[DH / 16];
 #pragma unroll
@@ -353,8 +364,8 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
       f32x4 e0, e1;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        e0[i] = fast_exp2(st[2 * u][i] - mx);
-        e1[i] = fast_exp2(st[2 * u + 1][i] - mx);
+        e0[i] = fast_exp2(fmaf(st[2 * u][i], scale_log2, mxs));
+        e1[i] = fast_exp2(fmaf(st[2 * u + 1][i], scale_log2, mxs));
         lsum += e0[i] + e1[i];
       }
       const bf16x8 pf = pack8(e0, e1);

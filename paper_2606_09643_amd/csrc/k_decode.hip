@@ -360,7 +360,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   for (int c = 0; c < 4; ++c) {
     float y = g4[c];
     if (swiglu) y = y / (1.f + __expf(-y)) * u4[c];
-    else if (a.epi == EPI_GELU) y = gelu_erf_fast(y);
+    else if (a.epi == EPI_GELU) y = gelu_fast(y);
     o[c] = (bf16)y;
   }
   *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + n) = o;

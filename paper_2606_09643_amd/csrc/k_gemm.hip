@@ -174,7 +174,7 @@ __device__ __forceinline__ void epilogue_frags(const GemmArgs& a, int wrow0, int
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float v = acc[mi][ni][r] + bv[ni][r];
-          o[r] = (bf16)(EPI == EPI_GELU ? gelu_erf_fast(v) : v);
+          o[r] = (bf16)(EPI == EPI_GELU ? gelu_fast(v) : v);
         }
         *reinterpret_cast<bf16x4*>(row + n) = o;
       }
@@ -242,7 +242,7 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float v = acc[mi][ni][e] + bv[e];
-            o[e] = (bf16)(EPI == EPI_GELU ? gelu_erf_fast(v) : v);
+            o[e] = (bf16)(EPI == EPI_GELU ? gelu_fast(v) : v);
           }
           *reinterpret_cast<bf16x4*>(T + r * NC + lds_chunk<QR>(r, j >> 3) * 8 + (j & 4)) = o;
         }

@@ -78,3 +78,38 @@ def test_lds_reads_stay_lds(all_asm):
     for name, body in _kernels(all_asm["k_gemm.hip"]).items():
         if "gemm_bf16_large_kernel" in name:
             assert not re.search(r"^\s+flat_(load|store)", body, re.M), name
+
+
+def test_gelu_polynomial_error_bound():
+    """The bf16 GELU epilogue's polynomial (coefficients read from the kernel
+    header, evaluated in float32 in the kernel's order) stays within its
+    stated error against the exact erf form: <= 1e-4 for |x| <= 4 and
+    5.4e-5 |x| beyond (the fit error at the clamp point plus the normal tail)."""
+    import numpy as np
+    from scipy.special import erf
+    src = open(os.path.join(CSRC, "vfm_internal.h")).read()
+    body = src[src.index("__device__ inline float gelu_fast"):]
+    body = body[:body.index("\n}\n")]
+    lits = [float(v) for v in re.findall(r"(-?\d+\.\d*(?:e-?\d+)?)f", body)]
+    assert len(lits) == 2 + 8 + 1, lits      # clamp +-4, the 8 coefficients, 0.5
+    assert lits[0] == -4.0 and lits[1] == 4.0 and lits[-1] == 0.5
+    coef = [np.float32(c) for c in lits[2:-1]]  # highest power first, as evaluated
+    x = np.linspace(-12, 12, 2_400_001).astype(np.float32)
+    t = np.clip(x, np.float32(-4), np.float32(4))
+    u = t * t
+    p = np.full_like(x, coef[0])
+    for c in coef[1:]:
+        p = (p * u + c).astype(np.float32)
+    g = (x * (p * t + np.float32(0.5))).astype(np.float32)
+    xd = x.astype(np.float64)
+    ref = 0.5 * xd * (1.0 + erf(xd / np.sqrt(2.0)))
+    err = np.abs(g - ref)
+    inner = np.abs(x) <= 4
+    assert err[inner].max() <= 1e-4, err[inner].max()
+    assert np.all(err[~inner] <= 5.4e-5 * np.abs(xd[~inner]))
+    # GELU(0) = 0 exactly, and odd symmetry of the polynomial part
+    x0 = np.zeros(1, np.float32)
+    p0 = np.full_like(x0, coef[0])
+    for c in coef[1:]:
+        p0 = (p0 * x0 * x0 + c).astype(np.float32)
+    assert float((x0 * (p0 * x0 + np.float32(0.5)))[0]) == 0.0
