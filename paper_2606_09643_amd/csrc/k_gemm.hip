@@ -49,6 +49,21 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
 typedef const void __attribute__((address_space(1)))* gptr_t;
 typedef void __attribute__((address_space(3)))* lptr_t;
 
+// Vector loads the compiler does not track: the kernel's own vmcnt waits
+// cover them (vector memory operations complete in issue order), and an
+// empty asm with the register as operand pins its first use after the wait.
+__device__ __forceinline__ void gload_b32_untracked(int& dst, const int32_t* p) {
+  asm volatile("global_load_dword %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
+}
+__device__ __forceinline__ void gload_b64_untracked(uint64_t& dst, const void* const* p) {
+  asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
+}
+__device__ __forceinline__ const void* uniform_ptr(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(((uint64_t)hi << 32) | lo);
+}
+
 // Fused per-task LoRA expand for one wave's FM x FN fragment grid (shared by
 // both bf16 kernels).  wrow0 / wcol0: the wave's first row / first B-tile row.
 template <int FM, int FN, bool SWIGLU>
@@ -226,25 +241,31 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
       }
     } else {
       const bf16* bias = (const bf16*)a.bias;
+      f32x4 bv[FN];
 #pragma unroll
       for (int ni = 0; ni < FN; ++ni) {
+        bv[ni] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int j = wn * TN + ni * 16 + 4 * g;
-        float bv[4] = {0.f, 0.f, 0.f, 0.f};
         if (bias && n0 + j < a.N) {
           const bf16x4 bb = *reinterpret_cast<const bf16x4*>(bias + n0 + j);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) bv[e] = (float)bb[e];
+          for (int e = 0; e < 4; ++e) bv[ni][e] = (float)bb[e];
         }
+      }
 #pragma unroll
-        for (int mi = 0; mi < FM; ++mi) {
-          const int r = wm * TM + mi * 16 + (lane & 15);
+      for (int mi = 0; mi < FM; ++mi) {
+        const int r = wm * TM + mi * 16 + (lane & 15);
+        bf16* row = T + r * NC + (g & 1) * 4;
+#pragma unroll
+        for (int ni = 0; ni < FN; ++ni) {
+          const int q = (wn * TN + ni * 16) / 8 + (g >> 1);   // 16-byte chunk of the lane's 4 values
           bf16x4 o;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float v = acc[mi][ni][e] + bv[e];
+            const float v = acc[mi][ni][e] + bv[ni][e];
             o[e] = (bf16)(EPI == EPI_GELU ? gelu_fast(v) : v);
           }
-          *reinterpret_cast<bf16x4*>(T + r * NC + lds_chunk<QR>(r, j >> 3) * 8 + (j & 4)) = o;
+          *reinterpret_cast<bf16x4*>(row + lds_chunk<QR>(r, q) * 8) = o;
         }
       }
     }
@@ -326,7 +347,6 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
 // ---------------------------------------------------------------------------
 constexpr int LGM = 4;
 
-__device__ __attribute__((aligned(16))) bf16 g_zero_page[8];  // zero-initialised at load
 
 template <int EPI, bool SWIGLU, int BMT, int BNT>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
@@ -385,43 +405,77 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     return (const bf16*)a.W;
   };
 
-  // The LoRA steps of this tile: every task t0..t1 with rows in
-  // [m0, m0 + BMT) (rows are sorted by task), `parts` steps each.  A task of
-  // rank 0 gets an all-zero B tile.  (Kept out of LDS on purpose: a second
-  // LDS object makes the compiler wait for the in-flight DMA before every
-  // fragment read.)
+  // LoRA steps.  Rows are sorted by task, so the tile's rows form runs of
+  // one task each.  The task ids of the tile's rows arrive with the first
+  // operand DMA (RPL per lane); ballots of the rows that start a run then
+  // list the runs, so a task without rows in the tile (an id absent from the
+  // batch included) costs no step.  Each run gets `parts` extra K steps whose
+  // A tile is U (the run's rows, the slot's columns; other rows zero) and B
+  // tile B_t of the run's task (zero past its rank).  A run's rank and B
+  // pointers are loaded while the previous run's first step is issued, with
+  // vector loads the compiler does not track (the loop's vmcnt waits cover
+  // them), so no step waits on a dependent load.  (Kept out of LDS on
+  // purpose: a second LDS object makes the compiler wait for the in-flight
+  // DMA before every fragment read.)
   const int nk = a.K / BK;
-  int t0 = 0, nlora = 0;
+  constexpr int RPL = BMT / 64;                    // tile rows per lane
+  static_assert(BMT % 64 == 0, "rows per lane");
   const int parts = (SWIGLU && L.max_rank > 32) ? 2 : 1;
+  const int rpad = L.max_rank > 32 ? 64 : 32;
+  // ranks <= 32 outside SwiGLU fill only the first 32 columns of a LoRA step
+  const bool half = !SWIGLU && rpad == 32;
+  bool live = false;
   if (L.enabled) {
-    bool live;
     if (SWIGLU) live = L.B[0] != nullptr || L.B[1] != nullptr;
     else live = L.B[min(n0 / L.slot_width, 2)] != nullptr;
-    if (live) {
-      t0 = L.row_task[m0];
-      nlora = (L.row_task[min(m0 + BMT, a.M) - 1] - t0 + 1) * parts;
-    }
   }
-  const int nsteps = nk + nlora;
-  // metadata of the first two tasks, loaded up front so the LoRA steps of a
-  // tile with one or two tasks issue their DMA without dependent loads
-  int c_r0 = 0, c_r1 = 0, c_a0 = 0, c_a1 = 0, c_e0 = 0, c_e1 = 0;
-  const bf16 *c_b00 = nullptr, *c_b01 = nullptr, *c_b10 = nullptr, *c_b11 = nullptr;
-  if (nlora > 0) {
-    const int slot = SWIGLU ? 0 : min(n0 / L.slot_width, 2);
-    c_r0 = min(L.rank[t0], L.max_rank) & ~7;
-    c_a0 = L.seg_row[t0];
-    c_e0 = L.seg_row[t0 + 1];
-    c_b00 = L.B[slot] ? (const bf16*)L.B[slot][t0] : nullptr;
-    if (SWIGLU) c_b01 = L.B[1] ? (const bf16*)L.B[1][t0] : nullptr;
-    if (nlora > parts) {
-      c_r1 = min(L.rank[t0 + 1], L.max_rank) & ~7;
-      c_a1 = c_e0;
-      c_e1 = L.seg_row[t0 + 2];
-      c_b10 = L.B[slot] ? (const bf16*)L.B[slot][t0 + 1] : nullptr;
-      if (SWIGLU) c_b11 = L.B[1] ? (const bf16*)L.B[1][t0 + 1] : nullptr;
-    }
+  const int lslot = SWIGLU ? 0 : min(n0 / L.slot_width, 2);
+  int rt[RPL];                                     // task of tile row RPL * lane + j
+#pragma unroll
+  for (int j = 0; j < RPL; ++j) {
+    rt[j] = 0;
+    if (live) gload_b32_untracked(rt[j], L.row_task + min(m0 + RPL * lane + j, a.M - 1));
   }
+  uint64_t rstart[RPL];                            // bit l of rstart[j]: row RPL*l + j starts a run
+  int nlora = 0, nsteps = nk;
+  // issue-side run state (wave-uniform): current run rows [cs, ce) of the
+  // tile, its rank and B pointers; the next run's rank / pointers in flight
+  int cs = 0, ce = 0, cr = 0;
+  const bf16 *cb0 = nullptr, *cb1 = nullptr;
+  int v_nr = 0;
+  uint64_t v_nb0 = 0, v_nb1 = 0;
+  auto first_start_ge = [&](int r) -> int {        // first run start at tile row >= r, else BMT
+    int best = BMT;
+#pragma unroll
+    for (int j = 0; j < RPL; ++j) {
+      const int lmin = r <= j ? 0 : (r - j + RPL - 1) / RPL;
+      if (lmin < 64) {
+        const uint64_t m = rstart[j] & (~0ull << lmin);
+        if (m) best = min(best, RPL * (int)__builtin_ctzll(m) + j);
+      }
+    }
+    return best;
+  };
+  // Run metadata flows through a two-deep pipeline of untracked loads: when
+  // run k becomes current, the task id of run k+2's first row and the rank /
+  // B pointers of run k+1 (whose task id arrived one run earlier) are issued.
+  int v_nt = 0;                                    // task of the run after next (in flight)
+  auto load_task = [&](int r) { gload_b32_untracked(v_nt, L.row_task + m0 + r); };
+  auto prefetch_run = [&](int t) {                 // rank and B pointers of task t
+    gload_b32_untracked(v_nr, L.rank + t);
+    if (SWIGLU) {
+      if (L.B[0]) gload_b64_untracked(v_nb0, L.B[0] + t);
+      if (L.B[1]) gload_b64_untracked(v_nb1, L.B[1] + t);
+    } else if (L.B[lslot]) {
+      gload_b64_untracked(v_nb0, L.B[lslot] + t);
+    }
+  };
+  auto take_run = [&]() {                          // the prefetched values become current
+    asm volatile("" : "+v"(v_nr), "+v"(v_nb0), "+v"(v_nb1));
+    cr = min(__builtin_amdgcn_readfirstlane(v_nr), L.max_rank) & ~7;
+    cb0 = (const bf16*)uniform_ptr(v_nb0);
+    cb1 = (const bf16*)uniform_ptr(v_nb1);
+  };
 
   f32x4 acc[FM][FN];
 #pragma unroll
@@ -441,6 +495,13 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       __builtin_amdgcn_global_load_lds((gptr_t)(wbase(i) + woff[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16,
                                        0, 0);
   };
+  // A LoRA-step chunk: lanes with data DMA it, the others write zeros into
+  // their own 16-byte LDS slot (a shared zero page read by every CU would
+  // funnel those loads into one L2 line).  The step's wait covers both.
+  auto dma_or_zero = [&](bool on, const bf16* src, bf16* dst) {
+    if (on) __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)dst, 16, 0, 0);
+    else *reinterpret_cast<bf16x8*>(dst + lane * 8) = bf16x8{};
+  };
   auto issue = [&](int e) {
     bf16* As = smem + (e & 1) * (SA + SB);
     bf16* Bs = As + SA;
@@ -455,18 +516,24 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
                                          0, 0);
       return;
     }
-    const int t = t0 + (e - nk) / parts, part = (e - nk) % parts;
-    const int ci = t - t0;
-    const bool cached = ci < 2;
-    const int r = ci == 0 ? c_r0 : (ci == 1 ? c_r1 : (min(L.rank[t], L.max_rank) & ~7));
-    const int s0 = ci == 0 ? c_a0 : (ci == 1 ? c_a1 : L.seg_row[t]);
-    const int s1 = ci == 0 ? c_e0 : (ci == 1 ? c_e1 : L.seg_row[t + 1]);
+    const int step = e - nk, part = step % parts;
+    if (part == 0) {                               // the next run becomes current
+      if (step > 0) cs = ce;
+      ce = first_start_ge(cs + 1);
+      take_run();
+      if (ce < BMT) {                              // run k+1 starts at ce
+        asm volatile("" : "+v"(v_nt));
+        prefetch_run(__builtin_amdgcn_readfirstlane(v_nt));
+        const int ce2 = first_start_ge(ce + 1);
+        if (ce2 < BMT) load_task(ce2);             // run k+2
+      }
+    }
+    const int r = cr;
+    const int s0 = m0 + cs, s1 = min(m0 + ce, a.M);
     const bf16* U = (const bf16*)L.U;
-    const bf16* zero = g_zero_page;
-    // A: the task's rows of U; 64 columns starting at the step's slot.  Only
-    // columns of slots the shrink wrote are read (the rest come from the zero
-    // page), so stale workspace bytes never meet a zero of B.
-    const int rpad = L.max_rank > 32 ? 64 : 32;
+    // A: the run's rows of U; 64 columns starting at the step's slot.  Only
+    // columns of slots the shrink wrote are read (the rest are zeroed in LDS),
+    // so stale workspace bytes never meet a zero of B.
     int ucolA;
     bool colA;
     if (SWIGLU && rpad == 32) {
@@ -476,20 +543,22 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       ucolA = L.ucol[part];
       colA = L.B[part] != nullptr;
     } else {
-      ucolA = L.ucol[min(n0 / L.slot_width, 2)];
+      ucolA = L.ucol[lslot];
       colA = kc0 * 8 < rpad;
     }
+    // with `half`, columns 32..63 are neither loaded nor read
+    const bool skip = half && kc0 >= 4;
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
       const int m = m0 + row0 + i * RSTEP;
-      const bf16* src = (colA && m >= s0 && m < s1 && m < a.M) ? U + (int64_t)m * L.ldu + ucolA + kc0 * 8 : zero;
-      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+      const bool on = colA && m >= s0 && m < s1;
+      if (!skip) dma_or_zero(on, U + (int64_t)m * L.ldu + ucolA + kc0 * 8, As + (i * NW + wave) * 512);
     }
     // B: B_t rows of this block's output columns, zero past the rank
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
       const int row = row0 + i * RSTEP;
-      const bf16* src = zero;
+      const bf16* src = nullptr;
       if (SWIGLU) {
         const int sub = row >> 4, which = sub & 1;
         const int j = n0 + (sub >> 1) * 16 + (row & 15);
@@ -497,28 +566,22 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
         bool on;
         if (L.max_rank > 32) on = (which == part) && L.B[part] != nullptr;
         else { on = which ? (kc0 >= 4) : (kc0 < 4); kc = which ? kc0 - 4 : kc0; }
-        if (on && kc * 8 < r && j < a.N && L.B[which] != nullptr) {
-          const bf16* Bt = cached ? (ci == 0 ? (which ? c_b01 : c_b00) : (which ? c_b11 : c_b10))
-                                  : (const bf16*)L.B[which][t];
-          src = Bt + (int64_t)j * r + kc * 8;
-        }
+        const bf16* Bt = which ? cb1 : cb0;
+        if (on && kc * 8 < r && j < a.N && Bt != nullptr) src = Bt + (int64_t)j * r + kc * 8;
       } else {
-        const int n = n0 + row;
-        const int slot = min(n / L.slot_width, 2);
-        const int nrow = n - slot * L.slot_width;
-        if (kc0 * 8 < r && n < a.N && nrow < L.slot_width && L.B[slot] != nullptr) {
-          const bf16* Bt = cached ? (ci == 0 ? c_b00 : c_b10) : (const bf16*)L.B[slot][t];
-          src = Bt + (int64_t)nrow * r + kc0 * 8;
-        }
+        const int nrow = n0 + row - lslot * L.slot_width;
+        if (kc0 * 8 < r && n0 + row < a.N && nrow < L.slot_width && cb0 != nullptr)
+          src = cb0 + (int64_t)nrow * r + kc0 * 8;
       }
-      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(Bs + (i * NW + wave) * 512), 16, 0, 0);
+      if (!skip) dma_or_zero(src != nullptr, src, Bs + (i * NW + wave) * 512);
     }
   };
-  auto compute = [&](int e) {
+  auto compute = [&](int e, bool first_half_only) {
     const bf16* As = smem + (e & 1) * (SA + SB);
     const bf16* Bs = As + SA;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
+      if (kk == 1 && first_half_only) break;
       const int kc = kk * 4 + (lane >> 4);
       bf16x8 wf[FN];
 #pragma unroll
@@ -542,19 +605,40 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // The backbone K steps run in a loop of their own (its loads are plain
   // strided tiles), then the LoRA steps; the loop that mixes both kinds of
   // issue costs the backbone loop about a tenth of its speed.
-  issue(0);
-  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0)
+  issue_bb(0);
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): step 0 and the tile's row tasks
   __builtin_amdgcn_s_barrier();
+  if (live) {
+#pragma unroll
+    for (int j = 0; j < RPL; ++j) asm volatile("" : "+v"(rt[j]));   // first use after the wait
+    int prev = __shfl_up(rt[RPL - 1], 1, 64);
+    if (lane == 0) prev = -1;
+    asm volatile("" : "+v"(prev));
+#pragma unroll
+    for (int j = 0; j < RPL; ++j) {
+      const int before = j == 0 ? prev : rt[j - 1];
+      rstart[j] = __ballot(rt[j] != before);
+    }
+    int nruns = 0;
+#pragma unroll
+    for (int j = 0; j < RPL; ++j) nruns += __builtin_popcountll(rstart[j]);
+    nlora = nruns * parts;
+    nsteps = nk + nlora;
+    prefetch_run(__builtin_amdgcn_readfirstlane(rt[0]));   // the first run (row 0: lane 0, j = 0)
+    const int c1 = first_start_ge(1);
+    if (c1 < BMT) load_task(c1);                   // task of the second run
+  }
+  if (nk < 2) __builtin_amdgcn_s_waitcnt(0xF70);   // no backbone step covers them
   for (int e = 0; e + 1 < nk; ++e) {
     issue_bb(e + 1);                   // the other stage: every wave left it at the last barrier
-    compute(e);
+    compute(e, false);
     __builtin_amdgcn_s_waitcnt(0xF70);
     __builtin_amdgcn_s_barrier();
   }
   for (int e = nk - 1; e < nsteps; ++e) {
     if (e + 1 < nsteps) issue(e + 1);
-    compute(e);
-    __builtin_amdgcn_s_waitcnt(0xF70);
+    compute(e, half && e >= nk);
+    __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0): DMA and zero writes done
     __builtin_amdgcn_s_barrier();
   }
   if (EPI == EPI_STORE)
