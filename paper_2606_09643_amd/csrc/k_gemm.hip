@@ -49,21 +49,6 @@ __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const 
 typedef const void __attribute__((address_space(1)))* gptr_t;
 typedef void __attribute__((address_space(3)))* lptr_t;
 
-// Vector loads the compiler does not track: the kernel's own vmcnt waits
-// cover them (vector memory operations complete in issue order), and an
-// empty asm with the register as operand pins its first use after the wait.
-__device__ __forceinline__ void gload_b32_untracked(int& dst, const int32_t* p) {
-  asm volatile("global_load_dword %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
-}
-__device__ __forceinline__ void gload_b64_untracked(uint64_t& dst, const void* const* p) {
-  asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
-}
-__device__ __forceinline__ const void* uniform_ptr(uint64_t v) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return (const void*)(((uint64_t)hi << 32) | lo);
-}
-
 // Fused per-task LoRA expand for one wave's FM x FN fragment grid (shared by
 // both bf16 kernels).  wrow0 / wcol0: the wave's first row / first B-tile row.
 template <int FM, int FN, bool SWIGLU>
@@ -412,11 +397,11 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // batch included) costs no step.  Each run gets `parts` extra K steps whose
   // A tile is U (the run's rows, the slot's columns; other rows zero) and B
   // tile B_t of the run's task (zero past its rank).  A run's rank and B
-  // pointers are loaded while the previous run's first step is issued, with
-  // vector loads the compiler does not track (the loop's vmcnt waits cover
-  // them), so no step waits on a dependent load.  (Kept out of LDS on
-  // purpose: a second LDS object makes the compiler wait for the in-flight
-  // DMA before every fragment read.)
+  // pointers are loaded while the previous run's first step is issued; their
+  // first use is a step later, after that step's vmcnt(0), so no step waits
+  // on a dependent load.  (Kept out of LDS on purpose: a second LDS object
+  // makes the compiler wait for the in-flight DMA before every fragment
+  // read.)
   const int nk = a.K / BK;
   constexpr int RPL = BMT / 64;                    // tile rows per lane
   static_assert(BMT % 64 == 0, "rows per lane");
@@ -432,10 +417,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   const int lslot = SWIGLU ? 0 : min(n0 / L.slot_width, 2);
   int rt[RPL];                                     // task of tile row RPL * lane + j
 #pragma unroll
-  for (int j = 0; j < RPL; ++j) {
-    rt[j] = 0;
-    if (live) gload_b32_untracked(rt[j], L.row_task + min(m0 + RPL * lane + j, a.M - 1));
-  }
+  for (int j = 0; j < RPL; ++j) rt[j] = live ? L.row_task[min(m0 + RPL * lane + j, a.M - 1)] : 0;
   uint64_t rstart[RPL];                            // bit l of rstart[j]: row RPL*l + j starts a run
   int nlora = 0, nsteps = nk;
   // issue-side run state (wave-uniform): current run rows [cs, ce) of the
@@ -443,7 +425,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   int cs = 0, ce = 0, cr = 0;
   const bf16 *cb0 = nullptr, *cb1 = nullptr;
   int v_nr = 0;
-  uint64_t v_nb0 = 0, v_nb1 = 0;
+  const void* v_nb0 = nullptr;
+  const void* v_nb1 = nullptr;
   auto first_start_ge = [&](int r) -> int {        // first run start at tile row >= r, else BMT
     int best = BMT;
 #pragma unroll
@@ -456,25 +439,24 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     }
     return best;
   };
-  // Run metadata flows through a two-deep pipeline of untracked loads: when
-  // run k becomes current, the task id of run k+2's first row and the rank /
-  // B pointers of run k+1 (whose task id arrived one run earlier) are issued.
-  int v_nt = 0;                                    // task of the run after next (in flight)
-  auto load_task = [&](int r) { gload_b32_untracked(v_nt, L.row_task + m0 + r); };
+  // Run metadata flows through a two-deep pipeline: when run k becomes
+  // current, the task id of run k+2's first row and the rank / B pointers of
+  // run k+1 (whose task id arrived one run earlier) are loaded.
+  int v_nt = 0;                                    // task of the run after next
+  auto load_task = [&](int r) { v_nt = L.row_task[m0 + r]; };
   auto prefetch_run = [&](int t) {                 // rank and B pointers of task t
-    gload_b32_untracked(v_nr, L.rank + t);
+    v_nr = L.rank[t];
     if (SWIGLU) {
-      if (L.B[0]) gload_b64_untracked(v_nb0, L.B[0] + t);
-      if (L.B[1]) gload_b64_untracked(v_nb1, L.B[1] + t);
+      if (L.B[0]) v_nb0 = L.B[0][t];
+      if (L.B[1]) v_nb1 = L.B[1][t];
     } else if (L.B[lslot]) {
-      gload_b64_untracked(v_nb0, L.B[lslot] + t);
+      v_nb0 = L.B[lslot][t];
     }
   };
   auto take_run = [&]() {                          // the prefetched values become current
-    asm volatile("" : "+v"(v_nr), "+v"(v_nb0), "+v"(v_nb1));
-    cr = min(__builtin_amdgcn_readfirstlane(v_nr), L.max_rank) & ~7;
-    cb0 = (const bf16*)uniform_ptr(v_nb0);
-    cb1 = (const bf16*)uniform_ptr(v_nb1);
+    cr = min(v_nr, L.max_rank) & ~7;
+    cb0 = (const bf16*)v_nb0;
+    cb1 = (const bf16*)v_nb1;
   };
 
   f32x4 acc[FM][FN];
@@ -522,8 +504,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       ce = first_start_ge(cs + 1);
       take_run();
       if (ce < BMT) {                              // run k+1 starts at ce
-        asm volatile("" : "+v"(v_nt));
-        prefetch_run(__builtin_amdgcn_readfirstlane(v_nt));
+        prefetch_run(v_nt);
         const int ce2 = first_start_ge(ce + 1);
         if (ce2 < BMT) load_task(ce2);             // run k+2
       }
@@ -609,11 +590,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): step 0 and the tile's row tasks
   __builtin_amdgcn_s_barrier();
   if (live) {
-#pragma unroll
-    for (int j = 0; j < RPL; ++j) asm volatile("" : "+v"(rt[j]));   // first use after the wait
     int prev = __shfl_up(rt[RPL - 1], 1, 64);
     if (lane == 0) prev = -1;
-    asm volatile("" : "+v"(prev));
 #pragma unroll
     for (int j = 0; j < RPL; ++j) {
       const int before = j == 0 ? prev : rt[j - 1];

@@ -339,6 +339,35 @@ def test_layer_parity_long_prompts():
     assert worst < tol(w)
 
 
+def test_large_gemm_many_task_runs():
+    """Large-batch projections (T >= 1024 rows) where each 256-row tile holds
+    many short requests of different tasks, with task ids absent from the
+    batch between them and ranks 0 / 8 / 16 mixed: the tile's LoRA steps
+    must visit exactly the task runs present (up to ~20 per tile here) and
+    no others.  Decoder layer, 0.1 adapters, every request checked."""
+    rng = np.random.default_rng(7)
+    n = 96
+    present = np.sort(rng.choice(64, size=40, replace=False))   # 24 task ids absent
+    task_id = rng.choice(present, size=n)
+    seq_len = 1 + (np.arange(n) * 7) % 25
+    ranks = np.array([8 * (t % 3) for t in range(64)], np.int32)
+    case = dict(task_id=task_id.tolist(), seq_len=seq_len.tolist())
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(4, n_layers=1, b_std=0.1, ranks=ranks, case=case)
+    assert pb.T >= 1024, pb.T                      # the large-tile GEMM path
+    log(f"layer workload 4, {n} short requests over {len(present)} tasks, T={pb.T}")
+    fwd.embed()
+    x_in = fwd.x.double().cpu().numpy()
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    res = oracle_layer_rows(w, oracle_weights(model.layers[0]), model.adapters[0], pl, x_in,
+                            range(batch.n_req))
+    cu = pl["cu_seqlens"]
+    worst = max(O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]) for p in range(batch.n_req))
+    log(f"  max row rel err {worst:.3e}")
+    assert worst < tol(w)
+
+
 @pytest.mark.parametrize("idx", [1, 3, 4, 5])
 def test_full_size_sampled(idx):
     """Each remaining workload at its full batch, in the bench's launch
