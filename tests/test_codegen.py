@@ -113,3 +113,61 @@ def test_gelu_polynomial_error_bound():
     for c in coef[1:]:
         p0 = (p0 * x0 * x0 + c).astype(np.float32)
     assert float((x0 * (p0 * x0 + np.float32(0.5)))[0]) == 0.0
+
+
+def _regs(op):
+    """Registers named by an operand: v5 -> {5}, v[4:7] -> {4..7} (VGPRs only)."""
+    m = re.fullmatch(r"v(\d+)", op)
+    if m:
+        return {int(m.group(1))}
+    m = re.fullmatch(r"v\[(\d+):(\d+)\]", op)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    return set()
+
+
+def test_untracked_loads_not_touched_before_their_wait(all_asm):
+    """Loads issued from inline asm are invisible to the compiler's wait
+    insertion: the kernel's own s_waitcnt vmcnt must come before anything
+    reads (or overwrites) their destination registers.  A register copy
+    placed between such a load and its wait (for instance to carry the value
+    around a loop) would read the register before the data landed.  The scan
+    follows each kernel's instructions in program order, keeping the vector
+    memory operations in flight; vmcnt(N) retires all but the last N."""
+    vmem = re.compile(r"^(global_|buffer_|flat_|scratch_)")
+    checked = 0
+    for f, asm in all_asm.items():
+        for name, body in _kernels(asm).items():
+            inflight = []                                 # per VMEM op: its register set if untracked, else None
+            in_asm = False
+            for raw in body.splitlines():
+                t = raw.strip()
+                if t.startswith(";;#ASMSTART"):
+                    in_asm = True
+                    continue
+                if t.startswith(";;#ASMEND"):
+                    in_asm = False
+                    continue
+                l = t.split(";")[0].strip()
+                if not l or l.endswith(":") or l.startswith("."):
+                    continue
+                mnem, _, rest = l.partition(" ")
+                ops = [o.strip() for o in rest.split(",")] if rest else []
+                if mnem == "s_waitcnt":
+                    m = re.search(r"vmcnt\((\d+)\)", rest)
+                    if m:
+                        n = int(m.group(1))
+                        inflight = inflight[len(inflight) - n:] if n else []
+                    continue
+                if not in_asm:
+                    used = set().union(*(_regs(o) for o in ops)) if ops else set()
+                    for regs in inflight:
+                        if regs is not None:
+                            assert not (used & regs), f"{f}: {name}: '{l}' touches an in-flight untracked load"
+                if vmem.match(mnem):
+                    if in_asm and mnem.startswith("global_load") and ops:
+                        inflight.append(_regs(ops[0]))
+                        checked += 1
+                    else:
+                        inflight.append(None)
+    assert checked > 0
