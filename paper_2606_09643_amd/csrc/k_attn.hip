@@ -481,7 +481,7 @@ __device__ inline void load8<float>(const float* p, float (&v)[8]) {
 // (the usual rescaling of partial softmax sums by 2^(m_c - m)).
 // Inside a block, each group of LPK lanes walks one key stream; every step
 // issues the K and V loads of UNR keys of the stream before any is used.
-constexpr int DEC_CHUNK = 256;
+constexpr int DEC_CHUNK = 512;
 
 template <typename T, int DH, int UNR>
 __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __restrict__ qkv, int d,
