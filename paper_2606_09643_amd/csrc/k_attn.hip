@@ -97,6 +97,23 @@ __device__ __forceinline__ int kswz(int r, int kc) {
   return DH == 64 ? (kc ^ ((r >> 1) & 7)) : (kc ^ (r & 15));
 }
 
+// Short-sequence kernel: score sub-tiles 2u and 2u+1 take the keys of the
+// 32-key block u in the order that leaves each lane, after S^T = K Q^T, with
+// 8 consecutive keys across the pair (row x of the even sub-tile is key
+// 32u + 8(x >> 2) + (x & 3), of the odd one 4 keys further), so the P^T
+// operand's keys are contiguous and each V^T fragment is one 16-byte read.
+// The K rows' chunk swizzle is a bijection of the bits that differ among the
+// 16 rows one fragment read touches (row & 3 and (row >> 3) & 3), so those
+// reads stay bank-conflict free.
+template <int DH>
+__device__ __forceinline__ int sswz(int r, int kc) {
+  return DH == 64 ? (kc ^ (((r >> 1) & 1) | (((r >> 3) & 3) << 1)))
+                  : (kc ^ ((r & 3) | (((r >> 3) & 3) << 2)));
+}
+__device__ __forceinline__ int pair_key(int ks, int x) {  // key of row x of sub-tile ks
+  return (ks >> 1) * 32 + 8 * (x >> 2) + (x & 3) + 4 * (ks & 1);
+}
+
 // ---------------------------------------------------------------------------
 // Prefill attention, bf16, MFMA.
 // ---------------------------------------------------------------------------
@@ -278,7 +295,7 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
-      if (c < LMAX * CH) *reinterpret_cast<bf16x8*>(&Ks[key * DH + kswz<DH>(key, ch) * 8]) = kr[i];
+      if (c < LMAX * CH) *reinterpret_cast<bf16x8*>(&Ks[key * DH + sswz<DH>(key, ch) * 8]) = kr[i];
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
@@ -322,28 +339,38 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     asm volatile("" : "+v"(koff));
     const bf16* kbase = Ks + koff;
     // Scores stay unscaled here (the scale is positive, so the max commutes
-    // with it); only sub-tiles that can hold a masked key pay for the mask:
-    // the padded tail past L, and for causal rows the sub-tiles that reach
-    // past the group's first query.
+    // with it); only key pairs that can hold a masked key pay for the mask:
+    // the padded tail past L, and for causal rows the pairs that reach past
+    // the group's first query.  Lane (x = lane & 15, g) of sub-tile ks holds
+    // keys pair_key(ks, 4g + i), i < 4, of query x.
+    const int x = lane & 15;
+    const int ke = pair_key(0, x), ko = pair_key(1, x);   // rows of the even / odd sub-tile of pair 0
+    // key pairs below nfull hold no masked key for any query of the group;
+    // in the others, keys >= lim are masked for this lane's query (lim is
+    // made opaque per group so the compares are not hoisted out of the loop
+    // as dozens of lane masks held in scalar registers)
+    const int nfull = (CAUSAL ? min(L, qg * 16 + 1) : L) >> 5;
+    int lim = CAUSAL ? min(L, qi + 1) : L;
+    asm volatile("" : "+v"(lim));
+    int koff_e = ke * DH, koff_o = ko * DH;
+    asm volatile("" : "+v"(koff_e), "+v"(koff_o));
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
+      const int row0 = (ks & 1) ? ko : ke;
+      const bf16* kb = Ks + ((ks & 1) ? koff_o : koff_e) + (ks >> 1) * 32 * DH;
       f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s2 = 0; s2 < DH / 32; ++s2) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-            kbase + ks * 16 * DH + kswz<DH>(lane & 15, s2 * 4 + g) * 8);
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + sswz<DH>(row0, s2 * 4 + g) * 8);
         a = mfma16(kf, qf[s2], a);
       }
-      const bool full = (ks + 1) * 16 <= L && (!CAUSAL || (ks + 1) * 16 <= qg * 16 + 1);
-      if (full) {
+      if ((ks >> 1) < nfull) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) mx = fmaxf(mx, a[i]);
       } else {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = ks * 16 + 4 * g + i;
-          const bool masked = key >= L || (CAUSAL && key > qi);
-          a[i] = masked ? -INFINITY : a[i];
+          a[i] = pair_key(ks, 4 * g + i) >= lim ? -INFINITY : a[i];
           mx = fmaxf(mx, a[i]);
         }
       }
@@ -356,7 +383,7 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     f32x4 o[DH / 16];
 #pragma unroll
     for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    int voff = (lane & 15) * VP + 4 * g;
+    int voff = (lane & 15) * VP + 8 * g;
     asm volatile("" : "+v"(voff));
     const bf16* vbase = Vt + voff;
 #pragma unroll
@@ -371,10 +398,8 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
       const bf16x8 pf = pack8(e0, e1);
 #pragma unroll
       for (int ds = 0; ds < DH / 16; ++ds) {
-        const bf16* vrow = vbase + ds * 16 * VP + 32 * u;
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-        o[ds] = mfma16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pf, o[ds]);
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vbase + ds * 16 * VP + 32 * u);
+        o[ds] = mfma16(vf, pf, o[ds]);
       }
     }
     lsum += __shfl_xor(lsum, 16, 64);
