@@ -34,20 +34,31 @@ template <> __device__ inline void store4<bf16>(bf16* p, float4 v) {
 }
 
 // Normalise one fp32 row held by one wave; MAXI = max float4 chunks per lane.
+// For narrow rows (MAXI <= 8) the gain / shift loads are issued with the
+// row's loads, so their latency overlaps the row's instead of following the
+// two reductions; wide rows load them last (registers).
 template <typename TW, int MAXI>
 __device__ inline void norm_row_regs(const float* xr, int d, const TW* g, const TW* b, int kind,
                                      float eps, float4 (&v)[MAXI]) {
   const int lane = threadIdx.x & 63;
   const int nch = d >> 2;
-  float sum = 0.f;
+  constexpr bool EARLY = MAXI <= 8;
+  float4 gg[EARLY ? MAXI : 1], bb[EARLY ? MAXI : 1];
 #pragma unroll
   for (int i = 0; i < MAXI; ++i) {
     const int c = lane + 64 * i;
     if (c < nch) {
       v[i] = *reinterpret_cast<const float4*>(xr + 4 * c);
-      sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+      if (EARLY) {
+        gg[EARLY ? i : 0] = load4<TW>(g + 4 * c);
+        bb[EARLY ? i : 0] = b ? load4<TW>(b + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
   }
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXI; ++i)
+    if (lane + 64 * i < nch) sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   float mean = 0.f;
   if (kind == VFM_NORM_LAYER) mean = wave_sum(sum) / (float)d;
   float sq = 0.f;
@@ -55,8 +66,8 @@ __device__ inline void norm_row_regs(const float* xr, int d, const TW* g, const 
   for (int i = 0; i < MAXI; ++i) {
     const int c = lane + 64 * i;
     if (c < nch) {
-      const float a = v[i].x - mean, bb = v[i].y - mean, cc = v[i].z - mean, dd = v[i].w - mean;
-      sq += (a * a + bb * bb) + (cc * cc + dd * dd);
+      const float a = v[i].x - mean, b2 = v[i].y - mean, cc = v[i].z - mean, dd = v[i].w - mean;
+      sq += (a * a + b2 * b2) + (cc * cc + dd * dd);
     }
   }
   const float rstd = rsqrtf(wave_sum(sq) / (float)d + eps);
@@ -64,13 +75,18 @@ __device__ inline void norm_row_regs(const float* xr, int d, const TW* g, const 
   for (int i = 0; i < MAXI; ++i) {
     const int c = lane + 64 * i;
     if (c < nch) {
-      const float4 gg = load4<TW>(g + 4 * c);
-      float4 bb = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (b) bb = load4<TW>(b + 4 * c);
-      v[i].x = (v[i].x - mean) * rstd * gg.x + bb.x;
-      v[i].y = (v[i].y - mean) * rstd * gg.y + bb.y;
-      v[i].z = (v[i].z - mean) * rstd * gg.z + bb.z;
-      v[i].w = (v[i].w - mean) * rstd * gg.w + bb.w;
+      float4 g4, b4;
+      if (EARLY) {
+        g4 = gg[EARLY ? i : 0];
+        b4 = bb[EARLY ? i : 0];
+      } else {
+        g4 = load4<TW>(g + 4 * c);
+        b4 = b ? load4<TW>(b + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      v[i].x = (v[i].x - mean) * rstd * g4.x + b4.x;
+      v[i].y = (v[i].y - mean) * rstd * g4.y + b4.y;
+      v[i].z = (v[i].z - mean) * rstd * g4.z + b4.z;
+      v[i].w = (v[i].w - mean) * rstd * g4.w + b4.w;
     }
   }
 }
