@@ -115,14 +115,25 @@ __device__ __forceinline__ int pair_key(int ks, int x) {  // key of row x of sub
 }
 
 // ---------------------------------------------------------------------------
-// Prefill attention, bf16, MFMA.
+// Prefill attention, bf16, MFMA: one block = 64 queries of one request and
+// one head, 4 waves x 16 queries, online softmax over 64-key blocks.  K (rows
+// swizzled) and V^T (through 8x8 register transposes) of a key block are
+// staged in LDS; the next block's K / V are loaded into registers while the
+// current one is computed.  Score sub-tiles take the keys of each 32-key pair
+// in the pair_key order, so a lane's P^T keys are contiguous and each V^T
+// fragment is one 16-byte read.  Causal: a wave skips key blocks entirely
+// past its queries and masks only the block on its diagonal.
 // ---------------------------------------------------------------------------
 template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                                 int d, bf16* __restrict__ out,
                                                                 float scale_log2) {
-  constexpr int VP = 64 + 8;   // padded LDS row of V^T
-  __shared__ __attribute__((aligned(16))) bf16 Ks[64 * DH];   // swizzled rows (kswz)
+  constexpr int KB = 64;          // keys per block step
+  constexpr int CH = DH / 8;      // 16-byte chunks per key row
+  constexpr int VP = KB + 8;      // V^T row stride (bf16): 36 dwords, conflict-free 16-byte reads
+  constexpr int KPT = KB * CH / 256;          // K chunks per thread
+  constexpr int VTILES = (KB / 8) * CH;       // 8x8 V tiles per key block (<= 256)
+  __shared__ __attribute__((aligned(16))) bf16 Ks[KB * DH];
   __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
   const int b = blockIdx.x, h = blockIdx.y;
   const int p = upper_index(pl.qblk_off, pl.n_req + 1, b);
@@ -133,99 +144,125 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
   const int g = lane >> 4;
   const int qi = q0 + wave * 16 + (lane & 15);  // this lane's query (B-operand column)
   const int64_t ld = 3 * (int64_t)d;
+  const bf16* base = qkv + (int64_t)R * ld + h * DH;
 
   bf16x8 qf[DH / 32];
   {
-    const bf16* qrow = qkv + (int64_t)(R + min(qi, L - 1)) * ld + h * DH + 8 * g;
+    const bf16* qrow = base + (int64_t)min(qi, L - 1) * ld + 8 * g;
 #pragma unroll
-    for (int s = 0; s < DH / 32; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(qrow + s * 32);
+    for (int s2 = 0; s2 < DH / 32; ++s2) qf[s2] = *reinterpret_cast<const bf16x8*>(qrow + s2 * 32);
   }
   f32x4 o[DH / 16];
 #pragma unroll
   for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = NEG_BIG, l_run = 0.f;
 
-  const int kend = CAUSAL ? min(L, q0 + 64) : L;
-  for (int kb = 0; kb < kend; kb += 64) {
-    // stage K (swizzled rows) and V^T into LDS; rows past the request are
-    // zero.  All of a thread's loads are issued before its first store.
-    constexpr int CH = DH / 8;            // 16-byte chunks per key row
-    constexpr int PT = 64 * CH / 256;     // chunks per thread (2 or 4)
-    bf16x8 kv[PT], vv[PT];
+  // staging registers of one key block
+  bf16x8 kr[KPT], vr[8];
+  auto load = [&](int kb) {
 #pragma unroll
-    for (int i = 0; i < PT; ++i) {
+    for (int i = 0; i < KPT; ++i) {
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
-      kv[i] = bf16x8{};
-      vv[i] = bf16x8{};
-      if (kb + key < L) {
-        const bf16* src = qkv + (int64_t)(R + kb + key) * ld + h * DH + ch * 8;
-        kv[i] = *reinterpret_cast<const bf16x8*>(src + d);
-        vv[i] = *reinterpret_cast<const bf16x8*>(src + 2 * d);
+      kr[i] = bf16x8{};
+      if (kb + key < L) kr[i] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + key) * ld + d + ch * 8);
+    }
+    if (tid < VTILES) {
+      const int k8 = (tid / CH) * 8, d8 = (tid % CH) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        vr[e] = bf16x8{};
+        if (kb + k8 + e < L) vr[e] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + k8 + e) * ld + 2 * d + d8);
       }
     }
+  };
+  auto store = [&]() {
 #pragma unroll
-    for (int i = 0; i < PT; ++i) {
+    for (int i = 0; i < KPT; ++i) {
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
-      *reinterpret_cast<bf16x8*>(&Ks[key * DH + kswz<DH>(key, ch) * 8]) = kv[i];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(ch * 8 + e) * VP + key] = vv[i][e];
+      *reinterpret_cast<bf16x8*>(&Ks[key * DH + sswz<DH>(key, ch) * 8]) = kr[i];
     }
-    __syncthreads();
+    if (tid < VTILES) {
+      const int k8 = (tid / CH) * 8, d8 = (tid % CH) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        bf16x8 col;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) col[e] = vr[e][j];
+        *reinterpret_cast<bf16x8*>(&Vt[(d8 + j) * VP + k8]) = col;
+      }
+    }
+  };
 
-    f32x4 st[4];
+  const int kend = CAUSAL ? min(L, q0 + 64) : L;
+  const int x = lane & 15;
+  const int ke = pair_key(0, x), ko = pair_key(1, x);
+  int koff_e = ke * DH, koff_o = ko * DH;
+  int voff = x * VP + 8 * g;
+  asm volatile("" : "+v"(koff_e), "+v"(koff_o), "+v"(voff));
+  const int wq0 = q0 + wave * 16;                 // the wave's first query
+  int lim = CAUSAL ? min(L, qi + 1) : L;          // keys >= lim are masked for this lane
+
+  load(0);
+  store();
+  __syncthreads();
+  for (int kb = 0; kb < kend; kb += KB) {
+    const bool more = kb + KB < kend;
+    if (more) load(kb + KB);                      // in flight during this block's compute
+    // keys of this block past the wave's last query (causal) or past L are all masked
+    if (!CAUSAL || kb <= wq0 + 15) {
+      f32x4 st[4];
+      float mb = NEG_BIG;
+      const bool full = kb + KB <= L && (!CAUSAL || kb + KB <= wq0 + 1);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      st[ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int ks = 0; ks < 4; ++ks) {
+        const int row0 = (ks & 1) ? ko : ke;
+        const bf16* kp = Ks + ((ks & 1) ? koff_o : koff_e) + (ks >> 1) * 32 * DH;
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < DH / 32; ++s) {
-        const int r = ks * 16 + (lane & 15);
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[r * DH + kswz<DH>(r, s * 4 + g) * 8]);
-        st[ks] = mfma16(kf, qf[s], st[ks]);
+        for (int s2 = 0; s2 < DH / 32; ++s2) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kp + sswz<DH>(row0, s2 * 4 + g) * 8);
+          a = mfma16(kf, qf[s2], a);
+        }
+        if (!full) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) a[i] = kb + pair_key(ks, 4 * g + i) >= lim ? -INFINITY : a[i];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mb = fmaxf(mb, a[i]);
+        st[ks] = a;
       }
+      mb = fmaxf(mb, __shfl_xor(mb, 16, 64));
+      mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
+      const float m_new = fmaxf(m_run, mb * scale_log2);
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      float lsum = 0.f;
+#pragma unroll
+      for (int i = 0; i < DH / 16; ++i) o[i] *= alpha;
+      const bf16* vb = Vt + voff;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        f32x4 e0, e1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          e0[i] = fast_exp2(fmaf(st[2 * u][i], scale_log2, -m_new));
+          e1[i] = fast_exp2(fmaf(st[2 * u + 1][i], scale_log2, -m_new));
+          lsum += e0[i] + e1[i];
+        }
+        const bf16x8 pf = pack8(e0, e1);
+#pragma unroll
+        for (int ds = 0; ds < DH / 16; ++ds) {
+          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + ds * 16 * VP + 32 * u);
+          o[ds] = mfma16(vf, pf, o[ds]);
+        }
+      }
+      l_run = l_run * alpha + lsum;
     }
-    // scale, mask, block max
-    float mb = NEG_BIG;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kb + ks * 16 + 4 * g + i;
-        float v = st[ks][i] * scale_log2;
-        const bool masked = key >= L || (CAUSAL && key > qi);
-        v = masked ? -INFINITY : v;
-        st[ks][i] = v;
-        mb = fmaxf(mb, v);
-      }
-    mb = fmaxf(mb, __shfl_xor(mb, 16, 64));
-    mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
-    const float m_new = fmaxf(m_run, mb);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
-    float lsum = 0.f;
-    bf16x8 pf[2];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float e = fast_exp2(st[ks][i] - m_new);
-        lsum += e;
-        pf[ks >> 1][(ks & 1) * 4 + i] = (bf16)e;
-      }
-    l_run = l_run * alpha + lsum;
-#pragma unroll
-    for (int i = 0; i < DH / 16; ++i) o[i] *= alpha;
-    // O^T += V^T P^T over two 32-key steps
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-#pragma unroll
-      for (int ds = 0; ds < DH / 16; ++ds) {
-        const bf16* vrow = &Vt[(ds * 16 + (lane & 15)) * VP + 32 * u + 4 * g];
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-        o[ds] = mfma16(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7), pf[u], o[ds]);
-      }
+    __syncthreads();                              // every wave is done with this block's K / V^T
+    if (more) {
+      store();
+      __syncthreads();
     }
-    __syncthreads();
   }
   l_run += __shfl_xor(l_run, 16, 64);
   l_run += __shfl_xor(l_run, 32, 64);
