@@ -136,7 +136,8 @@ def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
         if kv is None:
             return None
         c, s0 = int(batch.ctx[i]), int(kv.kv_start[i])
-        return (np64(kv.k[li][s0:s0 + c]), np64(kv.v[li][s0:s0 + c]))
+        kr, vr = kv.rows(li, s0, c)
+        return (np64(kr), np64(vr))
 
     def run_layer(Wn, li, i, kvp):
         p = int(inv[i])

@@ -206,9 +206,11 @@ int vfm_embed_forward(const vfm_cfg* cfg, const vfm_batch* batch, int32_t mode, 
  * a2-a10. One backbone layer over the whole mixed batch, in place on x.
  *   x: device float32 [T, d], plan order (residual stream).
  *   lora: NULL for the bare backbone.
- *   k_cache, v_cache: device [kv_slots, d] (dtype), rotated keys; used when
- *     cfg->attn is VFM_ATTN_DECODE (required) or VFM_ATTN_CAUSAL (optional,
- *     NULL to skip): each row's K/V is written at slot kv_start + pos.
+ *   k_cache, v_cache: device [n_heads, kv_slots, head_dim] (dtype), head-major,
+ *     rotated keys; used when cfg->attn is VFM_ATTN_DECODE (required) or
+ *     VFM_ATTN_CAUSAL (optional, NULL to skip): each row's K/V is written at
+ *     slot kv_start + pos of every head.  Head-major keeps one head's keys
+ *     of a request contiguous, which is what decode attention streams.
  *   workspace: device, >= vfm_workspace_size bytes, 256-byte aligned.
  * Per layer: h = Norm1(x); [q|k|v] = h W_qkv^T + b (+ per-task LoRA);
  * RoPE; attention per request; x += attn W_o^T + b_o (+ LoRA_o);

@@ -328,8 +328,8 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
     VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta, s));
   // a6: attention per request (and the KV-cache write)
   // (timed per kernel inside the launcher)
-  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, base + ws.aws, ws.z - ws.aws,
-                           max_keys, s));
+  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, base + ws.aws,
+                           ws.z - ws.aws, max_keys, s));
   // a7: output projection + LoRA_o + residual
   VFM_TRY(project(VFM_PROF_GEMM_O, attn, d, w->w_o, nullptr, w->b_o, d, EPI_RESID, x, d, {VFM_O}, d));
   // a8: pre-norm 2

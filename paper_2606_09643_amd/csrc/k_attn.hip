@@ -17,6 +17,7 @@
 // 16 lanes stream the request's cached keys, 16 bytes per lane per key row,
 // each group with its own running max / sum / output, merged through LDS.
 #include <algorithm>
+#include <type_traits>
 
 #include "vfm_internal.h"
 
@@ -31,6 +32,21 @@ constexpr float LOG2E = 1.4426950408889634f;
 // 2^x for the softmax, where x <= 0 after the max subtraction: the hardware
 // v_exp_f32 directly (no range reduction needed; -inf gives 0).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+// Sum over aligned groups of N lanes (N = 8 or 16) with DPP moves, which
+// stay in the VALU: quad swaps, then the 8-lane and 16-lane mirrors pair
+// each half with the other.
+template <int N>
+__device__ __forceinline__ float key_row_sum(float s) {
+  static_assert(N == 8 || N == 16, "8 or 16 lanes per key row");
+  auto dpp = [](float v, auto ctrl) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), decltype(ctrl)::value, 0xF, 0xF, true));
+  };
+  s += dpp(s, std::integral_constant<int, 0xB1>{});    // quad_perm [1, 0, 3, 2]
+  s += dpp(s, std::integral_constant<int, 0x4E>{});    // quad_perm [2, 3, 0, 1]
+  s += dpp(s, std::integral_constant<int, 0x141>{});   // row_half_mirror
+  if constexpr (N == 16) s += dpp(s, std::integral_constant<int, 0x140>{});   // row_mirror
+  return s;
+}
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -48,44 +64,93 @@ constexpr float NEG_BIG = -1e30f;
 
 // ---------------------------------------------------------------------------
 // RoPE, rotate-half: (x_i, x_{i+dh/2}) rotated by pos * theta^(-2i/dh).
+// One block per row: the row's dh/2 angles (they do not depend on the head)
+// go through LDS once, then each thread rotates 8 pairs of one head of q and
+// of k with 16-byte accesses.
 // ---------------------------------------------------------------------------
+// 8 consecutive elements (16-byte aligned for bf16, 32-byte for fp32) as floats
+template <typename T>
+__device__ inline void load8(const T* p, float (&v)[8]);
+template <>
+__device__ inline void load8<bf16>(const bf16* p, float (&v)[8]) {
+  const bf16x8 x = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (float)x[i];
+}
+template <>
+__device__ inline void load8<float>(const float* p, float (&v)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+template <typename T>
+__device__ inline void store8(T* p, const float (&v)[8]);
+template <>
+__device__ inline void store8<bf16>(bf16* p, const float (&v)[8]) {
+  bf16x8 x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = (bf16)v[i];
+  *reinterpret_cast<bf16x8*>(p) = x;
+}
+template <>
+__device__ inline void store8<float>(float* p, const float (&v)[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv, int d, int H, int dh,
                                                    float log2_theta) {
+  __shared__ float cs_s[64], sn_s[64];        // dh / 2 <= 64
+  const int r = blockIdx.x;
   const int half = dh >> 1;
-  const int64_t total = (int64_t)pl.T * H * half;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int i = (int)(e % half);
-    const int hh = (int)((e / half) % H);
-    const int r = (int)(e / ((int64_t)half * H));
-    const float inv = exp2f(-(2.0f * (float)i / (float)dh) * log2_theta);
-    const float ang = (float)pl.pos[r] * inv;
+  if (threadIdx.x < half) {
+    const float inv = exp2f(-(2.0f * (float)threadIdx.x / (float)dh) * log2_theta);
     float sn, cs;
-    sincosf(ang, &sn, &cs);
-    T* row = qkv + (int64_t)r * 3 * d + hh * dh;
+    sincosf((float)pl.pos[r] * inv, &sn, &cs);
+    cs_s[threadIdx.x] = cs;
+    sn_s[threadIdx.x] = sn;
+  }
+  __syncthreads();
+  const int per_head = half / 8;              // 8-pair groups per head
+  T* row = qkv + (int64_t)r * 3 * d;
+  for (int w = threadIdx.x; w < 2 * H * per_head; w += blockDim.x) {
+    const int part = w / (H * per_head);      // q, then k
+    const int hh = (w / per_head) % H;
+    const int i0 = (w % per_head) * 8;
+    T* x = row + part * d + hh * dh + i0;
+    float a[8], b[8];
+    load8<T>(x, a);
+    load8<T>(x + half, b);
+    float ya[8], yb[8];
 #pragma unroll
-    for (int part = 0; part < 2; ++part) {  // q, then k
-      T* x = row + part * d;
-      const float a = to_f32(x[i]), b = to_f32(x[i + half]);
-      x[i] = from_f32<T>(a * cs - b * sn);
-      x[i + half] = from_f32<T>(a * sn + b * cs);
+    for (int j = 0; j < 8; ++j) {
+      const float c = cs_s[i0 + j], sv = sn_s[i0 + j];
+      ya[j] = a[j] * c - b[j] * sv;
+      yb[j] = a[j] * sv + b[j] * c;
     }
+    store8<T>(x, ya);
+    store8<T>(x + half, yb);
   }
 }
 
 // ---------------------------------------------------------------------------
-// KV-cache write: row r's k / v go to slot kv_start[p] + pos[r].
+// KV-cache write: row r's k / v go to slot kv_start[p] + pos[r] of every
+// head.  The caches are head-major, [n_heads][kv_slots][head_dim], so one
+// head's keys of one request are a contiguous run.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(256) void kv_write_kernel(Plan pl, const T* __restrict__ qkv, int d,
-                                                       T* __restrict__ kc, T* __restrict__ vc) {
+__global__ __launch_bounds__(256) void kv_write_kernel(Plan pl, const T* __restrict__ qkv, int d, int dh,
+                                                       int64_t kv_slots, T* __restrict__ kc,
+                                                       T* __restrict__ vc) {
   const int r = blockIdx.x;
   const int p = pl.row_req[r];
   const int64_t slot = (int64_t)pl.kv_start[p] + pl.pos[r];
   const T* src = qkv + (int64_t)r * 3 * d;
   for (int c = threadIdx.x; c < d; c += 256) {
-    kc[slot * d + c] = src[d + c];
-    vc[slot * d + c] = src[2 * d + c];
+    const int h = c / dh;
+    const int64_t o = ((int64_t)h * kv_slots + slot) * dh + (c - h * dh);
+    kc[o] = src[d + c];
+    vc[o] = src[2 * d + c];
   }
 }
 
@@ -522,19 +587,6 @@ __global__ __launch_bounds__(256) void attn_prefill_simt_kernel(Plan pl, const T
 // Decode attention: one query row per request against its cached keys
 // (slots kv_start .. kv_start + ctx, the last one just written).
 // ---------------------------------------------------------------------------
-template <typename T>
-__device__ inline void load8(const T* p, float (&v)[8]);
-template <>
-__device__ inline void load8<bf16>(const bf16* p, float (&v)[8]) {
-  const bf16x8 x = *reinterpret_cast<const bf16x8*>(p);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = (float)x[i];
-}
-template <>
-__device__ inline void load8<float>(const float* p, float (&v)[8]) {
-  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-}
 
 // The keys of a request are cut into DEC_CHUNK-key chunks, one block per
 // (request, head, chunk), so long contexts spread over many CUs instead of
@@ -548,16 +600,13 @@ constexpr int DEC_CHUNK = 512;
 template <typename T, int DH, int UNR>
 __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __restrict__ qkv, int d,
                                                           const T* __restrict__ kc,
-                                                          const T* __restrict__ vc,
+                                                          const T* __restrict__ vc, int64_t kv_slots,
                                                           float* __restrict__ part, int nchunk,
                                                           float scale_log2) {
   constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
   constexpr int NG = 256 / LPK;        // key streams per block
   __shared__ float sm[NG], sl[NG];
   __shared__ float so[NG][DH + 1];
-  // heads vary fastest across consecutive blocks, so the blocks in flight
-  // read whole cache rows (all heads of a key) rather than one head's slice
-  // of many rows
   const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
   const int tid = threadIdx.x;
   const int grp = tid / LPK, sub = tid % LPK;
@@ -570,15 +619,15 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
   float q[8];
   load8<T>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8, q);
   float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
-  const T* kp = kc + base * d + h * DH + sub * 8;
-  const T* vp = vc + base * d + h * DH + sub * 8;
+  const T* kp = kc + ((int64_t)h * kv_slots + base) * DH + sub * 8;
+  const T* vp = vc + ((int64_t)h * kv_slots + base) * DH + sub * 8;
   for (int k0 = kbeg + grp; k0 < kend; k0 += UNR * NG) {
     float kv[UNR][8], vv[UNR][8];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int k = min(k0 + u * NG, kend - 1);   // clamped: masked below
-      load8<T>(kp + (int64_t)k * d, kv[u]);
-      load8<T>(vp + (int64_t)k * d, vv[u]);
+      load8<T>(kp + (int64_t)k * DH, kv[u]);
+      load8<T>(vp + (int64_t)k * DH, vv[u]);
     }
     float sc[UNR];
     float smax = NEG_BIG;
@@ -587,8 +636,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) s += q[i] * kv[u][i];
-#pragma unroll
-      for (int w = LPK / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+      s = key_row_sum<LPK>(s);
       sc[u] = k0 + u * NG < kend ? s * scale_log2 : NEG_BIG;
       smax = fmaxf(smax, sc[u]);
     }
@@ -630,6 +678,13 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
 // step is computed: a two-slot register ring filled by loads the compiler
 // does not track (so it does not wait for every load at the loop back-edge);
 // the kernel's own waits cover them, as loads complete in issue order.
+typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// a0 * b0 + a1 * b1 + c on bf16 pairs, fp32 accumulation
+__device__ __forceinline__ float dot2_bf16(bf16x2 a, bf16x2 b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(a, b, c, false);
+}
+__device__ __forceinline__ bf16x2 pair(const bf16x8& v, int j) { return bf16x2{v[2 * j], v[2 * j + 1]}; }
+
 __device__ __forceinline__ void gload16_untracked(bf16x8& dst, const bf16* p) {
   asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
 }
@@ -637,12 +692,13 @@ __device__ __forceinline__ void gload16_untracked(bf16x8& dst, const bf16* p) {
 template <int DH, int UNR>
 __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf16* __restrict__ qkv, int d,
                                                                const bf16* __restrict__ kc,
-                                                               const bf16* __restrict__ vc,
+                                                               const bf16* __restrict__ vc, int64_t kv_slots,
                                                                float* __restrict__ part, int nchunk,
                                                                float scale_log2) {
   constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
   constexpr int NG = 256 / LPK;        // key streams per block
   constexpr int STEP = UNR * NG;       // keys per step of the block
+  static_assert(UNR % 2 == 0, "keys are weighted in pairs");
   __shared__ float sm[NG], sl[NG];
   __shared__ float so[NG][DH + 1];
   const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
@@ -654,11 +710,10 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
   if (kbeg >= nkeys) return;                 // block-uniform
   const int kend = min(kbeg + DEC_CHUNK, nkeys);
   const int64_t base = (int64_t)pl.kv_start[p];
-  float q[8];
-  load8<bf16>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8, q);
+  const bf16x8 q = *reinterpret_cast<const bf16x8*>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8);
   float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
-  const bf16* kp = kc + base * d + h * DH + sub * 8;
-  const bf16* vp = vc + base * d + h * DH + sub * 8;
+  const bf16* kp = kc + ((int64_t)h * kv_slots + base) * DH + sub * 8;
+  const bf16* vp = vc + ((int64_t)h * kv_slots + base) * DH + sub * 8;
   bf16x8 kb[2][UNR], vb[2][UNR];
   // keys past the chunk re-read its last key (masked), so every step issues
   // 2 * UNR loads and one wait count holds throughout
@@ -666,8 +721,8 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int k = min(k0 + u * NG, kend - 1);
-      gload16_untracked(kb[slot][u], kp + (int64_t)k * d);
-      gload16_untracked(vb[slot][u], vp + (int64_t)k * d);
+      gload16_untracked(kb[slot][u], kp + (int64_t)k * DH);
+      gload16_untracked(vb[slot][u], vp + (int64_t)k * DH);
     }
   };
   auto step = [&](int slot, int k0) {
@@ -677,31 +732,34 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
     for (int u = 0; u < UNR; ++u) {
       float s = 0.f;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += q[i] * (float)kb[slot][u][i];
-#pragma unroll
-      for (int w = LPK / 2; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+      for (int j = 0; j < 4; ++j) s = dot2_bf16(pair(q, j), pair(kb[slot][u], j), s);
+      s = key_row_sum<LPK>(s);
       sc[u] = k0 + u * NG < kend ? s * scale_log2 : NEG_BIG;
       smax = fmaxf(smax, sc[u]);
     }
     const float m_new = fmaxf(m_run, smax);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = fast_exp2(m_run - m_new);
     l_run *= alpha;
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[i] *= alpha;
+    // weights rounded to bf16 (as the MFMA paths do); the sum l takes the
+    // rounded values so the normalisation matches
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const float e = k0 + u * NG < kend ? exp2f(sc[u] - m_new) : 0.f;
-      l_run += e;
+    for (int u = 0; u < UNR; u += 2) {
+      const float e0 = k0 + u * NG < kend ? fast_exp2(sc[u] - m_new) : 0.f;
+      const float e1 = k0 + (u + 1) * NG < kend ? fast_exp2(sc[u + 1] - m_new) : 0.f;
+      const bf16x2 ep = {(bf16)e0, (bf16)e1};
+      l_run += (float)ep[0] + (float)ep[1];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) o[i] += e * (float)vb[slot][u][i];
+      for (int i = 0; i < 8; ++i)
+        o[i] = dot2_bf16(ep, bf16x2{vb[slot][u][i], vb[slot][u + 1][i]}, o[i]);
     }
     m_run = m_new;
   };
   const int first = kbeg + grp;
   // q is needed by the first step: take its (tracked) load's wait here,
   // before the untracked K / V loads are in flight behind it
-#pragma unroll
-  for (int i = 0; i < 8; ++i) asm volatile("" ::"v"(q[i]));
+  asm volatile("" ::"v"(q));
   if (first < kend) {
     issue(0, first);
     for (int k0 = first; k0 < kend; k0 += 2 * STEP) {
@@ -783,13 +841,12 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const fl
 
 hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
                        float theta, hipStream_t s) {
-  const int64_t total = (int64_t)pl.T * n_heads * (head_dim / 2);
-  const int grid = (int)std::min<int64_t>((total + 255) / 256, 65536);
+  if (pl.T == 0) return hipSuccess;
   const float l2t = log2f(theta);
   if (dtype == VFM_BF16)
-    hipLaunchKernelGGL(rope_kernel<bf16>, dim3(grid), dim3(256), 0, s, pl, (bf16*)qkv, d, n_heads, head_dim, l2t);
+    hipLaunchKernelGGL(rope_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (bf16*)qkv, d, n_heads, head_dim, l2t);
   else
-    hipLaunchKernelGGL(rope_kernel<float>, dim3(grid), dim3(256), 0, s, pl, (float*)qkv, d, n_heads, head_dim, l2t);
+    hipLaunchKernelGGL(rope_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (float*)qkv, d, n_heads, head_dim, l2t);
   return hipGetLastError();
 }
 
@@ -800,8 +857,8 @@ size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys) {
 }
 
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv, void* out,
-                            void* k_cache, void* v_cache, void* ws, size_t ws_bytes, int max_keys,
-                            hipStream_t s) {
+                            void* k_cache, void* v_cache, int64_t kv_slots, void* ws, size_t ws_bytes,
+                            int max_keys, hipStream_t s) {
   const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
   // timing classes: the attention kernel itself is VFM_PROF_ATTN, the cache
@@ -810,11 +867,11 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   if (k_cache && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
     pi = prof_begin(VFM_PROF_OTHER, s);
     if (dtype == VFM_BF16)
-      hipLaunchKernelGGL(kv_write_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (const bf16*)qkv, d,
-                         (bf16*)k_cache, (bf16*)v_cache);
+      hipLaunchKernelGGL(kv_write_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (const bf16*)qkv, d, DH,
+                         kv_slots, (bf16*)k_cache, (bf16*)v_cache);
     else
-      hipLaunchKernelGGL(kv_write_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (const float*)qkv, d,
-                         (float*)k_cache, (float*)v_cache);
+      hipLaunchKernelGGL(kv_write_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (const float*)qkv, d, DH,
+                         kv_slots, (float*)k_cache, (float*)v_cache);
     prof_end(pi, s);
   }
   if (c.attn == VFM_ATTN_DECODE) {
@@ -826,10 +883,12 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   pi = prof_begin(VFM_PROF_ATTN, s);                                                                   \
   if (dtype == VFM_BF16)                                                                               \
     hipLaunchKernelGGL((attn_decode_bf16_kernel<D_, 4>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
-                       d, (const bf16*)k_cache, (const bf16*)v_cache, part, nchunk, scale_log2);     \
+                       d, (const bf16*)k_cache, (const bf16*)v_cache, kv_slots, part, nchunk,       \
+                       scale_log2);                                                                  \
   else                                                                                                 \
     hipLaunchKernelGGL((attn_decode_kernel<float, D_, 4>), grid, dim3(256), 0, s, pl, (const float*)qkv, \
-                       d, (const float*)k_cache, (const float*)v_cache, part, nchunk, scale_log2);   \
+                       d, (const float*)k_cache, (const float*)v_cache, kv_slots, part, nchunk,     \
+                       scale_log2);                                                                  \
   prof_end(pi, s);                                                                                     \
   pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
   hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \

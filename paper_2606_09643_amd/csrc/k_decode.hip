@@ -40,48 +40,83 @@ constexpr int SBM = 256, SBK = 64;
 
 // ---------------------------------------------------------------------------
 // Split-K GEMM, BN = 64 * NWN columns per block, 4 x NWN waves of 64 x 64.
+//
+// Every weight element is used by the few hundred rows of one tile only, so
+// the weight stream comes from HBM at full latency while the activation
+// columns are L2 hits.  Half of the waves load activation stages (one step
+// ahead, two LDS stages), the other half weight stages (WST - 1 steps
+// ahead, WST LDS stages): a wave's loads complete in issue order, so
+// keeping the two streams in different waves lets the short-latency
+// activation loads be waited on without waiting for the weight loads
+// behind them.  All waves take part in the MFMA work.
 // ---------------------------------------------------------------------------
-template <int NWN>
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);   // vmcnt(N), lgkmcnt / expcnt not waited
+}
+
+template <int NWN, int WST>
 __global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
-  constexpr int BN = 64 * NWN, NW = 4 * NWN;
+  constexpr int BN = 64 * NWN, NW = 4 * NWN, XW = NW / 2, WW = NW - XW;
   constexpr int SA = SBM * SBK, SB = BN * SBK;
-  constexpr int ARND = SBM / (8 * NW), BRND = BN / (8 * NW);
-  __shared__ __attribute__((aligned(16))) bf16 smem[2 * (SA + SB)];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int XR = SBM / (8 * XW), WR = BN / (8 * WW);    // 1 KB rounds per stage and loader wave
+  static_assert(XR * 8 * XW == SBM && WR * 8 * WW == BN, "loader rounds");
+  static_assert(WST == 3 || WST == 4, "weight stages");
+  static_assert(WR * (WST - 2) < 16, "vmcnt range");
+  __shared__ __attribute__((aligned(16))) bf16 smem[2 * SA + WST * SB];
+  // wave index in an SGPR, so the loader roles below are scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 3, wn = wave >> 2;
   const int ntn = (a.N + BN - 1) / BN;
-  const int tn = blockIdx.x % ntn, split = blockIdx.x / ntn;
+  // consecutive blocks land on one XCD (the dispatcher deals block ids out
+  // to the 8 XCDs in turn), so the blocks of one K split share that XCD's
+  // L2 copy of the split's activation columns; the grid is padded to a
+  // multiple of 8 and the padding blocks leave at once
+  const int bx = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+  if (bx >= ntn * a.nsplit) return;
+  const int tn = bx % ntn, split = bx / ntn;
   const int m0 = blockIdx.y * SBM, n0 = tn * BN;
   const int nkt = a.K / SBK;
   const int kt0 = (int)((int64_t)split * nkt / a.nsplit);
   const int kt1 = (int)((int64_t)(split + 1) * nkt / a.nsplit);
-  const bf16* X = (const bf16*)a.X;
+  const int nk = kt1 - kt0;
 
-  // each wave fills 8 rows x 128 B (1 KB) of LDS per round; the swizzle is
-  // applied on the global side, so lane l writes chunk (l & 7) of its row
-  const int row0 = wave * 8 + (lane >> 3);
-  const int kc0 = (lane & 7) ^ ((row0 >> 1) & 7);  // same for row0 + 8 * NW * i
-  const bf16* xsrc[ARND];
+  // loader rows: wave lw of its operand fills rows lw * 8 + (lane >> 3) +
+  // 8 * (loader waves) * i; the swizzle is applied on the global side, so
+  // lane l writes chunk (l & 7) of its row (the chunk permutation is the
+  // same for every round because 4 * loader waves is a multiple of 8)
+  const bool xload = wave < XW;
+  const int lw = xload ? wave : wave - XW;
+  const int row0 = lw * 8 + (lane >> 3);
+  const int kc0 = (lane & 7) ^ ((row0 >> 1) & 7);
+  constexpr int MR = XR > WR ? XR : WR;
+  const bf16* src[MR];
+  if (xload) {
 #pragma unroll
-  for (int i = 0; i < ARND; ++i)
-    xsrc[i] = X + (int64_t)min(m0 + row0 + i * 8 * NW, a.M - 1) * a.ldx + kc0 * 8;
-  const bf16* wsrc[BRND];
+    for (int i = 0; i < XR; ++i)
+      src[i] = (const bf16*)a.X + (int64_t)min(m0 + row0 + i * 8 * XW, a.M - 1) * a.ldx + kt0 * SBK + kc0 * 8;
+  } else {
 #pragma unroll
-  for (int i = 0; i < BRND; ++i) {
-    const int n = min(n0 + row0 + i * 8 * NW, a.N - 1);
-    const bool hi = a.W2 != nullptr && n >= a.n_half;
-    wsrc[i] = (const bf16*)(hi ? a.W2 : a.W) + (int64_t)(hi ? n - a.n_half : n) * a.K + kc0 * 8;
+    for (int i = 0; i < WR; ++i) {
+      const int n = min(n0 + row0 + i * 8 * WW, a.N - 1);
+      const bool hi = a.W2 != nullptr && n >= a.n_half;
+      src[i] = (const bf16*)(hi ? a.W2 : a.W) + (int64_t)(hi ? n - a.n_half : n) * a.K + kt0 * SBK + kc0 * 8;
+    }
   }
-  auto issue = [&](int kt, int st) {
-    bf16* As = smem + st * (SA + SB);
-    bf16* Bs = As + SA;
-    const int k0 = kt * SBK;
+  bf16* const Xs = smem;
+  bf16* const Ws = smem + 2 * SA;
+  auto issue_x = [&](int j) {   // step j of the block's K range into X stage j & 1
 #pragma unroll
-    for (int i = 0; i < ARND; ++i)
-      __builtin_amdgcn_global_load_lds((gptr_t)(xsrc[i] + k0), (lptr_t)(As + (i * NW + wave) * 512), 16, 0, 0);
+    for (int i = 0; i < XR; ++i)
+      __builtin_amdgcn_global_load_lds((gptr_t)(src[i] + j * SBK),
+                                       (lptr_t)(Xs + (j & 1) * SA + (i * XW + lw) * 512), 16, 0, 0);
+  };
+  auto issue_w = [&](int j, int slot) {
 #pragma unroll
-    for (int i = 0; i < BRND; ++i)
-      __builtin_amdgcn_global_load_lds((gptr_t)(wsrc[i] + k0), (lptr_t)(Bs + (i * NW + wave) * 512), 16, 0, 0);
+    for (int i = 0; i < WR; ++i)
+      __builtin_amdgcn_global_load_lds((gptr_t)(src[i] + j * SBK),
+                                       (lptr_t)(Ws + slot * SB + (i * WW + lw) * 512), 16, 0, 0);
   };
 
   f32x4 acc[4][4];
@@ -89,15 +124,40 @@ __global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
   for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (kt0 < kt1) {
-    issue(kt0, 0);
-    __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): the stage has landed in LDS
-    __builtin_amdgcn_s_barrier();
-    for (int kt = kt0; kt < kt1; ++kt) {
-      const int st = (kt - kt0) & 1;
-      if (kt + 1 < kt1) issue(kt + 1, st ^ 1);
-      const bf16* As = smem + st * (SA + SB);
-      const bf16* Bs = As + SA;
+  if (nk > 0) {
+    if (xload) {
+      issue_x(0);
+    } else {
+#pragma unroll
+      for (int j = 0; j < WST - 1; ++j)
+        if (j < nk) issue_w(j, j);
+    }
+    int ws = 0;                                   // W stage of step j
+    for (int j = 0; j < nk; ++j) {
+      // this wave's loads of step j have landed: the X loaders have nothing
+      // newer in flight, the W loaders up to WST - 2 newer steps
+      if (xload) {
+        wait_vm<0>();
+      } else {
+        const int newer = min(nk - 1 - j, WST - 2);
+        if constexpr (WST >= 4) {
+          if (newer >= 2) wait_vm<2 * WR>();
+          else if (newer == 1) wait_vm<WR>();
+          else wait_vm<0>();
+        } else {
+          if (newer >= 1) wait_vm<WR>();
+          else wait_vm<0>();
+        }
+      }
+      __builtin_amdgcn_s_barrier();
+      // every wave is past step j - 1, whose X stage and W stage are free
+      if (xload) {
+        if (j + 1 < nk) issue_x(j + 1);
+      } else {
+        if (j + WST - 1 < nk) issue_w(j + WST - 1, ws == 0 ? WST - 1 : ws - 1);
+      }
+      const bf16* As = Xs + (j & 1) * SA;
+      const bf16* Bs = Ws + ws * SB;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         const int kc = kk * 4 + (lane >> 4);
@@ -117,8 +177,7 @@ __global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
 #pragma unroll
           for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = mfma16(wf[ni], xf[mi], acc[mi][ni]);
       }
-      __builtin_amdgcn_s_waitcnt(0xF70);
-      __builtin_amdgcn_s_barrier();
+      ws = ws == WST - 1 ? 0 : ws + 1;
     }
   }
   // lane holds D[n = 4 * (lane >> 4) + i][m = lane & 15] of each 16 x 16 block
@@ -367,21 +426,19 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
 }
 
 // Column-tile width and K split of the small-batch GEMM for an N x K
-// weight, from a sweep of 256-row products on MI355X: wide weights (N >=
-// 8192) take 256-column tiles, narrow ones 64-column tiles (two blocks per
-// CU), and K is split until one row tile fills the chip once (256 or 512
-// blocks), at most 4 ways for wide weights so the fp32 partials stay below
-// the weight bytes.  The split depends on the weight shape only, never on
-// the batch, so a row's result does not depend on the other rows.
+// weight: wide weights (N >= 8192) take 256-column tiles, narrow ones
+// 128-column tiles, and K is split until one row tile fills the chip once
+// (one block per CU), at most 6 ways for wide weights so the fp32 partials
+// stay below the weight bytes.  The split depends on the weight shape only,
+// never on the batch, so a row's result does not depend on the other rows.
 void skinny_shape(int N, int K, int* bn, int* nsplit) {
   const int nkt = K / SBK;
   const bool wide = N >= 8192;
-  const int b = wide ? 256 : 64;
-  const int slots = wide ? 256 : 512;
+  const int b = wide ? 256 : 128;
   const int tiles = (N + b - 1) / b;
-  const int cap = wide ? 4 : 16;
+  const int cap = wide ? 6 : 16;
   *bn = b;
-  *nsplit = std::max(1, std::min(std::min(slots / tiles, cap), nkt));
+  *nsplit = std::max(1, std::min(std::min(256 / tiles, cap), nkt));
 }
 
 }  // namespace
@@ -398,12 +455,11 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& a0, hipStream_t s) {
   int bn;
   skinny_shape(a.N, a.K, &bn, &a.nsplit);
   const int ntn = (a.N + bn - 1) / bn;
-  dim3 grid(ntn * a.nsplit, (a.M + SBM - 1) / SBM);
-  switch (bn) {
-    case 64: hipLaunchKernelGGL(gemm_skinny_kernel<1>, grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL(gemm_skinny_kernel<2>, grid, dim3(512), 0, s, a); break;
-    default: hipLaunchKernelGGL(gemm_skinny_kernel<4>, grid, dim3(1024), 0, s, a); break;
-  }
+  dim3 grid((ntn * a.nsplit + 7) & ~7, (a.M + SBM - 1) / SBM);
+  if (bn == 128)
+    hipLaunchKernelGGL((gemm_skinny_kernel<2, 4>), grid, dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_skinny_kernel<4, 3>), grid, dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 

@@ -250,8 +250,8 @@ hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads,
 // Decode needs attention_workspace() bytes of ws; max_keys = the largest
 // ctx + length over the batch's requests.
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv,
-                            void* out, void* k_cache, void* v_cache, void* ws, size_t ws_bytes,
-                            int max_keys, hipStream_t s);
+                            void* out, void* k_cache, void* v_cache, int64_t kv_slots, void* ws,
+                            size_t ws_bytes, int max_keys, hipStream_t s);
 size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys);
 
 // Input rows into the fp32 residual stream (plan order).

@@ -75,16 +75,28 @@ class Inputs:
 
 
 class KVCache:
-    """Per-layer cached K / V for the decode workload ([sum(ctx + 1), d] each)."""
+    """Per-layer cached K / V for the decode workload, in the library's
+    head-major layout [n_heads, sum(ctx + 1), head_dim]."""
 
     def __init__(self, w: wl.Workload, batch: wl.Batch, n_layers, device="cuda", seed=wl.DEFAULT_SEED):
         self.kv_start = wl.kv_offsets(batch).astype(np.int32)
         self.slots = int((batch.ctx.astype(np.int64) + 1).sum())
+        self.n_heads, self.head_dim = w.n_heads, w.head_dim
         self.k, self.v = [], []
         for i in range(n_layers):
             k, v = wl.kv_cache_layer(w, batch, i, device, seed)
-            self.k.append(k)
-            self.v.append(v)
+            self.k.append(self._head_major(k))
+            self.v.append(self._head_major(v))
+            del k, v
+
+    def _head_major(self, t):
+        return t.view(t.shape[0], self.n_heads, self.head_dim).permute(1, 0, 2).contiguous()
+
+    def rows(self, li, s0, n):
+        """(K, V) of slots s0 .. s0 + n - 1 of layer li as [n, d] tensors."""
+        def take(c):
+            return c[:, s0:s0 + n, :].permute(1, 0, 2).reshape(n, self.n_heads * self.head_dim)
+        return take(self.k[li]), take(self.v[li])
 
 
 def make_batch(w: wl.Workload, batch: wl.Batch, heads: wl.Heads | None, kv: KVCache | None = None,

@@ -38,8 +38,9 @@ def expected_embed(w, batch, inp, pl):
     return np.concatenate([src[cu_o[i]:cu_o[i + 1]] for i in pl["order"]])
 
 
-def oracle_layer_rows(w, W_np, ad, pl, x_plan, reqs, kv=None, kv_start=None):
-    """Oracle layer for the chosen plan positions; returns {p: (y, k, v)}."""
+def oracle_layer_rows(w, W_np, ad, pl, x_plan, reqs, kv=None, li=0):
+    """Oracle layer for the chosen plan positions; returns {p: (y, k, v)}.
+    kv: the decode KV cache (layer li's cached keys are read from it)."""
     spec = spec_of(w)
     cu = pl["cu_seqlens"]
     res = {}
@@ -50,8 +51,8 @@ def oracle_layer_rows(w, W_np, ad, pl, x_plan, reqs, kv=None, kv_start=None):
         if kv is not None:
             i = int(pl["order"][p])
             c = int(pl["pos"][sl][0])
-            s0 = int(kv_start[i])
-            kvp = (np64(kv[0][s0:s0 + c]), np64(kv[1][s0:s0 + c]))
+            kr, vr = kv.rows(li, int(kv.kv_start[i]), c)
+            kvp = (np64(kr), np64(vr))
         res[p] = O.layer(spec, W_np, oracle_adapter(ad, t), x_plan[sl], pos=pl["pos"][sl], kv=kvp)
     return res
 

@@ -84,9 +84,7 @@ def test_layer_parity(idx, b_std):
     got = fwd.x.double().cpu().numpy()
     W_np = oracle_weights(model.layers[0])
     reqs = list(range(batch.n_req))
-    kvc = (kv.k[0], kv.v[0]) if kv is not None else None
-    res = oracle_layer_rows(w, W_np, model.adapters[0], pl, x_in, reqs, kv=kvc,
-                            kv_start=kv.kv_start if kv is not None else None)
+    res = oracle_layer_rows(w, W_np, model.adapters[0], pl, x_in, reqs, kv=kv, li=0)
     cu = pl["cu_seqlens"]
     worst = 0.0
     for p in reqs:
@@ -98,8 +96,9 @@ def test_layer_parity(idx, b_std):
         for p in reqs:
             i = int(pl["order"][p])
             slot = int(kv.kv_start[i] + batch.ctx[i])
-            kg = kv.k[0][slot].double().cpu().numpy()[None]
-            vg = kv.v[0][slot].double().cpu().numpy()[None]
+            kr, vr = kv.rows(0, slot, 1)
+            kg = kr.double().cpu().numpy()
+            vg = vr.double().cpu().numpy()
             assert O.row_rel_error(kg, res[p][1]) < tol(w)
             assert O.row_rel_error(vg, res[p][2]) < tol(w)
 
@@ -396,16 +395,16 @@ def test_full_size_sampled(idx):
         fwd.layer(li)
         torch.cuda.synchronize()
         got = fwd.x.double().cpu().numpy()
-        kvc = (kv.k[li], kv.v[li]) if kv is not None else None
         res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_in, reqs,
-                                kv=kvc, kv_start=kv.kv_start if kv is not None else None)
+                                kv=kv, li=li)
         for p in reqs:
             worst = max(worst, O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]))
             if kv is not None:
                 i = int(pl["order"][p])
                 slot = int(kv.kv_start[i] + batch.ctx[i])
-                assert O.row_rel_error(kv.k[li][slot].double().cpu().numpy()[None], res[p][1]) < tol(w)
-                assert O.row_rel_error(kv.v[li][slot].double().cpu().numpy()[None], res[p][2]) < tol(w)
+                kr, vr = kv.rows(li, slot, 1)
+                assert O.row_rel_error(kr.double().cpu().numpy(), res[p][1]) < tol(w)
+                assert O.row_rel_error(vr.double().cpu().numpy(), res[p][2]) < tol(w)
         log(f"  layer {li}: max row rel err so far {worst:.3e}")
     assert worst < tol(w)
     if model.heads is not None and n_layers == w.n_layers:
