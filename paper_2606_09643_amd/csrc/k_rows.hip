@@ -188,39 +188,73 @@ __global__ __launch_bounds__(256) void norm_rows_unpermute_kernel(
   }
 }
 
-// Final norm + pooling: one block (4 waves) per request in plan order.
+// Final norm + pooling: one block per request in plan order, 16 / 8 / 4
+// waves by row width, each summing its rows in registers.
+template <int MAXI>
+constexpr int pool_waves() { return MAXI <= 4 ? 16 : (MAXI <= 8 ? 8 : 4); }
+
 template <typename T, int MAXI>
-__global__ __launch_bounds__(256) void norm_pool_kernel(Plan pl, const float* __restrict__ x,
-                                                        int d, const T* __restrict__ g,
-                                                        const T* __restrict__ b, int kind,
-                                                        float eps, int pool,
-                                                        T* __restrict__ pooled) {
+__global__ __launch_bounds__((64 * pool_waves<MAXI>())) void norm_pool_kernel(
+    Plan pl, const float* __restrict__ x, int d, const T* __restrict__ g, const T* __restrict__ b, int kind,
+    float eps, int pool, T* __restrict__ pooled) {
+  constexpr int NWV = pool_waves<MAXI>();
+  constexpr bool REG = MAXI <= 8;        // narrow rows: per-wave sums stay in registers
   extern __shared__ float acc[];  // [d]
   const int p = blockIdx.x;
   const int r0 = pl.cu_seqlens[p], r1 = pl.cu_seqlens[p + 1];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int i = threadIdx.x; i < d; i += 256) acc[i] = 0.f;
-  __syncthreads();
+  const int nch = d >> 2;
   int first = r0, last = r1;
   if (pool == VFM_POOL_FIRST) last = r0 + 1;
   if (pool == VFM_POOL_LAST) first = r1 - 1;
-  for (int r = first + wave; r < last; r += 4) {
-    float4 v[MAXI];
-    norm_row_regs<T, MAXI>(x + (int64_t)r * d, d, g, b, kind, eps, v);
+  for (int i = threadIdx.x; i < d; i += 64 * NWV) acc[i] = 0.f;
+  __syncthreads();
+  // adds a wave's float4 chunks into acc; the callers take the waves in a
+  // fixed order, so the sum does not depend on scheduling
+  auto add_to_acc = [&](const float4 (&u)[MAXI]) {
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int c = lane + 64 * i;
-      if (c < (d >> 2)) {
-        atomicAdd(&acc[4 * c + 0], v[i].x);
-        atomicAdd(&acc[4 * c + 1], v[i].y);
-        atomicAdd(&acc[4 * c + 2], v[i].z);
-        atomicAdd(&acc[4 * c + 3], v[i].w);
+      if (c < nch) {
+        float4* a4 = reinterpret_cast<float4*>(acc) + c;
+        float4 o = *a4;
+        o.x += u[i].x; o.y += u[i].y; o.z += u[i].z; o.w += u[i].w;
+        *a4 = o;
+      }
+    }
+  };
+  if constexpr (REG) {
+    // each wave sums its rows (first + wave, + NWV, ...) in registers, then
+    // the wave sums are added in wave order
+    float4 sum[MAXI];
+#pragma unroll
+    for (int i = 0; i < MAXI; ++i) sum[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int r = first + wave; r < last; r += NWV) {
+      float4 v[MAXI];
+      norm_row_regs<T, MAXI>(x + (int64_t)r * d, d, g, b, kind, eps, v);
+#pragma unroll
+      for (int i = 0; i < MAXI; ++i) {
+        sum[i].x += v[i].x; sum[i].y += v[i].y; sum[i].z += v[i].z; sum[i].w += v[i].w;
+      }
+    }
+    for (int w = 0; w < NWV; ++w) {
+      if (wave == w) add_to_acc(sum);
+      __syncthreads();
+    }
+  } else {
+    // wide rows: NWV rows per round, added in row order
+    for (int rb = first; rb < last; rb += NWV) {
+      const int r = rb + wave;
+      float4 v[MAXI];
+      if (r < last) norm_row_regs<T, MAXI>(x + (int64_t)r * d, d, g, b, kind, eps, v);
+      for (int w = 0; w < NWV; ++w) {
+        if (wave == w && r < last) add_to_acc(v);
+        __syncthreads();
       }
     }
   }
-  __syncthreads();
   const float inv = 1.f / (float)(last - first);
-  for (int i = threadIdx.x; i < d; i += 256)
+  for (int i = threadIdx.x; i < d; i += 64 * NWV)
     pooled[(int64_t)p * d + i] = from_f32<T>(acc[i] * inv);
 }
 
@@ -259,6 +293,17 @@ __global__ __launch_bounds__(256) void embed_tokens_kernel(Plan pl, const int32_
 }
 
 // Patch embedding x = W_pe patch + b_pe, one wave per row, width <= 64.
+// 8 consecutive weights (16-byte aligned for bf16, 32-byte for fp32) as floats
+__device__ inline void load8w(const bf16* p, float (&v)[8]) {
+  const bf16x8 q = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = (float)q[k];
+}
+__device__ inline void load8w(const float* p, float (&v)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void embed_patches_kernel(Plan pl, const float* __restrict__ src,
                                                             int width, const T* __restrict__ W,
@@ -268,8 +313,29 @@ __global__ __launch_bounds__(256) void embed_patches_kernel(Plan pl, const float
   if (row >= pl.T) return;
   const int lane = threadIdx.x & 63;
   const float* s = src + (int64_t)orig_row(pl, row) * width;
-  const float mine = lane < width ? s[lane] : 0.f;
   float* o = x + (int64_t)row * d;
+  if (width == 8 && (d & 3) == 0) {
+    // 8-wide patches: the patch in registers, 4 outputs per lane and pass,
+    // each output's weight row one 16-byte load
+    float pv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) pv[k] = s[k];
+    for (int n0 = 4 * lane; n0 < d; n0 += 256) {
+      float r4[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float wv[8];
+        load8w(W + (int64_t)(n0 + j) * 8, wv);
+        float acc = bias ? to_f32(bias[n0 + j]) : 0.f;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc += wv[k] * pv[k];
+        r4[j] = acc;
+      }
+      *reinterpret_cast<float4*>(o + n0) = make_float4(r4[0], r4[1], r4[2], r4[3]);
+    }
+    return;
+  }
+  const float mine = lane < width ? s[lane] : 0.f;
   for (int n = lane; n < d; n += 64) {
     const T* w = W + (int64_t)n * width;
     float acc = bias ? to_f32(bias[n]) : 0.f;
@@ -324,11 +390,11 @@ hipError_t launch_norm_pool(int dtype, const Plan& pl, const float* x, int d, co
 #undef NP_LAUNCH
     return hipGetLastError();
   }
-  dim3 grid(pl.n_req), block(256);
+  dim3 grid(pl.n_req);
   const size_t lds = (size_t)d * sizeof(float);
-#define PL_LAUNCH(TT, MI)                                                                     \
-  hipLaunchKernelGGL((norm_pool_kernel<TT, MI>), grid, block, lds, s, pl, x, d, (const TT*)g, \
-                     (const TT*)b, kind, eps, pool, (TT*)pooled)
+#define PL_LAUNCH(TT, MI)                                                                            \
+  hipLaunchKernelGGL((norm_pool_kernel<TT, MI>), grid, dim3(64 * pool_waves<MI>()), lds, s, pl, x, d, \
+                     (const TT*)g, (const TT*)b, kind, eps, pool, (TT*)pooled)
   if (dtype == VFM_BF16) {
     if (mi == 4) PL_LAUNCH(bf16, 4); else if (mi == 16) PL_LAUNCH(bf16, 16); else PL_LAUNCH(bf16, 32);
   } else {
