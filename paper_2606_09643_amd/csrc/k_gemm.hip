@@ -619,7 +619,10 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0): DMA and zero writes done
     __builtin_amdgcn_s_barrier();
   }
-  if (EPI == EPI_STORE)
+  // whole rows through LDS (16 B per lane) for the bf16 outputs and for the
+  // fp32 residual of tiles narrower than 256 columns; the 256-column
+  // residual tile writes from registers (its staged form spills)
+  if (EPI != EPI_RESID || BNT < 256)
     epilogue_lds<EPI, SWIGLU, BMT, BNT, FM, FN>(a, reinterpret_cast<char*>(smem), m0, n0, wm, wn, lane, tid,
                                                  acc);
   else
