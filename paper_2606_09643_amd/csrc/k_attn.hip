@@ -592,17 +592,19 @@ __global__ __launch_bounds__(256) void attn_prefill_simt_kernel(Plan pl, const T
 // (request, head, chunk), so long contexts spread over many CUs instead of
 // finishing as a long tail; each block leaves its chunk's running max m,
 // sum l and unnormalised output o, and a merge kernel combines the chunks
-// (the usual rescaling of partial softmax sums by 2^(m_c - m)).
+// (the usual rescaling of partial softmax sums by 2^(m_c - m)).  A request
+// with a single chunk gets its output from the attention kernel directly.
 // Inside a block, each group of LPK lanes walks one key stream; every step
 // issues the K and V loads of UNR keys of the stream before any is used.
-constexpr int DEC_CHUNK = 512;
+constexpr int DEC_CHUNK = 1024;
 
 template <typename T, int DH, int UNR>
 __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __restrict__ qkv, int d,
                                                           const T* __restrict__ kc,
                                                           const T* __restrict__ vc, int64_t kv_slots,
                                                           float* __restrict__ part, int nchunk,
-                                                          float scale_log2) {
+                                                          float scale_log2, T* __restrict__ out) {
+  using OT = T;
   constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
   constexpr int NG = 256 / LPK;        // key streams per block
   __shared__ float sm[NG], sl[NG];
@@ -668,9 +670,14 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
       acc += so[gq][tid] * w;
     }
     // partial record of (p, h, c): [m, l, o[0..DH)]
-    float* rec = part + (((int64_t)p * gridDim.x + h) * nchunk + c) * (DH + 2);
-    rec[2 + tid] = acc;
-    if (tid == 0) { rec[0] = M; rec[1] = lsum; }
+    if (nkeys <= DEC_CHUNK) {
+      // the request's only chunk: its output directly (the merge skips it)
+      out[(int64_t)R * d + h * DH + tid] = from_f32<OT>(acc / lsum);
+    } else {
+      float* rec = part + (((int64_t)p * gridDim.x + h) * nchunk + c) * (DH + 2);
+      rec[2 + tid] = acc;
+      if (tid == 0) { rec[0] = M; rec[1] = lsum; }
+    }
   }
 }
 
@@ -694,7 +701,8 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
                                                                const bf16* __restrict__ kc,
                                                                const bf16* __restrict__ vc, int64_t kv_slots,
                                                                float* __restrict__ part, int nchunk,
-                                                               float scale_log2) {
+                                                               float scale_log2, bf16* __restrict__ out) {
+  using OT = bf16;
   constexpr int LPK = DH / 8;          // lanes per key row (8 dims each)
   constexpr int NG = 256 / LPK;        // key streams per block
   constexpr int STEP = UNR * NG;       // keys per step of the block
@@ -790,9 +798,14 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
       lsum += sl[gq] * w;
       acc += so[gq][tid] * w;
     }
-    float* rec = part + (((int64_t)p * gridDim.x + h) * nchunk + c) * (DH + 2);
-    rec[2 + tid] = acc;
-    if (tid == 0) { rec[0] = M; rec[1] = lsum; }
+    if (nkeys <= DEC_CHUNK) {
+      // the request's only chunk: its output directly (the merge skips it)
+      out[(int64_t)R * d + h * DH + tid] = from_f32<OT>(acc / lsum);
+    } else {
+      float* rec = part + (((int64_t)p * gridDim.x + h) * nchunk + c) * (DH + 2);
+      rec[2 + tid] = acc;
+      if (tid == 0) { rec[0] = M; rec[1] = lsum; }
+    }
   }
 }
 
@@ -805,6 +818,7 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const fl
   const int R = pl.cu_seqlens[p];
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int nc = min((nkeys + DEC_CHUNK - 1) / DEC_CHUNK, nchunk);
+  if (nc <= 1) return;                       // written by the attention kernel itself
   const float* rec = part + ((int64_t)p * gridDim.y + h) * nchunk * (DH + 2);
   // global max of the chunk maxima (all threads read the same few values)
   float M = NEG_BIG;
@@ -884,11 +898,11 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   if (dtype == VFM_BF16)                                                                               \
     hipLaunchKernelGGL((attn_decode_bf16_kernel<D_, 4>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
                        d, (const bf16*)k_cache, (const bf16*)v_cache, kv_slots, part, nchunk,       \
-                       scale_log2);                                                                  \
+                       scale_log2, (bf16*)out);                                                      \
   else                                                                                                 \
     hipLaunchKernelGGL((attn_decode_kernel<float, D_, 4>), grid, dim3(256), 0, s, pl, (const float*)qkv, \
                        d, (const float*)k_cache, (const float*)v_cache, kv_slots, part, nchunk,     \
-                       scale_log2);                                                                  \
+                       scale_log2, (float*)out);                                                     \
   prof_end(pi, s);                                                                                     \
   pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
   hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
