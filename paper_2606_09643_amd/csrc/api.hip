@@ -232,9 +232,15 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
   // One projection group: X [T, K] times the stacked weights (W, then W2
   // for SwiGLU), the per-task LoRA of `projs` (column slots of slot_width),
   // and the epilogue.
+  // norm_into: for a residual projection, the pre-norm that follows it (its
+  // output buffer); the small-batch path then fuses the two, and the caller
+  // skips its own norm launch when `fused_norm` comes back true
+  bool fused_norm = false;
   auto project = [&](int cls, const void* X, int K, const void* W, const void* W2,
                      const void* bias, int N, int epi, void* out, int ldo,
-                     std::initializer_list<int> projs, int slot_width) -> int {
+                     std::initializer_list<int> projs, int slot_width, const void* norm_g = nullptr,
+                     const void* norm_b = nullptr, void* norm_into = nullptr) -> int {
+    fused_norm = false;
     bool any = false;
     for (int p : projs) any = any || has(p);
     if (!skinny) {
@@ -313,8 +319,12 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
     }
     const int pi = prof_begin(cls, s);
     hipError_t e = launch_gemm_skinny(k, s);
-    if (e == hipSuccess) e = launch_finalize(fa, s);
+    const bool fuse = norm_into != nullptr && epi == EPI_RESID && c.dtype == VFM_BF16 && ldo == N && N <= 8192;
+    if (e == hipSuccess)
+      e = fuse ? launch_finalize_norm(c.dtype, fa, norm_g, norm_b, c.norm, c.norm_eps, norm_into, s)
+               : launch_finalize(fa, s);
     prof_end(pi, s);
+    fused_norm = fuse && e == hipSuccess;
     return hip_status(e);
   };
 
@@ -324,16 +334,23 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
   VFM_TRY(project(VFM_PROF_GEMM_QKV, h, d, w->w_qkv, nullptr, w->b_qkv, 3 * d, EPI_STORE, qkv,
                   3 * d, {VFM_Q, VFM_K, VFM_V}, d));
   // a5: rotary embedding of q and k
+  // (with a KV cache the same pass writes each row's rotated k and its v)
+  const bool cache_write = k_cache != nullptr && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL);
+  const bool rope_writes_kv = c.rope_theta > 0.f && cache_write;
   if (c.rope_theta > 0.f)
-    VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta, s));
+    VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta,
+                                          rope_writes_kv ? k_cache : nullptr, rope_writes_kv ? v_cache : nullptr,
+                                          kv_slots, s));
   // a6: attention per request (and the KV-cache write)
   // (timed per kernel inside the launcher)
-  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, base + ws.aws,
-                           ws.z - ws.aws, max_keys, s));
+  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, rope_writes_kv,
+                           base + ws.aws, ws.z - ws.aws, max_keys, s));
   // a7: output projection + LoRA_o + residual
-  VFM_TRY(project(VFM_PROF_GEMM_O, attn, d, w->w_o, nullptr, w->b_o, d, EPI_RESID, x, d, {VFM_O}, d));
-  // a8: pre-norm 2
-  VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm2_w, w->norm2_b, c.norm, c.norm_eps, h, s));
+  VFM_TRY(project(VFM_PROF_GEMM_O, attn, d, w->w_o, nullptr, w->b_o, d, EPI_RESID, x, d, {VFM_O}, d,
+                  w->norm2_w, w->norm2_b, h));
+  // a8: pre-norm 2 (already done with the residual finalize on small batches)
+  if (!fused_norm)
+    VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm2_w, w->norm2_b, c.norm, c.norm_eps, h, s));
   // a9: MLP up (+ gate) with LoRA and the activation fused
   if (c.mlp == VFM_MLP_SWIGLU)
     VFM_TRY(project(VFM_PROF_GEMM_UP, h, d, w->w_gate, w->w_up, nullptr, f, EPI_SWIGLU, act, f,

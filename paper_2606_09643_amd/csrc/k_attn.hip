@@ -66,7 +66,9 @@ constexpr float NEG_BIG = -1e30f;
 // RoPE, rotate-half: (x_i, x_{i+dh/2}) rotated by pos * theta^(-2i/dh).
 // One block per row: the row's dh/2 angles (they do not depend on the head)
 // go through LDS once, then each thread rotates 8 pairs of one head of q and
-// of k with 16-byte accesses.
+// of k with 16-byte accesses.  With a KV cache the same pass writes the
+// rotated key and the value row to their cache slots (the cache-write kernel
+// is then skipped).
 // ---------------------------------------------------------------------------
 // 8 consecutive elements (16-byte aligned for bf16, 32-byte for fp32) as floats
 template <typename T>
@@ -99,7 +101,8 @@ __device__ inline void store8<float>(float* p, const float (&v)[8]) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv, int d, int H, int dh,
-                                                   float log2_theta) {
+                                                   float log2_theta, T* __restrict__ kc, T* __restrict__ vc,
+                                                   int64_t kv_slots) {
   __shared__ float cs_s[64], sn_s[64];        // dh / 2 <= 64
   const int r = blockIdx.x;
   const int half = dh >> 1;
@@ -113,6 +116,7 @@ __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv,
   __syncthreads();
   const int per_head = half / 8;              // 8-pair groups per head
   T* row = qkv + (int64_t)r * 3 * d;
+  const int64_t slot = kc != nullptr ? (int64_t)pl.kv_start[pl.row_req[r]] + pl.pos[r] : 0;
   for (int w = threadIdx.x; w < 2 * H * per_head; w += blockDim.x) {
     const int part = w / (H * per_head);      // q, then k
     const int hh = (w / per_head) % H;
@@ -130,6 +134,19 @@ __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv,
     }
     store8<T>(x, ya);
     store8<T>(x + half, yb);
+    if (kc != nullptr && part == 1) {         // the rotated key also goes to the cache
+      T* kd = kc + ((int64_t)hh * kv_slots + slot) * dh + i0;
+      store8<T>(kd, ya);
+      store8<T>(kd + half, yb);
+    }
+  }
+  if (kc != nullptr) {                        // and the value row, 8 elements per thread
+    for (int c = 8 * threadIdx.x; c < d; c += 8 * blockDim.x) {
+      const int hh = c / dh;
+      float v[8];
+      load8<T>(row + 2 * d + c, v);
+      store8<T>(vc + ((int64_t)hh * kv_slots + slot) * dh + (c - hh * dh), v);
+    }
   }
 }
 
@@ -146,11 +163,14 @@ __global__ __launch_bounds__(256) void kv_write_kernel(Plan pl, const T* __restr
   const int p = pl.row_req[r];
   const int64_t slot = (int64_t)pl.kv_start[p] + pl.pos[r];
   const T* src = qkv + (int64_t)r * 3 * d;
-  for (int c = threadIdx.x; c < d; c += 256) {
+  for (int c = 8 * threadIdx.x; c < d; c += 8 * 256) {   // 8 elements (16 B bf16) per thread
     const int h = c / dh;
     const int64_t o = ((int64_t)h * kv_slots + slot) * dh + (c - h * dh);
-    kc[o] = src[d + c];
-    vc[o] = src[2 * d + c];
+    float kv8[8];
+    load8<T>(src + d + c, kv8);
+    store8<T>(kc + o, kv8);
+    load8<T>(src + 2 * d + c, kv8);
+    store8<T>(vc + o, kv8);
   }
 }
 
@@ -854,13 +874,15 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const fl
 }  // namespace
 
 hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
-                       float theta, hipStream_t s) {
+                       float theta, void* k_cache, void* v_cache, int64_t kv_slots, hipStream_t s) {
   if (pl.T == 0) return hipSuccess;
   const float l2t = log2f(theta);
   if (dtype == VFM_BF16)
-    hipLaunchKernelGGL(rope_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (bf16*)qkv, d, n_heads, head_dim, l2t);
+    hipLaunchKernelGGL(rope_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (bf16*)qkv, d, n_heads, head_dim, l2t,
+                       (bf16*)k_cache, (bf16*)v_cache, kv_slots);
   else
-    hipLaunchKernelGGL(rope_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (float*)qkv, d, n_heads, head_dim, l2t);
+    hipLaunchKernelGGL(rope_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (float*)qkv, d, n_heads, head_dim, l2t,
+                       (float*)k_cache, (float*)v_cache, kv_slots);
   return hipGetLastError();
 }
 
@@ -871,14 +893,14 @@ size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys) {
 }
 
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv, void* out,
-                            void* k_cache, void* v_cache, int64_t kv_slots, void* ws, size_t ws_bytes,
-                            int max_keys, hipStream_t s) {
+                            void* k_cache, void* v_cache, int64_t kv_slots, bool kv_written, void* ws,
+                            size_t ws_bytes, int max_keys, hipStream_t s) {
   const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
   // timing classes: the attention kernel itself is VFM_PROF_ATTN, the cache
   // write and the decode merge VFM_PROF_OTHER
   int pi = -1;
-  if (k_cache && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
+  if (k_cache && !kv_written && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
     pi = prof_begin(VFM_PROF_OTHER, s);
     if (dtype == VFM_BF16)
       hipLaunchKernelGGL(kv_write_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (const bf16*)qkv, d, DH,

@@ -362,31 +362,6 @@ __global__ __launch_bounds__(256) void lora_expand_z_kernel(Plan pl, ExpandZArgs
 // thread per row and 4 output columns; every load is independent of the
 // others, so the kernel streams the partials.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void add4(float4& a, const float4& b) {
-  a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
-}
-
-__device__ __forceinline__ float4 sum_slices(const float* z, int64_t zs, int ns) {
-  float4 s4[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) s4[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-  int sp = 0;
-  for (; sp + 4 <= ns; sp += 4) {
-    float4 v[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4*>(z + (sp + j) * zs);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) add4(s4[j], v[j]);
-  }
-#pragma unroll
-  for (int j = 0; j < 3; ++j)  // the last ns mod 4 slices
-    if (sp + j < ns) add4(s4[j], *reinterpret_cast<const float4*>(z + (sp + j) * zs));
-  add4(s4[0], s4[1]);
-  add4(s4[2], s4[3]);
-  add4(s4[0], s4[2]);
-  return s4[0];
-}
-
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   const int per_row = a.N / 4;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;

@@ -94,22 +94,20 @@ __device__ inline void norm_row_regs(const float* xr, int d, const TW* g, const 
 // Few rows (decode): one 256-thread block per row, MAXC float4 chunks per
 // thread, block reductions through LDS, so a small batch still keeps every
 // CU busy.
+// Normalise one row held by a 256-thread block (MAXC float4 chunks per
+// thread in v) and store it; block reductions through red.
 template <typename T, int MAXC>
-__global__ __launch_bounds__(256) void norm_rows_block_kernel(const float* __restrict__ x, int d,
-                                                              const T* __restrict__ g,
-                                                              const T* __restrict__ b, int kind,
-                                                              float eps, T* __restrict__ out) {
-  __shared__ float red[2][4];
-  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__device__ inline void norm_block_row(const float4 (&v)[MAXC], int d, const T* __restrict__ g,
+                                      const T* __restrict__ b, int kind, float eps, T* __restrict__ o,
+                                      float (&red)[2][4]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = d >> 2;
-  const float* xr = x + (int64_t)row * d;
-  float4 v[MAXC], gg[MAXC], bb[MAXC];
+  float4 gg[MAXC], bb[MAXC];
   float sum = 0.f;
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
     const int c = tid + 256 * i;
     if (c < nch) {
-      v[i] = *reinterpret_cast<const float4*>(xr + 4 * c);
       gg[i] = load4<T>(g + 4 * c);
       bb[i] = b ? load4<T>(b + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
       sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
@@ -135,7 +133,6 @@ __global__ __launch_bounds__(256) void norm_rows_block_kernel(const float* __res
   if (lane == 0) red[1][wave] = sq;
   __syncthreads();
   const float rstd = rsqrtf(((red[1][0] + red[1][1]) + (red[1][2] + red[1][3])) / (float)d + eps);
-  T* o = out + (int64_t)row * d;
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
     const int c = tid + 256 * i;
@@ -148,6 +145,55 @@ __global__ __launch_bounds__(256) void norm_rows_block_kernel(const float* __res
       store4<T>(o + 4 * c, y);
     }
   }
+}
+
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void norm_rows_block_kernel(const float* __restrict__ x, int d,
+                                                              const T* __restrict__ g,
+                                                              const T* __restrict__ b, int kind,
+                                                              float eps, T* __restrict__ out) {
+  __shared__ float red[2][4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int nch = d >> 2;
+  const float* xr = x + (int64_t)row * d;
+  float4 v[MAXC];
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = tid + 256 * i;
+    v[i] = c < nch ? *reinterpret_cast<const float4*>(xr + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  norm_block_row<T, MAXC>(v, d, g, b, kind, eps, out + (int64_t)row * d, red);
+}
+
+// Residual finalize + pre-norm, one block per row: x += (sum of the partial
+// slices) + bias, then the row is normalised into h.
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, const T* __restrict__ g,
+                                                            const T* __restrict__ b, int kind, float eps,
+                                                            T* __restrict__ h) {
+  __shared__ float red[2][4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int nch = a.N >> 2;
+  const int64_t zs = (int64_t)a.M * a.N;
+  float* xr = (float*)a.out + (int64_t)row * a.ldo;
+  float4 v[MAXC];
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = tid + 256 * i;
+    v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c < nch) {
+      float4 s4 = sum_slices(a.Z + (int64_t)row * a.N + 4 * c, zs, a.nslices);
+      if (a.bias) {
+        const bf16x4 bv = *reinterpret_cast<const bf16x4*>((const bf16*)a.bias + 4 * c);
+        s4.x += (float)bv[0]; s4.y += (float)bv[1]; s4.z += (float)bv[2]; s4.w += (float)bv[3];
+      }
+      float4 xv = *reinterpret_cast<const float4*>(xr + 4 * c);
+      add4(xv, s4);
+      *reinterpret_cast<float4*>(xr + 4 * c) = xv;
+      v[i] = xv;
+    }
+  }
+  norm_block_row<T, MAXC>(v, a.N, g, b, kind, eps, h + (int64_t)row * a.N, red);
 }
 
 template <typename T, int MAXI>
@@ -370,6 +416,16 @@ hipError_t launch_norm(int dtype, const float* x, int T, int d, const void* g, c
     if (mi == 4) NORM_LAUNCH(float, 4); else if (mi == 16) NORM_LAUNCH(float, 16); else NORM_LAUNCH(float, 32);
   }
 #undef NORM_LAUNCH
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize_norm(int dtype, const FinalizeArgs& a, const void* g, const void* b, int kind,
+                                float eps, void* h, hipStream_t s) {
+  if (a.M == 0) return hipSuccess;
+  if (a.epi != EPI_RESID || dtype != VFM_BF16 || a.N % 4 || a.N > 8192 || a.ldo != a.N)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL((finalize_norm_kernel<bf16, 8>), dim3(a.M), dim3(256), 0, s, a, (const bf16*)g,
+                     (const bf16*)b, kind, eps, (bf16*)h);
   return hipGetLastError();
 }
 

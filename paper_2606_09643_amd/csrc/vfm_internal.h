@@ -99,6 +99,34 @@ __device__ inline int block_tile_task(const Plan& pl, int tile, int* slot) {
   return *slot;
 }
 
+__device__ __forceinline__ void add4(float4& a, const float4& b) {
+  a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+}
+
+// Sum of ns fp32 partial slices (stride zs floats) at z, 4 columns, in a
+// fixed order: slice j goes to lane j mod 4 of four running sums, which are
+// then added pairwise.
+__device__ __forceinline__ float4 sum_slices(const float* z, int64_t zs, int ns) {
+  float4 s4[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s4[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+  int sp = 0;
+  for (; sp + 4 <= ns; sp += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4*>(z + (sp + j) * zs);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) add4(s4[j], v[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < 3; ++j)  // the last ns mod 4 slices
+    if (sp + j < ns) add4(s4[j], *reinterpret_cast<const float4*>(z + (sp + j) * zs));
+  add4(s4[0], s4[1]);
+  add4(s4[2], s4[3]);
+  add4(s4[0], s4[2]);
+  return s4[0];
+}
+
 __device__ inline float to_f32(float v) { return v; }
 __device__ inline float to_f32(bf16 v) { return (float)v; }
 template <typename T> __device__ inline T from_f32(float v);
@@ -241,17 +269,25 @@ struct FinalizeArgs {
   void* out; int ldo;
 };
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
+// Residual finalize fused with the next pre-norm (small batches): per row,
+// x += sum of the slices + bias (exactly as launch_finalize with EPI_RESID),
+// then h = Norm(x) as launch_norm.
+hipError_t launch_finalize_norm(int dtype, const FinalizeArgs& a, const void* g, const void* b, int kind,
+                                float eps, void* h, hipStream_t s);
 
-// In-place rotary embedding of the q and k parts of qkv [T, 3d].
+// In-place rotary embedding of the q and k parts of qkv [T, 3d]; with
+// k_cache / v_cache (head-major [n_heads, kv_slots, head_dim]) non-null, each
+// row's rotated k and its v are also written to slot kv_start + pos.
 hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
-                       float theta, hipStream_t s);
+                       float theta, void* k_cache, void* v_cache, int64_t kv_slots, hipStream_t s);
 
 // Attention per request over qkv [T, 3d] (plan order) into out [T, d].
 // Decode needs attention_workspace() bytes of ws; max_keys = the largest
-// ctx + length over the batch's requests.
+// ctx + length over the batch's requests.  kv_written: the rows' K / V are
+// already in the cache (written by the RoPE pass), so no cache write here.
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv,
-                            void* out, void* k_cache, void* v_cache, int64_t kv_slots, void* ws,
-                            size_t ws_bytes, int max_keys, hipStream_t s);
+                            void* out, void* k_cache, void* v_cache, int64_t kv_slots, bool kv_written,
+                            void* ws, size_t ws_bytes, int max_keys, hipStream_t s);
 size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys);
 
 // Input rows into the fp32 residual stream (plan order).
