@@ -16,7 +16,7 @@ from paper_2606_09643_amd import runner as R
 from paper_2606_09643_amd import workloads as wl
 from tests.gpu_common import (expected_embed, log, oracle_heads, oracle_layer_rows, oracle_plan,
                               pick_requests, tol)
-from tests.helpers import np64, oracle_adapter, oracle_weights
+from tests.helpers import np64, oracle_adapter, oracle_weights, spec_of
 
 pytestmark = pytest.mark.gpu
 
@@ -416,3 +416,59 @@ def test_full_size_sampled(idx):
         hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
         log(f"  head max rel err {hw:.3e}")
         assert hw < tol(w)
+
+
+@pytest.mark.parametrize("rope", [True, False])
+def test_prefill_writes_kv_cache(rope):
+    """A causal (prefill) layer given a KV cache writes each row's rotated
+    key and its value at slot kv_start + pos of every head of the head-major
+    cache: with RoPE the rotation pass writes them, without it the cache-write
+    kernel does.  Slots between the requests keep their previous contents.
+    Decoder layer, ragged prompts (1, 130, 64, 77 tokens)."""
+    w = wl.WORKLOADS[4]
+    case = SMALL[4]
+    batch = _batch(w, **case)
+    model = R.Model(w, n_layers=1, b_std=0.1)
+    inp = R.Inputs(w, batch)
+    gap = 3
+    lens = batch.seq_len.astype(np.int64)
+    kvs = np.zeros(batch.n_req, np.int64)
+    kvs[1:] = np.cumsum(lens + gap)[:-1]
+    slots = int((lens + gap).sum())
+    pb = B.Batch(batch.task_id, batch.seq_len, w.n_tasks, ctx_len=np.zeros(batch.n_req, np.int32),
+                 kv_start=kvs.astype(np.int32))
+    fwd = R.Forward(model, pb, inp)
+    cfg = R.cfg_for(w)
+    if not rope:
+        cfg.rope_theta = 0.0
+    sentinel = 7.0
+    kc = torch.full((w.n_heads, slots, w.head_dim), sentinel, dtype=torch.bfloat16, device="cuda")
+    vc = torch.full_like(kc, sentinel)
+    log(f"prefill layer with KV cache, rope={rope}, T={pb.T}, slots={slots}")
+    fwd.embed()
+    x_in = fwd.x.double().cpu().numpy()
+    B.vfm_layer_forward(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, kc, vc, slots, fwd.ws)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    pl = oracle_plan(w, batch)
+    spec = spec_of(w)
+    if not rope:
+        spec["rope_theta"] = 0.0
+    cu = pl["cu_seqlens"]
+    W_np = oracle_weights(model.layers[0])
+    k_all = kc.permute(1, 0, 2).reshape(slots, w.d).double().cpu().numpy()
+    v_all = vc.permute(1, 0, 2).reshape(slots, w.d).double().cpu().numpy()
+    written = np.zeros(slots, bool)
+    worst = 0.0
+    for p in range(batch.n_req):
+        sl = slice(int(cu[p]), int(cu[p + 1]))
+        t = int(pl["task"][p])
+        y, k, v = O.layer(spec, W_np, oracle_adapter(model.adapters[0], t), x_in[sl], pos=pl["pos"][sl])
+        i = int(pl["order"][p])
+        s0, n = int(kvs[i]), int(lens[i])
+        worst = max(worst, O.row_rel_error(got[sl], y), O.row_rel_error(k_all[s0:s0 + n], k),
+                    O.row_rel_error(v_all[s0:s0 + n], v))
+        written[s0:s0 + n] = True
+    log(f"  max row rel err (output, cached k, cached v) {worst:.3e}")
+    assert worst < tol(w)
+    assert np.all(k_all[~written] == sentinel) and np.all(v_all[~written] == sentinel)
