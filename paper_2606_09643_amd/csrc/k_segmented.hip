@@ -258,33 +258,52 @@ __global__ __launch_bounds__(256) void expand_f32_kernel(Plan pl, ExpandArgs a) 
 __global__ __launch_bounds__(256) void heads_bf16_kernel(Plan pl, const bf16* __restrict__ pooled,
                                                          int d, vfm_head_table h,
                                                          float* __restrict__ out) {
+  __shared__ f32x4 red[4][64];
   const int t = blockIdx.x;
   const int n_out = h.n_out[t];
   const int n0 = blockIdx.y * 64;
   const int p0 = pl.seg_req[t], p1 = pl.seg_req[t + 1];
-  if (p0 == p1 || n0 >= n_out) return;
+  if (p0 == p1 || n0 >= n_out) return;                // block-uniform
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const bf16* Wt = (const bf16*)h.W[t];
   const bf16* bt = h.b ? (const bf16*)h.b[t] : nullptr;
-  const int nrow = n0 + wave * 16 + (lane & 15);
-  const bf16* wrow = Wt + (int64_t)min(nrow, n_out - 1) * d + 8 * (lane >> 4);
+  // at most 16 outputs left in this block: the 4 waves split K over the same
+  // 16 rows and add their sums in wave order; otherwise each wave owns 16 rows
+  const bool ksplit = n_out - n0 <= 16 && d % 128 == 0;
+  const int rb = ksplit ? n0 : n0 + wave * 16;        // the wave's first output row
+  const int kq = ksplit ? d / 4 : d;                  // K per wave
+  const int kb = ksplit ? wave * kq : 0;
+  const int nrow = rb + (lane & 15);
+  const bf16* wrow = Wt + (int64_t)min(nrow, n_out - 1) * d + kb + 8 * (lane >> 4);
   for (int pb = p0; pb < p1; pb += 16) {
     const int p = pb + (lane & 15);
-    const bf16* xrow = pooled + (int64_t)min(p, p1 - 1) * d + 8 * (lane >> 4);
+    const bf16* xrow = pooled + (int64_t)min(p, p1 - 1) * d + kb + 8 * (lane >> 4);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-    for (int k = 0; k < d; k += 32) {
+#pragma unroll 8
+    for (int k = 0; k < kq; k += 32) {
       const bf16x8 wf = *reinterpret_cast<const bf16x8*>(wrow + k);
       const bf16x8 xf = *reinterpret_cast<const bf16x8*>(xrow + k);
       acc = mfma16(wf, xf, acc);
     }
-    if (p < p1) {
+    if (ksplit) {
+      red[wave][lane] = acc;
+      __syncthreads();
+      if (wave == 0) {
+#pragma unroll
+        for (int w = 1; w < 4; ++w) {
+          const f32x4 u = red[w][lane];
+          acc[0] += u[0]; acc[1] += u[1]; acc[2] += u[2]; acc[3] += u[3];
+        }
+      }
+      __syncthreads();                                // red is reused by the next group
+    }
+    if (p < p1 && (!ksplit || wave == 0)) {
       const int req = pl.order[p];
       const int lim = min(n_out, pl.out_off[req + 1] - pl.out_off[req]);
       float* o = out + pl.out_off[req];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int n = n0 + wave * 16 + 4 * (lane >> 4) + i;
+        const int n = rb + 4 * (lane >> 4) + i;
         if (n < lim) o[n] = acc[i] + (bt ? (float)bt[n] : 0.f);
       }
     }
