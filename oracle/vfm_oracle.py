@@ -28,9 +28,10 @@ request at a time, in float64:
 The backbone architectures (pre-LN ViT/T5-style encoder; Llama-style decoder
 with RMSNorm, RoPE and SwiGLU) are the standard ones of the backbones the paper
 serves (Table 2); the paper defines none of their arithmetic itself.  Where the
-paper is silent the readings are listed in the design doc (norm epsilons, exact-erf
-GELU, rotate-half RoPE with base 10000, decode attends to ctx cached keys plus
-itself, pooling per workload).
+paper is silent this module takes these readings: LayerNorm eps 1e-5 with the
+biased variance, RMSNorm eps 1e-6, exact-erf GELU, rotate-half RoPE with base
+10000, decode attending to its ctx cached keys plus itself, and pooling per
+workload (mean, first token or the decoded token).
 
 Pins (tests/test_oracle_pins.py): plan vs brute force; merged == unmerged LoRA;
 zero rank / zero B == bare backbone; LoRA closed form on unit vectors; encoder

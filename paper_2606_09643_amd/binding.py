@@ -33,7 +33,9 @@ PROJ = ("q", "k", "v", "o", "gate", "up", "down")
 
 EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size",
            "vfm_embed_forward", "vfm_layer_forward", "vfm_lora_apply", "vfm_head_forward",
-           "vfm_profile_enable", "vfm_profile_read")
+           "vfm_profile_enable", "vfm_profile_read",
+           "vfm_bfq_state_size", "vfm_bfq_init", "vfm_bfq_enqueue", "vfm_bfq_next_batch",
+           "vfm_bfq_queued", "vfm_bfq_tags")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -103,6 +105,14 @@ def _lib_handle():
                                          C.c_void_p]
         lib.vfm_profile_enable.argtypes = [C.c_uint32]
         lib.vfm_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
+        lib.vfm_bfq_state_size.argtypes = [C.POINTER(vfm_bfq_config), C.POINTER(C.c_size_t)]
+        lib.vfm_bfq_init.argtypes = [C.POINTER(vfm_bfq_config), C.c_void_p, C.c_size_t]
+        lib.vfm_bfq_enqueue.argtypes = [C.c_void_p, C.c_int32, C.c_int64, C.c_double, C.c_double]
+        lib.vfm_bfq_next_batch.argtypes = [C.c_void_p, C.c_double, C.c_void_p, C.c_void_p, C.c_int32,
+                                           C.POINTER(C.c_int32)]
+        lib.vfm_bfq_queued.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32)]
+        lib.vfm_bfq_tags.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double),
+                                     C.POINTER(C.c_double)]
         for name in EXPORTS:
             getattr(lib, name).restype = C.c_int if name != "vfm_status_string" else C.c_char_p
         _LIB = lib
@@ -293,3 +303,51 @@ class HeadTable:
         self.pb = torch.tensor([_ptr(b) if b is not None else 0 for b in bs], dtype=torch.int64).to(device)
         self.c = vfm_head_table(len(n_out), pool, int(n_out.max()) if n_out.size else 0,
                                 self.n_out.data_ptr(), self.pw.data_ptr(), self.pb.data_ptr())
+
+
+# ---- batch-aware fair queueing (host scheduler, include/vfm_bfq.h) --------
+class vfm_bfq_config(C.Structure):
+    _fields_ = [("n_tasks", C.c_int32), ("b_max", C.c_int32), ("max_queued", C.c_int32),
+                ("weight", C.POINTER(C.c_double)), ("batch_time", C.POINTER(C.c_double))]
+
+
+class BFQ:
+    """The library's BFQ scheduler on a host state buffer (numpy-owned)."""
+
+    def __init__(self, weights, batch_time, b_max, max_queued=4096):
+        self._w = np.ascontiguousarray(weights, np.float64)
+        self._t = np.ascontiguousarray(batch_time, np.float64)
+        self.b_max = int(b_max)
+        self.cfg = vfm_bfq_config(len(self._w), self.b_max, int(max_queued),
+                                  self._w.ctypes.data_as(C.POINTER(C.c_double)),
+                                  self._t.ctypes.data_as(C.POINTER(C.c_double)))
+        n = C.c_size_t()
+        _check(_lib_handle().vfm_bfq_state_size(C.byref(self.cfg), C.byref(n)), "vfm_bfq_state_size")
+        self.state = np.zeros((n.value + 7) // 8, np.float64)   # 8-byte aligned
+        _check(_lib_handle().vfm_bfq_init(C.byref(self.cfg), self.state.ctypes.data, self.state.nbytes),
+               "vfm_bfq_init")
+        self._req = np.zeros(self.b_max, np.int64)
+        self._task = np.zeros(self.b_max, np.int32)
+
+    def enqueue(self, task, req, arrival, deadline=float("inf")):
+        _check(_lib_handle().vfm_bfq_enqueue(self.state.ctypes.data, int(task), int(req), float(arrival),
+                                             float(deadline)), "vfm_bfq_enqueue")
+
+    def next_batch(self, now):
+        """[(request id, task id)] of the next batch, in admission order."""
+        n = C.c_int32()
+        _check(_lib_handle().vfm_bfq_next_batch(self.state.ctypes.data, float(now), self._req.ctypes.data,
+                                                self._task.ctypes.data, self.b_max, C.byref(n)),
+               "vfm_bfq_next_batch")
+        return [(int(self._req[k]), int(self._task[k])) for k in range(n.value)]
+
+    def queued(self, task):
+        n = C.c_int32()
+        _check(_lib_handle().vfm_bfq_queued(self.state.ctypes.data, int(task), C.byref(n)), "vfm_bfq_queued")
+        return n.value
+
+    def tags(self, task, k):
+        s, f = C.c_double(), C.c_double()
+        _check(_lib_handle().vfm_bfq_tags(self.state.ctypes.data, int(task), int(k), C.byref(s), C.byref(f)),
+               "vfm_bfq_tags")
+        return s.value, f.value
