@@ -183,6 +183,29 @@ typedef struct vfm_head_table {
 
 const char* vfm_status_string(int status);
 
+/* ------------------------------------------------------------------------
+ * Runtime attach / remove of one task's extensions between batches
+ * (Section 4.1 task extensions; Table 1 attach_adapter / remove_adapter,
+ * add_decoder).  Task `task`'s entries of the table's device arrays (which
+ * must be writable) are rewritten by a kernel on `stream`, so the update is
+ * ordered with the forward calls on that stream; the backbone weights and
+ * the other tasks' entries are not touched, nothing is allocated and the
+ * host does not wait.
+ *   vfm_lora_attach: rank 0 removes the task's adapters (entries become
+ *     NULL, rank 0).  Otherwise A, B are host arrays [VFM_NPROJ] of device
+ *     pointers A_t [rank, d_in], B_t [d_out, rank] (NULL for a projection
+ *     the task leaves bare; A and B in pairs).  Errors: VFM_ERR_TASK for a
+ *     task out of range; VFM_ERR_SHAPE for a rank that is not a multiple of 8
+ *     or exceeds table->max_rank; VFM_ERR_ARG for null table arrays, an
+ *     unpaired A / B, or a factor for a projection whose table array is NULL.
+ *   vfm_head_attach: n_out 0 removes the head; W = W_t [n_out, d], b = b_t
+ *     [n_out] or NULL (device).  VFM_ERR_SHAPE for n_out > table->max_out.
+ *     Later batches must give vfm_plan the new n_out. */
+int vfm_lora_attach(const vfm_lora_table* table, int32_t task, int32_t rank, float scale,
+                    const void* const* A, const void* const* B, void* stream);
+int vfm_head_attach(const vfm_head_table* table, int32_t task, int32_t n_out, const void* W,
+                    const void* b, void* stream);
+
 /* Device workspace needed by vfm_layer_forward / vfm_lora_apply /
  * vfm_head_forward for this batch (lora may be NULL). */
 int vfm_workspace_size(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_lora_table* lora,

@@ -35,7 +35,7 @@ EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size
            "vfm_embed_forward", "vfm_layer_forward", "vfm_lora_apply", "vfm_head_forward",
            "vfm_profile_enable", "vfm_profile_read",
            "vfm_bfq_state_size", "vfm_bfq_init", "vfm_bfq_enqueue", "vfm_bfq_next_batch",
-           "vfm_bfq_queued", "vfm_bfq_tags")
+           "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -105,6 +105,10 @@ def _lib_handle():
                                          C.c_void_p]
         lib.vfm_profile_enable.argtypes = [C.c_uint32]
         lib.vfm_profile_read.argtypes = [C.c_void_p, C.c_void_p, C.c_int32]
+        lib.vfm_lora_attach.argtypes = [C.POINTER(vfm_lora_table), C.c_int32, C.c_int32, C.c_float,
+                                        C.c_void_p, C.c_void_p, C.c_void_p]
+        lib.vfm_head_attach.argtypes = [C.POINTER(vfm_head_table), C.c_int32, C.c_int32, C.c_void_p,
+                                        C.c_void_p, C.c_void_p]
         lib.vfm_bfq_state_size.argtypes = [C.POINTER(vfm_bfq_config), C.POINTER(C.c_size_t)]
         lib.vfm_bfq_init.argtypes = [C.POINTER(vfm_bfq_config), C.c_void_p, C.c_size_t]
         lib.vfm_bfq_enqueue.argtypes = [C.c_void_p, C.c_int32, C.c_int64, C.c_double, C.c_double]
@@ -292,6 +296,26 @@ class LoraTable:
             A[p] = pa.data_ptr()
             B[p] = pb.data_ptr()
         self.c = vfm_lora_table(n_tasks, mr, self.rank.data_ptr(), self.scale.data_ptr(), A, B)
+
+
+def vfm_lora_attach(table, task, rank, scale, A=None, B=None, stream=None):
+    """Rewrites task `task`'s adapter entries of a LoRA table (rank 0 removes
+    them).  A, B: {proj name: device tensor} of the task's factors."""
+    a = (C.c_void_p * VFM_NPROJ)()
+    b = (C.c_void_p * VFM_NPROJ)()
+    for p, name in enumerate(PROJ):
+        if A is not None and name in A:
+            a[p] = _ptr(A[name])
+            b[p] = _ptr(B[name])
+    st = _lib_handle().vfm_lora_attach(C.byref(table.c), int(task), int(rank), float(scale),
+                                       C.cast(a, C.c_void_p), C.cast(b, C.c_void_p), _stream(stream))
+    _check(st, "vfm_lora_attach")
+
+
+def vfm_head_attach(table, task, n_out, W=None, b=None, stream=None):
+    st = _lib_handle().vfm_head_attach(C.byref(table.c), int(task), int(n_out), _ptr(W), _ptr(b),
+                                       _stream(stream))
+    _check(st, "vfm_head_attach")
 
 
 class HeadTable:

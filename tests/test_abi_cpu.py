@@ -141,3 +141,33 @@ def test_binding_constants_match_header():
     defs = dict(re.findall(r"#define\s+(VFM_\w+)\s+(\d+)", src))
     for name in ("VFM_PLAN_HEADER", "VFM_ROW_TILE", "VFM_SMALL_BATCH_ROWS"):
         assert int(defs[name]) == getattr(B, name), name
+
+
+def test_attach_rejects_bad_arguments_before_launching():
+    """Argument errors of the runtime attach calls are found on the host (no
+    GPU needed: nothing is launched when a check fails)."""
+    lib = B.lib()
+    fake = 0x10000                      # never dereferenced on these paths
+    A = (B.C.c_void_p * B.VFM_NPROJ)()
+    Bp = (B.C.c_void_p * B.VFM_NPROJ)()
+    A[0] = fake
+    Bp[0] = fake
+    tab = B.vfm_lora_table(4, 16, fake, fake, (B.C.c_void_p * B.VFM_NPROJ)(fake, 0, 0, 0, 0, 0, 0),
+                           (B.C.c_void_p * B.VFM_NPROJ)(fake, 0, 0, 0, 0, 0, 0))
+    at = lambda t, r, a=A, b=Bp: lib.vfm_lora_attach(B.C.byref(tab), t, r, 1.0, B.C.cast(a, B.C.c_void_p),
+                                                     B.C.cast(b, B.C.c_void_p), None)
+    assert at(4, 8) == B.VFM_ERR_TASK
+    assert at(-1, 8) == B.VFM_ERR_TASK
+    assert at(0, 12) == B.VFM_ERR_SHAPE          # not a multiple of 8
+    assert at(0, 24) == B.VFM_ERR_SHAPE          # above max_rank
+    A2 = (B.C.c_void_p * B.VFM_NPROJ)(fake, fake, 0, 0, 0, 0, 0)
+    B2 = (B.C.c_void_p * B.VFM_NPROJ)(fake, fake, 0, 0, 0, 0, 0)
+    assert at(0, 8, A2, B2) == B.VFM_ERR_ARG     # projection 1 has no table array
+    B3 = (B.C.c_void_p * B.VFM_NPROJ)(0, 0, 0, 0, 0, 0, 0)
+    assert at(0, 8, A, B3) == B.VFM_ERR_ARG      # A without B
+    assert lib.vfm_lora_attach(None, 0, 0, 0.0, None, None, None) == B.VFM_ERR_ARG
+    ht = B.vfm_head_table(4, B.VFM_POOL_MEAN, 10, fake, fake, 0)
+    assert lib.vfm_head_attach(B.C.byref(ht), 4, 5, fake, None, None) == B.VFM_ERR_TASK
+    assert lib.vfm_head_attach(B.C.byref(ht), 0, 11, fake, None, None) == B.VFM_ERR_SHAPE
+    assert lib.vfm_head_attach(B.C.byref(ht), 0, 5, None, None, None) == B.VFM_ERR_ARG
+    assert lib.vfm_head_attach(B.C.byref(ht), 0, 5, fake, fake, None) == B.VFM_ERR_ARG   # no bias array

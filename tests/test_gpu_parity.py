@@ -472,3 +472,94 @@ def test_prefill_writes_kv_cache(rope):
     log(f"  max row rel err (output, cached k, cached v) {worst:.3e}")
     assert worst < tol(w)
     assert np.all(k_all[~written] == sentinel) and np.all(v_all[~written] == sentinel)
+
+
+def test_attach_and_remove_adapter_between_batches():
+    """Task extensions are replaced at run time without touching the
+    backbone: vfm_lora_attach gives task 5 a new rank-8 adapter, then removes
+    it.  After each change the task's rows match the oracle with its new
+    adapter (or the bare backbone), and every other task's rows stay
+    bit-identical to the first run.  ViT-B layer, tasks 5, 0, 5, 2, 9, 0."""
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(2, n_layers=1, b_std=0.1)
+    fwd.embed()
+    x0 = fwd.x.clone()
+    x_in = x0.double().cpu().numpy()
+    spec = spec_of(w)
+    W_np = oracle_weights(model.layers[0])
+    cu = pl["cu_seqlens"]
+    tasks = [int(pl["task"][p]) for p in range(batch.n_req)]
+
+    def run():
+        fwd.x.copy_(x0)
+        fwd.layer(0)
+        torch.cuda.synchronize()
+        return fwd.x.double().cpu().numpy()
+
+    first = run()
+    g = torch.Generator(device="cuda").manual_seed(11)
+    r, sc = 8, 1.5
+    A = {p: (torch.randn(r, w.d, generator=g, device="cuda") / w.d ** 0.5).to(torch.bfloat16)
+         for p in ("q", "k", "v", "o")}
+    Bm = {p: (0.1 * torch.randn(w.d, r, generator=g, device="cuda")).to(torch.bfloat16)
+          for p in ("q", "k", "v", "o")}
+    new_ad = {p: (np64(A[p]), np64(Bm[p]), sc) for p in A}
+    for stage, ad5 in (("attach", new_ad), ("remove", None)):
+        if ad5 is None:
+            B.vfm_lora_attach(model.lora[0], 5, 0, 0.0)
+        else:
+            B.vfm_lora_attach(model.lora[0], 5, r, sc, A, Bm)
+        got = run()
+        worst = 0.0
+        for p in range(batch.n_req):
+            sl = slice(int(cu[p]), int(cu[p + 1]))
+            if tasks[p] == 5:
+                y = O.layer(spec, W_np, ad5, x_in[sl], pos=pl["pos"][sl])[0]
+                worst = max(worst, O.row_rel_error(got[sl], y))
+            else:
+                assert np.array_equal(got[sl], first[sl]), (stage, p)
+        log(f"  {stage}: task 5 max row rel err {worst:.3e}")
+        assert worst < tol(w)
+    # cost of one table update (host call + its one-thread kernel)
+    import time
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(200):
+        B.vfm_lora_attach(model.lora[0], 5, r if i % 2 else 0, sc, A, Bm)
+    torch.cuda.synchronize()
+    log(f"  attach / remove: {(time.perf_counter() - t0) / 200 * 1e6:.1f} us per call")
+
+
+def test_attach_head_between_batches():
+    """vfm_head_attach swaps task 2's head for a new 17-output one: the next
+    batch (planned with the new width) gives the oracle's logits for task 2
+    and the unchanged ones for the other tasks."""
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(2, n_layers=1)
+    out_a = fwd().cpu().numpy()
+    x_fin = fwd.x.double().cpu().numpy()
+    n_out = model.heads.n_out.copy()
+    g = torch.Generator(device="cuda").manual_seed(5)
+    Wn = (torch.randn(17, w.d, generator=g, device="cuda") / w.d ** 0.5).to(torch.bfloat16)
+    bn = (0.02 * torch.randn(17, generator=g, device="cuda")).to(torch.bfloat16)
+    B.vfm_head_attach(model.head_tab, 2, 17, Wn, bn)
+    n_out[2] = 17
+    pb2 = B.Batch(batch.task_id, batch.seq_len, w.n_tasks, n_out=n_out)
+    fwd2 = R.Forward(model, pb2, inp)
+    fwd2.x.copy_(fwd.x)
+    fwd2.head()
+    torch.cuda.synchronize()
+    out_b = fwd2.out.cpu().numpy()
+    heads_np = [(np64(model.heads.W[t]), np64(model.heads.b[t])) for t in range(w.n_tasks)]
+    heads_np[2] = (np64(Wn), np64(bn))
+    pl2 = oracle_plan(w, batch, n_out)
+    off_a, off_b = pl["logit_off"], pl2["logit_off"]
+    for i in range(batch.n_req):
+        t = int(batch.task_id[i])
+        ob = out_b[off_b[i]:off_b[i + 1]]
+        if t == 2:
+            p = int(np.nonzero(pl2["order"] == i)[0][0])
+            sl = slice(int(pl2["cu_seqlens"][p]), int(pl2["cu_seqlens"][p + 1]))
+            xn = O.final(spec_of(w), np64(model.final["w"]), np64(model.final["b"]), x_fin[sl])
+            ref = O.head(O.pool(xn, w.pool), heads_np[2][0], heads_np[2][1])
+            assert len(ob) == 17 and O.row_rel_error(ob[None], ref[None]) < tol(w)
+        else:
+            assert np.array_equal(ob, out_a[off_a[i]:off_a[i + 1]])
