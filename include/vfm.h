@@ -171,14 +171,23 @@ typedef struct vfm_lora_table {
   const void* const* B[VFM_NPROJ];  /* device [n_tasks] -> B_t [d_out, rank_t] */
 } vfm_lora_table;
 
-/* Per-task linear heads (the vFM's decoder, Section 2.2). */
+/* Per-task decoder heads (the vFM's decoder, Section 2.2): linear, or a
+ * two-layer MLP (the MLP decoders of Section 4.3's pipeline example):
+ *   linear:  out = W_t pooled + b_t
+ *   MLP:     out = W_t act(W1_t pooled + b1_t) + b_t
+ * A task has an MLP head when W1 is non-NULL and its entry W1[t] is. */
+enum { VFM_ACT_GELU = 0, VFM_ACT_RELU = 1 };
 typedef struct vfm_head_table {
   int32_t n_tasks;
   int32_t pool;                /* VFM_POOL_MEAN | VFM_POOL_FIRST | VFM_POOL_LAST */
   int32_t max_out;             /* >= every n_out[t] */
   const int32_t* n_out;        /* device [n_tasks]; must equal the n_out given to vfm_plan */
-  const void* const* W;        /* device [n_tasks] -> W_t [n_out_t, d] */
+  const void* const* W;        /* device [n_tasks] -> W_t [n_out_t, d] (linear) or [n_out_t, hidden] (MLP) */
   const void* const* b;        /* device [n_tasks] -> b_t [n_out_t], entries may be NULL */
+  int32_t hidden;              /* MLP heads' hidden width: a multiple of 64, <= d; 0 without MLP heads */
+  int32_t act;                 /* VFM_ACT_GELU (exact erf form) | VFM_ACT_RELU */
+  const void* const* W1;       /* device [n_tasks] -> W1_t [hidden, d], NULL entries = linear head; or NULL */
+  const void* const* b1;       /* device [n_tasks] -> b1_t [hidden], entries may be NULL; or NULL */
 } vfm_head_table;
 
 const char* vfm_status_string(int status);
@@ -198,13 +207,16 @@ const char* vfm_status_string(int status);
  *     task out of range; VFM_ERR_SHAPE for a rank that is not a multiple of 8
  *     or exceeds table->max_rank; VFM_ERR_ARG for null table arrays, an
  *     unpaired A / B, or a factor for a projection whose table array is NULL.
- *   vfm_head_attach: n_out 0 removes the head; W = W_t [n_out, d], b = b_t
- *     [n_out] or NULL (device).  VFM_ERR_SHAPE for n_out > table->max_out.
+ *   vfm_head_attach: n_out 0 removes the head; W = W_t, b = b_t [n_out] or
+ *     NULL (device); W1 = W1_t [hidden, d] and b1 = b1_t [hidden] (or NULL)
+ *     make it an MLP head (W_t is then [n_out, hidden]), W1 = NULL a linear
+ *     one (W_t [n_out, d]).  VFM_ERR_SHAPE for n_out > table->max_out;
+ *     VFM_ERR_ARG for a bias or MLP layer the table has no array for.
  *     Later batches must give vfm_plan the new n_out. */
 int vfm_lora_attach(const vfm_lora_table* table, int32_t task, int32_t rank, float scale,
                     const void* const* A, const void* const* B, void* stream);
 int vfm_head_attach(const vfm_head_table* table, int32_t task, int32_t n_out, const void* W,
-                    const void* b, void* stream);
+                    const void* b, const void* W1, const void* b1, void* stream);
 
 /* Device workspace needed by vfm_layer_forward / vfm_lora_apply /
  * vfm_head_forward for this batch (lora may be NULL). */

@@ -279,6 +279,15 @@ def head(pooled, W, b):
     return linear(pooled[None, :], W, b)[0]
 
 
+def head_mlp(pooled, W1, b1, W, b, act="gelu"):
+    """Task-specific two-layer MLP decoder head (Section 4.3's pipeline
+    example: an MLP decoder with a hidden width on the backbone output):
+    act(pooled W1^T + b1) W^T + b, act the exact-erf GELU or ReLU."""
+    h = linear(pooled[None, :], W1, b1)
+    h = gelu(h) if act == "gelu" else np.maximum(h, 0.0)
+    return linear(h, W, b)[0]
+
+
 def final(spec, fn_w, fn_b, x):
     return norm(x, fn_w, fn_b, spec["norm"], spec["eps"])
 

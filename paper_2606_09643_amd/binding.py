@@ -25,6 +25,7 @@ VFM_MLP_GELU, VFM_MLP_SWIGLU = 0, 1
 VFM_ATTN_BIDIR, VFM_ATTN_CAUSAL, VFM_ATTN_DECODE = 0, 1, 2
 VFM_POOL_MEAN, VFM_POOL_FIRST, VFM_POOL_LAST = 0, 1, 2
 VFM_EMBED_ROWS, VFM_EMBED_TOKENS, VFM_EMBED_PATCHES = 0, 1, 2
+VFM_ACT_GELU, VFM_ACT_RELU = 0, 1
 VFM_NPROJ = 7
 VFM_PLAN_HEADER = 16
 VFM_ROW_TILE = 64
@@ -70,7 +71,8 @@ class vfm_lora_table(C.Structure):
 
 class vfm_head_table(C.Structure):
     _fields_ = [("n_tasks", C.c_int32), ("pool", C.c_int32), ("max_out", C.c_int32),
-                ("n_out", C.c_void_p), ("W", C.c_void_p), ("b", C.c_void_p)]
+                ("n_out", C.c_void_p), ("W", C.c_void_p), ("b", C.c_void_p),
+                ("hidden", C.c_int32), ("act", C.c_int32), ("W1", C.c_void_p), ("b1", C.c_void_p)]
 
 
 _LIB = None
@@ -108,7 +110,7 @@ def _lib_handle():
         lib.vfm_lora_attach.argtypes = [C.POINTER(vfm_lora_table), C.c_int32, C.c_int32, C.c_float,
                                         C.c_void_p, C.c_void_p, C.c_void_p]
         lib.vfm_head_attach.argtypes = [C.POINTER(vfm_head_table), C.c_int32, C.c_int32, C.c_void_p,
-                                        C.c_void_p, C.c_void_p]
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
         lib.vfm_bfq_state_size.argtypes = [C.POINTER(vfm_bfq_config), C.POINTER(C.c_size_t)]
         lib.vfm_bfq_init.argtypes = [C.POINTER(vfm_bfq_config), C.c_void_p, C.c_size_t]
         lib.vfm_bfq_enqueue.argtypes = [C.c_void_p, C.c_int32, C.c_int64, C.c_double, C.c_double]
@@ -312,21 +314,31 @@ def vfm_lora_attach(table, task, rank, scale, A=None, B=None, stream=None):
     _check(st, "vfm_lora_attach")
 
 
-def vfm_head_attach(table, task, n_out, W=None, b=None, stream=None):
+def vfm_head_attach(table, task, n_out, W=None, b=None, W1=None, b1=None, stream=None):
     st = _lib_handle().vfm_head_attach(C.byref(table.c), int(task), int(n_out), _ptr(W), _ptr(b),
-                                       _stream(stream))
+                                       _ptr(W1), _ptr(b1), _stream(stream))
     _check(st, "vfm_head_attach")
 
 
 class HeadTable:
-    def __init__(self, n_out, Ws, bs, pool, device="cuda"):
+    """Device tables of per-task heads.  W1s / b1s (optional): per task the
+    MLP head's first layer [hidden, d] / [hidden] (None = linear head)."""
+
+    def __init__(self, n_out, Ws, bs, pool, device="cuda", W1s=None, b1s=None, hidden=0,
+                 act=VFM_ACT_GELU):
         n_out = np.asarray(n_out, np.int32)
         self.n_out = torch.from_numpy(n_out).to(device)
-        self._keep = [Ws, bs]
-        self.pw = torch.tensor([_ptr(w) if w is not None else 0 for w in Ws], dtype=torch.int64).to(device)
-        self.pb = torch.tensor([_ptr(b) if b is not None else 0 for b in bs], dtype=torch.int64).to(device)
+        self._keep = [Ws, bs, W1s, b1s]
+        ptrs = lambda xs: torch.tensor([_ptr(x) if x is not None else 0 for x in xs],
+                                       dtype=torch.int64).to(device)
+        self.pw, self.pb = ptrs(Ws), ptrs(bs)
+        self.pw1 = ptrs(W1s) if W1s is not None else None
+        self.pb1 = ptrs(b1s) if b1s is not None else None
         self.c = vfm_head_table(len(n_out), pool, int(n_out.max()) if n_out.size else 0,
-                                self.n_out.data_ptr(), self.pw.data_ptr(), self.pb.data_ptr())
+                                self.n_out.data_ptr(), self.pw.data_ptr(), self.pb.data_ptr(),
+                                int(hidden), int(act),
+                                self.pw1.data_ptr() if self.pw1 is not None else None,
+                                self.pb1.data_ptr() if self.pb1 is not None else None)
 
 
 # ---- batch-aware fair queueing (host scheduler, include/vfm_bfq.h) --------

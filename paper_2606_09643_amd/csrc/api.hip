@@ -105,8 +105,9 @@ LayerWs layer_ws(const vfm_cfg& c, const Plan& pl, const vfm_lora_table* l, int 
   return w;
 }
 
+// pooled rows, then room for the MLP heads' hidden rows (hidden <= d)
 size_t head_ws(const vfm_cfg& c, const Plan& pl) {
-  return align_up((size_t)pl.n_req * c.d_model * elem_size(c.dtype));
+  return 2 * align_up((size_t)pl.n_req * c.d_model * elem_size(c.dtype));
 }
 
 inline int hip_status(hipError_t e) { return e == hipSuccess ? VFM_OK : VFM_ERR_HIP; }
@@ -409,6 +410,10 @@ extern "C" int vfm_head_forward(const vfm_cfg* cfg, const void* final_norm_w,
   if (heads->n_tasks != pl.n_tasks || !heads->n_out || !heads->W) return VFM_ERR_ARG;
   if (heads->pool < VFM_POOL_MEAN || heads->pool > VFM_POOL_LAST) return VFM_ERR_ARG;
   if (heads->max_out < 0) return VFM_ERR_SHAPE;
+  if (heads->W1) {
+    if (heads->hidden < 64 || heads->hidden % 64 || heads->hidden > c.d_model) return VFM_ERR_SHAPE;
+    if (heads->act != VFM_ACT_GELU && heads->act != VFM_ACT_RELU) return VFM_ERR_ARG;
+  }
   if ((size_t)c.d_model * elem_size(c.dtype) > 64 * 1024) return VFM_ERR_UNSUPPORTED;
   const size_t need = head_ws(c, pl);
   if (!workspace || ws_bytes < need || ((uintptr_t)workspace % ALIGN)) return VFM_ERR_WORKSPACE;

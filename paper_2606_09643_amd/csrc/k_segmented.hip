@@ -255,29 +255,39 @@ __global__ __launch_bounds__(256) void expand_f32_kernel(Plan pl, ExpandArgs a) 
 // One block per (task, 64-column chunk); the block walks the task's
 // requests 16 at a time; each wave owns 16 of the 64 columns.
 // ---------------------------------------------------------------------------
+// Head GEMMs of one task's requests.  HID: the MLP heads' first layer,
+// hid[p, n] = act(pooled[p] . W1_t[n] + b1_t[n]) for tasks with an MLP head;
+// otherwise the output layer, out = in[p] . W_t[n] + b_t[n] with `in` the
+// pooled row (linear head) or the hidden row (MLP head).
+template <bool HID>
 __global__ __launch_bounds__(256) void heads_bf16_kernel(Plan pl, const bf16* __restrict__ pooled,
-                                                         int d, vfm_head_table h,
+                                                         int d, vfm_head_table h, bf16* __restrict__ hid,
                                                          float* __restrict__ out) {
   __shared__ f32x4 red[4][64];
   const int t = blockIdx.x;
-  const int n_out = h.n_out[t];
+  const bool mlp = h.W1 != nullptr && h.W1[t] != nullptr;
+  if (HID && !mlp) return;                            // block-uniform
+  const int n_out = HID ? h.hidden : h.n_out[t];
   const int n0 = blockIdx.y * 64;
   const int p0 = pl.seg_req[t], p1 = pl.seg_req[t + 1];
   if (p0 == p1 || n0 >= n_out) return;                // block-uniform
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const bf16* Wt = (const bf16*)h.W[t];
-  const bf16* bt = h.b ? (const bf16*)h.b[t] : nullptr;
+  const bf16* Wt = (const bf16*)(HID ? h.W1[t] : h.W[t]);
+  const bf16* bt = HID ? (h.b1 ? (const bf16*)h.b1[t] : nullptr) : (h.b ? (const bf16*)h.b[t] : nullptr);
+  const bool from_hid = !HID && mlp;
+  const int K = from_hid ? h.hidden : d;
+  const bf16* in = from_hid ? hid : pooled;
   // at most 16 outputs left in this block: the 4 waves split K over the same
   // 16 rows and add their sums in wave order; otherwise each wave owns 16 rows
-  const bool ksplit = n_out - n0 <= 16 && d % 128 == 0;
+  const bool ksplit = n_out - n0 <= 16 && K % 128 == 0;
   const int rb = ksplit ? n0 : n0 + wave * 16;        // the wave's first output row
-  const int kq = ksplit ? d / 4 : d;                  // K per wave
+  const int kq = ksplit ? K / 4 : K;                  // K per wave
   const int kb = ksplit ? wave * kq : 0;
   const int nrow = rb + (lane & 15);
-  const bf16* wrow = Wt + (int64_t)min(nrow, n_out - 1) * d + kb + 8 * (lane >> 4);
+  const bf16* wrow = Wt + (int64_t)min(nrow, n_out - 1) * K + kb + 8 * (lane >> 4);
   for (int pb = p0; pb < p1; pb += 16) {
     const int p = pb + (lane & 15);
-    const bf16* xrow = pooled + (int64_t)min(p, p1 - 1) * d + kb + 8 * (lane >> 4);
+    const bf16* xrow = in + (int64_t)min(p, p1 - 1) * K + kb + 8 * (lane >> 4);
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
     for (int k = 0; k < kq; k += 32) {
@@ -298,35 +308,56 @@ __global__ __launch_bounds__(256) void heads_bf16_kernel(Plan pl, const bf16* __
       __syncthreads();                                // red is reused by the next group
     }
     if (p < p1 && (!ksplit || wave == 0)) {
-      const int req = pl.order[p];
-      const int lim = min(n_out, pl.out_off[req + 1] - pl.out_off[req]);
-      float* o = out + pl.out_off[req];
+      if (HID) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int n = rb + 4 * (lane >> 4) + i;
-        if (n < lim) o[n] = acc[i] + (bt ? (float)bt[n] : 0.f);
+        for (int i = 0; i < 4; ++i) {
+          const int n = rb + 4 * (lane >> 4) + i;
+          const float v = acc[i] + (bt ? (float)bt[n] : 0.f);
+          hid[(int64_t)p * h.hidden + n] = (bf16)(h.act == VFM_ACT_RELU ? fmaxf(v, 0.f) : gelu_fast(v));
+        }
+      } else {
+        const int req = pl.order[p];
+        const int lim = min(n_out, pl.out_off[req + 1] - pl.out_off[req]);
+        float* o = out + pl.out_off[req];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int n = rb + 4 * (lane >> 4) + i;
+          if (n < lim) o[n] = acc[i] + (bt ? (float)bt[n] : 0.f);
+        }
       }
     }
   }
 }
 
+template <bool HID>
 __global__ __launch_bounds__(256) void heads_f32_kernel(Plan pl, const float* __restrict__ pooled,
-                                                        int d, vfm_head_table h,
+                                                        int d, vfm_head_table h, float* __restrict__ hid,
                                                         float* __restrict__ out) {
   const int t = blockIdx.x;
-  const int n_out = h.n_out[t];
+  const bool mlp = h.W1 != nullptr && h.W1[t] != nullptr;
+  if (HID && !mlp) return;
+  const int n_out = HID ? h.hidden : h.n_out[t];
   const int n0 = blockIdx.y * 64;
   const int p0 = pl.seg_req[t], p1 = pl.seg_req[t + 1];
   if (p0 == p1 || n0 >= n_out) return;
-  const float* Wt = (const float*)h.W[t];
-  const float* bt = h.b ? (const float*)h.b[t] : nullptr;
+  const float* Wt = (const float*)(HID ? h.W1[t] : h.W[t]);
+  const float* bt = HID ? (h.b1 ? (const float*)h.b1[t] : nullptr) : (h.b ? (const float*)h.b[t] : nullptr);
+  const bool from_hid = !HID && mlp;
+  const int K = from_hid ? h.hidden : d;
+  const float* in = from_hid ? hid : pooled;
   for (int e = threadIdx.x; e < (p1 - p0) * 64; e += 256) {
     const int p = p0 + e / 64, n = n0 + e % 64;
-    const int req = pl.order[p];
-    if (n >= min(n_out, pl.out_off[req + 1] - pl.out_off[req])) continue;
+    if (n >= n_out) continue;
     float s = bt ? bt[n] : 0.f;
-    for (int k = 0; k < d; ++k) s += pooled[(int64_t)p * d + k] * Wt[(int64_t)n * d + k];
-    out[pl.out_off[req] + n] = s;
+    for (int k = 0; k < K; ++k) s += in[(int64_t)p * K + k] * Wt[(int64_t)n * K + k];
+    if (HID) {
+      hid[(int64_t)p * h.hidden + n] =
+          h.act == VFM_ACT_RELU ? fmaxf(s, 0.f) : 0.5f * s * (1.f + erff(s * 0.70710678118654752440f));
+    } else {
+      const int req = pl.order[p];
+      if (n >= min(n_out, pl.out_off[req + 1] - pl.out_off[req])) continue;
+      out[pl.out_off[req] + n] = s;
+    }
   }
 }
 
@@ -358,13 +389,28 @@ hipError_t launch_lora_expand(int dtype, const Plan& pl, const ExpandArgs& a, hi
   return hipGetLastError();
 }
 
+// The pooled rows sit at the start of the head workspace; the MLP heads'
+// hidden rows follow at the next 256-byte boundary ([n_req, hidden]).
 hipError_t launch_heads(int dtype, const Plan& pl, const void* pooled, int d,
                         const vfm_head_table& h, float* out, hipStream_t s) {
+  const size_t es = dtype == VFM_BF16 ? 2 : 4;
+  char* hid = (char*)pooled + (((size_t)pl.n_req * d * es + 255) & ~(size_t)255);
+  if (h.W1 && h.hidden > 0) {
+    dim3 g1(h.n_tasks, (h.hidden + 63) / 64);
+    if (dtype == VFM_BF16)
+      hipLaunchKernelGGL((heads_bf16_kernel<true>), g1, dim3(256), 0, s, pl, (const bf16*)pooled, d, h,
+                         (bf16*)hid, out);
+    else
+      hipLaunchKernelGGL((heads_f32_kernel<true>), g1, dim3(256), 0, s, pl, (const float*)pooled, d, h,
+                         (float*)hid, out);
+  }
   dim3 grid(h.n_tasks, (h.max_out + 63) / 64);
-  if (grid.y == 0) return hipSuccess;
+  if (grid.y == 0) return hipGetLastError();
   if (dtype == VFM_BF16)
-    hipLaunchKernelGGL(heads_bf16_kernel, grid, dim3(256), 0, s, pl, (const bf16*)pooled, d, h, out);
+    hipLaunchKernelGGL((heads_bf16_kernel<false>), grid, dim3(256), 0, s, pl, (const bf16*)pooled, d, h,
+                       (bf16*)hid, out);
   else
-    hipLaunchKernelGGL(heads_f32_kernel, grid, dim3(256), 0, s, pl, (const float*)pooled, d, h, out);
+    hipLaunchKernelGGL((heads_f32_kernel<false>), grid, dim3(256), 0, s, pl, (const float*)pooled, d, h,
+                       (float*)hid, out);
   return hipGetLastError();
 }

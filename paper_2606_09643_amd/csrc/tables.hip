@@ -32,15 +32,21 @@ struct HeadEntry {
   int32_t* n_out;
   const void** W;
   const void** b;
+  const void** W1;
+  const void** b1;
   int32_t task, new_n_out;
   const void* w_new;
   const void* b_new;
+  const void* w1_new;
+  const void* b1_new;
 };
 
 __global__ void head_attach_kernel(HeadEntry e) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   e.W[e.task] = e.w_new;
   if (e.b) e.b[e.task] = e.b_new;
+  if (e.W1) e.W1[e.task] = e.w1_new;
+  if (e.b1) e.b1[e.task] = e.b1_new;
   e.n_out[e.task] = e.new_n_out;
 }
 
@@ -72,20 +78,27 @@ extern "C" int vfm_lora_attach(const vfm_lora_table* table, int32_t task, int32_
 }
 
 extern "C" int vfm_head_attach(const vfm_head_table* table, int32_t task, int32_t n_out, const void* W,
-                               const void* b, void* stream) {
+                               const void* b, const void* W1, const void* b1, void* stream) {
   if (!table || !table->n_out || !table->W) return VFM_ERR_ARG;
   if (task < 0 || task >= table->n_tasks) return VFM_ERR_TASK;
   if (n_out < 0 || n_out > table->max_out) return VFM_ERR_SHAPE;
   if (n_out > 0 && !W) return VFM_ERR_ARG;
   if (b && !table->b) return VFM_ERR_ARG;
+  if ((W1 || b1) && !table->W1) return VFM_ERR_ARG;   // MLP head without MLP tables
+  if (b1 && !table->b1) return VFM_ERR_ARG;
+  if (b1 && !W1) return VFM_ERR_ARG;
   HeadEntry e = {};
   e.n_out = const_cast<int32_t*>(table->n_out);
   e.W = const_cast<const void**>(table->W);
   e.b = const_cast<const void**>(table->b);
+  e.W1 = const_cast<const void**>(table->W1);
+  e.b1 = const_cast<const void**>(table->b1);
   e.task = task;
   e.new_n_out = n_out;
   e.w_new = n_out > 0 ? W : nullptr;
   e.b_new = n_out > 0 ? b : nullptr;
+  e.w1_new = n_out > 0 ? W1 : nullptr;
+  e.b1_new = n_out > 0 ? b1 : nullptr;
   hipLaunchKernelGGL(head_attach_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, e);
   return hipGetLastError() == hipSuccess ? VFM_OK : VFM_ERR_HIP;
 }

@@ -166,8 +166,10 @@ def test_attach_rejects_bad_arguments_before_launching():
     B3 = (B.C.c_void_p * B.VFM_NPROJ)(0, 0, 0, 0, 0, 0, 0)
     assert at(0, 8, A, B3) == B.VFM_ERR_ARG      # A without B
     assert lib.vfm_lora_attach(None, 0, 0, 0.0, None, None, None) == B.VFM_ERR_ARG
-    ht = B.vfm_head_table(4, B.VFM_POOL_MEAN, 10, fake, fake, 0)
-    assert lib.vfm_head_attach(B.C.byref(ht), 4, 5, fake, None, None) == B.VFM_ERR_TASK
-    assert lib.vfm_head_attach(B.C.byref(ht), 0, 11, fake, None, None) == B.VFM_ERR_SHAPE
-    assert lib.vfm_head_attach(B.C.byref(ht), 0, 5, None, None, None) == B.VFM_ERR_ARG
-    assert lib.vfm_head_attach(B.C.byref(ht), 0, 5, fake, fake, None) == B.VFM_ERR_ARG   # no bias array
+    ht = B.vfm_head_table(4, B.VFM_POOL_MEAN, 10, fake, fake, 0, 0, 0, None, None)
+    ha = lambda t, n, W, b, W1=None, b1=None: lib.vfm_head_attach(B.C.byref(ht), t, n, W, b, W1, b1, None)
+    assert ha(4, 5, fake, None) == B.VFM_ERR_TASK
+    assert ha(0, 11, fake, None) == B.VFM_ERR_SHAPE
+    assert ha(0, 5, None, None) == B.VFM_ERR_ARG
+    assert ha(0, 5, fake, fake) == B.VFM_ERR_ARG          # no bias array
+    assert ha(0, 5, fake, None, fake) == B.VFM_ERR_ARG    # MLP layer without MLP tables

@@ -563,3 +563,67 @@ def test_attach_head_between_batches():
             assert len(ob) == 17 and O.row_rel_error(ob[None], ref[None]) < tol(w)
         else:
             assert np.array_equal(ob, out_a[off_a[i]:off_a[i + 1]])
+
+
+@pytest.mark.parametrize("idx,act", [(3, B.VFM_ACT_GELU), (1, B.VFM_ACT_RELU)])
+def test_mlp_decoder_heads(idx, act):
+    """Per-task two-layer MLP decoder heads (hidden width 128) mixed with
+    linear ones in one batch: every request's outputs against the oracle's
+    act(pooled W1^T + b1) W^T + b (or W pooled + b for the linear tasks)."""
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1)
+    hd = model.heads
+    dt = w.torch_dtype
+    g = torch.Generator(device="cuda").manual_seed(21)
+    H = 128
+    W1s, b1s, Ws, bs = [], [], [], []
+    for t in range(w.n_tasks):
+        n = int(hd.n_out[t])
+        if t % 2:      # MLP head
+            W1s.append((torch.randn(H, w.d, generator=g, device="cuda") / w.d ** 0.5).to(dt))
+            b1s.append((0.1 * torch.randn(H, generator=g, device="cuda")).to(dt))
+            Ws.append((torch.randn(n, H, generator=g, device="cuda") / H ** 0.5).to(dt))
+        else:          # linear head, as drawn by the workload
+            W1s.append(None)
+            b1s.append(None)
+            Ws.append(hd.W[t])
+        bs.append(hd.b[t])
+    tab = B.HeadTable(hd.n_out, Ws, bs, model.head_tab.c.pool, W1s=W1s, b1s=b1s, hidden=H, act=act)
+    model.head_tab = tab
+    out = fwd().cpu().numpy()
+    x_fin = fwd.x.double().cpu().numpy()
+    spec = spec_of(w)
+    fw = np64(model.final["w"])
+    fb = np64(model.final["b"]) if model.final.get("b") is not None else None
+    cu, off = pl["cu_seqlens"], pl["logit_off"]
+    worst = 0.0
+    for p in range(batch.n_req):
+        i, t = int(pl["order"][p]), int(pl["task"][p])
+        pooled = O.pool(O.final(spec, fw, fb, x_fin[int(cu[p]):int(cu[p + 1])]), w.pool)
+        if t % 2:
+            ref = O.head_mlp(pooled, np64(W1s[t]), np64(b1s[t]), np64(Ws[t]), np64(bs[t]),
+                             act="gelu" if act == B.VFM_ACT_GELU else "relu")
+        else:
+            ref = O.head(pooled, np64(Ws[t]), np64(bs[t]))
+        worst = max(worst, O.row_rel_error(out[off[i]:off[i + 1]][None], ref[None]))
+    log(f"  MLP / linear heads, workload {idx}: max rel err {worst:.3e}")
+    assert worst < tol(w)
+    # attach an MLP head to task 0 (linear so far) between batches: task 0's
+    # outputs follow the new head, every other task's stay bit-identical
+    n0 = int(hd.n_out[0])
+    W1n = (torch.randn(H, w.d, generator=g, device="cuda") / w.d ** 0.5).to(dt)
+    b1n = (0.1 * torch.randn(H, generator=g, device="cuda")).to(dt)
+    Wn = (torch.randn(n0, H, generator=g, device="cuda") / H ** 0.5).to(dt)
+    B.vfm_head_attach(tab, 0, n0, Wn, hd.b[0], W1n, b1n)
+    fwd.head()
+    torch.cuda.synchronize()
+    out2 = fwd.out.cpu().numpy()
+    for p in range(batch.n_req):
+        i, t = int(pl["order"][p]), int(pl["task"][p])
+        sl = slice(off[i], off[i + 1])
+        if t == 0:
+            pooled = O.pool(O.final(spec, fw, fb, x_fin[int(cu[p]):int(cu[p + 1])]), w.pool)
+            ref = O.head_mlp(pooled, np64(W1n), np64(b1n), np64(Wn), np64(hd.b[0]),
+                             act="gelu" if act == B.VFM_ACT_GELU else "relu")
+            assert O.row_rel_error(out2[sl][None], ref[None]) < tol(w)
+        else:
+            assert np.array_equal(out2[sl], out[sl])

@@ -384,3 +384,23 @@ def test_row_rel_error_measure():
     got = np.array([[1.2, -4.0], [0.0, 0.5]])
     assert O.row_rel_error(got, ref) == pytest.approx(0.5)
     assert O.row_rel_error(ref, ref) == 0.0
+
+
+def test_mlp_head_pins():
+    """Two-layer MLP decoder head: a worked example with the standard normal
+    CDF values Phi(3) = 0.9986501, Phi(-1) = 0.1586553, and the reduction to
+    the linear head (identity first layer, ReLU, non-negative input)."""
+    pooled = np.array([1.0, -2.0])
+    W1 = np.array([[1.0, 1.0], [2.0, 0.0]])
+    b1 = np.array([0.0, 1.0])
+    W = np.array([[1.0, 2.0]])
+    b = np.array([0.5])
+    # pre-activation [-1, 3]
+    assert np.allclose(O.head_mlp(pooled, W1, b1, W, b, act="relu"), [0.0 + 2 * 3.0 + 0.5])
+    assert np.allclose(O.head_mlp(pooled, W1, b1, W, b, act="gelu"),
+                       [-1 * 0.1586553 + 2 * 3 * 0.9986501 + 0.5], atol=1e-6)
+    rng = np.random.default_rng(0)
+    x = np.abs(rng.normal(size=16))
+    W2 = rng.normal(size=(5, 16))
+    b2 = rng.normal(size=5)
+    assert np.allclose(O.head_mlp(x, np.eye(16), np.zeros(16), W2, b2, act="relu"), O.head(x, W2, b2))
