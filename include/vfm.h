@@ -190,6 +190,19 @@ typedef struct vfm_head_table {
   const void* const* b1;       /* device [n_tasks] -> b1_t [hidden], entries may be NULL; or NULL */
 } vfm_head_table;
 
+/* Per-task input encoders (the vFM's input-side extension, Section 2.2 and
+ * Section 4.1 task extensions): a linear channel combiner (the
+ * LinearChannelCombiner encoder of Section 4.3's pipeline example, 3 channels
+ * to 1).  A request of task t brings C channels x_0 .. x_{C-1} of its series;
+ * the backbone sees the one-channel series s = b_t + sum_c W_t[c] x_c.  Tasks
+ * whose W entry is NULL have no encoder: their channel 0 passes unchanged. */
+typedef struct vfm_encoder_table {
+  int32_t n_tasks;
+  int32_t n_channels;          /* C, 1..64 */
+  const float* const* W;       /* device [n_tasks] -> W_t float32 [C]; entries may be NULL */
+  const float* const* b;       /* device [n_tasks] -> b_t float32 [1], entries may be NULL; or NULL */
+} vfm_encoder_table;
+
 const char* vfm_status_string(int status);
 
 /* ------------------------------------------------------------------------
@@ -217,6 +230,12 @@ int vfm_lora_attach(const vfm_lora_table* table, int32_t task, int32_t rank, flo
                     const void* const* A, const void* const* B, void* stream);
 int vfm_head_attach(const vfm_head_table* table, int32_t task, int32_t n_out, const void* W,
                     const void* b, const void* W1, const void* b1, void* stream);
+/*   vfm_encoder_attach: W = W_t float32 [C] (device) gives the task an
+ *     encoder, W = NULL removes it (channel 0 passes); b = b_t [1] or NULL.
+ *     VFM_ERR_TASK for a task out of range; VFM_ERR_ARG for a null table or
+ *     table->W, or a bias when table->b is NULL. */
+int vfm_encoder_attach(const vfm_encoder_table* table, int32_t task, const float* W, const float* b,
+                       void* stream);
 
 /* Device workspace needed by vfm_layer_forward / vfm_lora_apply /
  * vfm_head_forward for this batch (lora may be NULL). */
@@ -236,6 +255,22 @@ int vfm_workspace_size(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_lor
 int vfm_embed_forward(const vfm_cfg* cfg, const vfm_batch* batch, int32_t mode, const void* src,
                       int32_t src_width, const void* table, const void* bias, float* x,
                       void* stream);
+
+/* a1'. Per-task encoder, then the shared patch embedding, in one pass.
+ *   src: device float32, requests in ORIGINAL order; request i (len_i rows,
+ *     patches of `patch` samples) occupies n_channels * len_i * patch floats
+ *     from n_channels * cu_orig[i] * patch, channel-major: channel c is the
+ *     request's whole series of len_i * patch samples.
+ *   enc: the encoder table (n_tasks equal to the plan's).
+ *   W_pe [d, patch], b_pe [d] or NULL (dtype), patch <= 64, as
+ *   VFM_EMBED_PATCHES.  x: fp32 [T, d], plan order.
+ * Row r of request i of task t: x_r = W_pe s[r * patch .. (r + 1) * patch) + b_pe
+ * with s the task's combined series (see vfm_encoder_table).
+ * Errors: VFM_ERR_ARG for null pointers, VFM_ERR_SHAPE for n_channels
+ * outside 1..64, patch outside 1..64 or an encoder table of another task count. */
+int vfm_embed_series(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_encoder_table* enc,
+                     const float* src, int32_t patch, const void* W_pe, const void* b_pe, float* x,
+                     void* stream);
 
 /* ------------------------------------------------------------------------
  * a2-a10. One backbone layer over the whole mixed batch, in place on x.

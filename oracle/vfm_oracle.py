@@ -25,6 +25,10 @@ request at a time, in float64:
                 x  = x + u W_down^T + b_down (+ LoRA_down)
     then final norm, pooling per request, and the task's linear head.
 
+A task's pipeline may also carry an input-side encoder (a linear channel
+combiner, C channels to one, ahead of the shared patch embedding) and an MLP
+decoder head in place of the linear one (Section 4.3's pipeline example).
+
 The backbone architectures (pre-LN ViT/T5-style encoder; Llama-style decoder
 with RMSNorm, RoPE and SwiGLU) are the standard ones of the backbones the paper
 serves (Table 2); the paper defines none of their arithmetic itself.  Where the
@@ -38,7 +42,9 @@ zero rank / zero B == bare backbone; LoRA closed form on unit vectors; encoder
 layer vs torch's TransformerEncoderLayer; decoder layer vs transformers'
 LlamaDecoderLayer; RoPE vs the complex-rotation form; attention special cases;
 decode step == last prefill row; batched re-association == per-request
-definition.  Every function here is pinned by at least one of them.
+definition; MLP head and channel combiner on hand-worked examples and their
+reductions to the linear head / a single channel.  Every function here is
+pinned by at least one of them.
 """
 from __future__ import annotations
 
@@ -286,6 +292,23 @@ def head_mlp(pooled, W1, b1, W, b, act="gelu"):
     h = linear(pooled[None, :], W1, b1)
     h = gelu(h) if act == "gelu" else np.maximum(h, 0.0)
     return linear(h, W, b)[0]
+
+
+def channel_combine(x, W, b=None):
+    """Task-specific input encoder: the linear channel combiner of Section
+    4.3's pipeline example (C channels to one).  x [C, L] (a request's
+    series, one row per channel), W [C], b scalar or None:
+    s[l] = b + sum_c W[c] x[c, l]."""
+    x = np.asarray(x, F64)
+    s = np.asarray(W, F64) @ x
+    return s + (float(np.asarray(b, F64).reshape(-1)[0]) if b is not None else 0.0)
+
+
+def patch_embed(series, patch, W_pe, b_pe):
+    """Shared patch embedding of a one-channel series: cut into consecutive
+    patches of `patch` samples, each mapped to W_pe p + b_pe."""
+    series = np.asarray(series, F64)
+    return linear(series.reshape(-1, patch), W_pe, b_pe)
 
 
 def final(spec, fn_w, fn_b, x):

@@ -36,7 +36,8 @@ EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size
            "vfm_embed_forward", "vfm_layer_forward", "vfm_lora_apply", "vfm_head_forward",
            "vfm_profile_enable", "vfm_profile_read",
            "vfm_bfq_state_size", "vfm_bfq_init", "vfm_bfq_enqueue", "vfm_bfq_next_batch",
-           "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach")
+           "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach",
+           "vfm_embed_series", "vfm_encoder_attach")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -111,6 +112,11 @@ def _lib_handle():
                                         C.c_void_p, C.c_void_p, C.c_void_p]
         lib.vfm_head_attach.argtypes = [C.POINTER(vfm_head_table), C.c_int32, C.c_int32, C.c_void_p,
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        lib.vfm_embed_series.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_batch),
+                                         C.POINTER(vfm_encoder_table), C.c_void_p, C.c_int32,
+                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+        lib.vfm_encoder_attach.argtypes = [C.POINTER(vfm_encoder_table), C.c_int32, C.c_void_p,
+                                           C.c_void_p, C.c_void_p]
         lib.vfm_bfq_state_size.argtypes = [C.POINTER(vfm_bfq_config), C.POINTER(C.c_size_t)]
         lib.vfm_bfq_init.argtypes = [C.POINTER(vfm_bfq_config), C.c_void_p, C.c_size_t]
         lib.vfm_bfq_enqueue.argtypes = [C.c_void_p, C.c_int32, C.c_int64, C.c_double, C.c_double]
@@ -339,6 +345,35 @@ class HeadTable:
                                 int(hidden), int(act),
                                 self.pw1.data_ptr() if self.pw1 is not None else None,
                                 self.pb1.data_ptr() if self.pb1 is not None else None)
+
+
+class vfm_encoder_table(C.Structure):
+    _fields_ = [("n_tasks", C.c_int32), ("n_channels", C.c_int32), ("W", C.c_void_p), ("b", C.c_void_p)]
+
+
+class EncoderTable:
+    """Device tables of per-task channel-combiner encoders: Ws[t] float32 [C]
+    or None (no encoder: channel 0 passes), bs[t] float32 [1] or None."""
+
+    def __init__(self, n_channels, Ws, bs=None, device="cuda"):
+        self._keep = [Ws, bs]
+        ptrs = lambda xs: torch.tensor([_ptr(x) if x is not None else 0 for x in xs],
+                                       dtype=torch.int64).to(device)
+        self.pw = ptrs(Ws)
+        self.pb = ptrs(bs) if bs is not None else None
+        self.c = vfm_encoder_table(len(Ws), int(n_channels), self.pw.data_ptr(),
+                                   self.pb.data_ptr() if self.pb is not None else None)
+
+
+def vfm_embed_series(cfg, batch, enc, src, patch, W_pe, b_pe, x, stream=None):
+    st = _lib_handle().vfm_embed_series(C.byref(cfg), C.byref(batch), C.byref(enc.c), _ptr(src), int(patch),
+                                        _ptr(W_pe), _ptr(b_pe), _ptr(x), _stream(stream))
+    _check(st, "vfm_embed_series")
+
+
+def vfm_encoder_attach(enc, task, W=None, b=None, stream=None):
+    st = _lib_handle().vfm_encoder_attach(C.byref(enc.c), int(task), _ptr(W), _ptr(b), _stream(stream))
+    _check(st, "vfm_encoder_attach")
 
 
 # ---- batch-aware fair queueing (host scheduler, include/vfm_bfq.h) --------

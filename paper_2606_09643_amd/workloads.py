@@ -376,6 +376,35 @@ def series_inputs(w: Workload, batch: Batch, device="cpu", seed: int = DEFAULT_S
     return torch.from_numpy(patches).to(device), W, b
 
 
+def multichannel_series_inputs(w: Workload, batch: Batch, n_channels: int, patch: int, device="cpu",
+                               seed: int = DEFAULT_SEED):
+    """Multi-channel time series (e.g. the 3-channel physiological signals of
+    the paper's MOMENT pipeline example): every channel of every request drawn
+    with the recipe of ``series_inputs`` (random walk + sinusoid + noise),
+    ``seq_len * patch`` samples per channel.  Returns the series float32 flat,
+    requests in original order, each ``[n_channels, seq_len * patch]``
+    channel-major, and a patch-embedding weight ``[d, patch]`` ~ N(0, 1/sqrt(patch))
+    with bias ``[d]`` ~ N(0, 0.02) (workload dtype)."""
+    c = _children(w, seed)
+    kid_s, kid_w = np.random.SeedSequence(c["inputs"].generate_state(2)).spawn(2)
+    r = np.random.default_rng(kid_s)
+    parts = []
+    for n_rows in batch.seq_len:
+        L = int(n_rows) * patch
+        t = np.arange(L, dtype=np.float64)
+        walk = np.cumsum(r.normal(0.0, 0.05, size=(n_channels, L)), axis=1)
+        amp = r.uniform(0.5, 2.0, size=(n_channels, 1))
+        period = r.uniform(8.0, 128.0, size=(n_channels, 1))
+        phase = r.uniform(0.0, 2 * np.pi, size=(n_channels, 1))
+        noise = r.normal(0.0, 0.1, size=(n_channels, L))
+        parts.append((walk + amp * np.sin(2 * np.pi * t / period + phase) + noise).ravel())
+    series = np.concatenate(parts).astype(np.float32)
+    g = _torch_gen(kid_w, device)
+    W = _normal((w.d, patch), 1.0 / np.sqrt(patch), g, device, w.torch_dtype)
+    b = _normal((w.d,), 0.02, g, device, w.torch_dtype)
+    return torch.from_numpy(series).to(device), W, b
+
+
 def kv_offsets(batch: Batch) -> np.ndarray:
     """Slot offset of each request's cache (original order); request i owns
     ``ctx[i] + 1`` slots, the last one for the token being decoded."""

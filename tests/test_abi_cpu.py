@@ -173,3 +173,30 @@ def test_attach_rejects_bad_arguments_before_launching():
     assert ha(0, 5, None, None) == B.VFM_ERR_ARG
     assert ha(0, 5, fake, fake) == B.VFM_ERR_ARG          # no bias array
     assert ha(0, 5, fake, None, fake) == B.VFM_ERR_ARG    # MLP layer without MLP tables
+
+
+def test_encoder_calls_reject_bad_arguments_before_launching():
+    """vfm_embed_series / vfm_encoder_attach argument errors are found on the
+    host (nothing is launched when a check fails)."""
+    lib = B.lib()
+    fake = 0x10000
+    host = B.vfm_plan([0, 1, 1], [5, 3, 2], 2)
+    bc = _batch_c(host)
+    cfg = B.make_cfg(B.VFM_BF16, 1024, 16, 64, 2816, 0, 0, 0, 1, 1e-5, 0.0)
+    emb = lambda enc, patch=8, src=fake, W=fake, x=fake: lib.vfm_embed_series(
+        C.byref(cfg), C.byref(bc), enc, src, patch, W, None, x, None)
+    good = B.vfm_encoder_table(2, 3, fake, None)
+    assert emb(None) == B.VFM_ERR_ARG
+    assert emb(C.byref(good), src=None) == B.VFM_ERR_ARG
+    assert emb(C.byref(good), W=None) == B.VFM_ERR_ARG
+    assert emb(C.byref(B.vfm_encoder_table(2, 3, None, None))) == B.VFM_ERR_ARG
+    assert emb(C.byref(B.vfm_encoder_table(3, 3, fake, None))) == B.VFM_ERR_SHAPE   # task count
+    assert emb(C.byref(B.vfm_encoder_table(2, 0, fake, None))) == B.VFM_ERR_SHAPE
+    assert emb(C.byref(B.vfm_encoder_table(2, 65, fake, None))) == B.VFM_ERR_SHAPE
+    assert emb(C.byref(good), patch=0) == B.VFM_ERR_SHAPE
+    assert emb(C.byref(good), patch=65) == B.VFM_ERR_SHAPE
+    att = lambda tab, t, W=fake, b=None: lib.vfm_encoder_attach(tab, t, W, b, None)
+    assert att(C.byref(good), 2) == B.VFM_ERR_TASK
+    assert att(C.byref(good), -1) == B.VFM_ERR_TASK
+    assert att(C.byref(good), 0, fake, fake) == B.VFM_ERR_ARG                        # no bias array
+    assert att(None, 0) == B.VFM_ERR_ARG

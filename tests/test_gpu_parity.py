@@ -627,3 +627,59 @@ def test_mlp_decoder_heads(idx, act):
             assert O.row_rel_error(out2[sl][None], ref[None]) < tol(w)
         else:
             assert np.array_equal(out2[sl], out[sl])
+
+
+def _expected_series_rows(batch, pl, src, C_, patch, Ws, bs, W_pe, b_pe):
+    """Oracle rows (plan order): each request's channels combined by its
+    task's encoder (or channel 0 without one), patched and embedded."""
+    cu_o = pl["cu_orig"]
+    rows = []
+    for p, i in enumerate(pl["order"]):
+        t = int(pl["task"][p])
+        L = int(batch.seq_len[i]) * patch
+        xr = src[C_ * int(cu_o[i]) * patch:C_ * int(cu_o[i + 1]) * patch].reshape(C_, L)
+        s = O.channel_combine(xr, Ws[t], bs[t]) if Ws[t] is not None else xr[0]
+        rows.append(O.patch_embed(s, patch, W_pe, b_pe))
+    return np.concatenate(rows)
+
+
+@pytest.mark.parametrize("idx", [3, 1])
+def test_channel_encoder_embed(idx):
+    """Per-task linear channel combiners (3 channels to 1) fused with the
+    shared patch embedding, tasks with an even id carrying one and the others
+    feeding channel 0: every row against the oracle's combine -> patch ->
+    embed; then an encoder attached to task 1 and removed from task 0 between
+    batches, the other tasks' rows bit-identical."""
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(idx)
+    C_, patch = 3, 8
+    src, W_pe, b_pe = wl.multichannel_series_inputs(w, batch, C_, patch, "cuda")
+    g = torch.Generator(device="cuda").manual_seed(31)
+    Ws = [torch.randn(C_, generator=g, device="cuda") if t % 2 == 0 else None for t in range(w.n_tasks)]
+    bs = [0.1 * torch.randn(1, generator=g, device="cuda") if t % 2 == 0 else None for t in range(w.n_tasks)]
+    enc = B.EncoderTable(C_, Ws, bs)
+    log(f"series encoder workload {idx} T={pb.T} channels {C_}")
+    x = torch.empty(pb.T, w.d, dtype=torch.float32, device="cuda")
+    B.vfm_embed_series(model.cfg, pb.c, enc, src, patch, W_pe, b_pe, x)
+    torch.cuda.synchronize()
+    src_np, Wpe_np, bpe_np = np64(src), np64(W_pe), np64(b_pe)
+    Ws_np, bs_np = [np64(v) for v in Ws], [np64(v) for v in bs]
+    got = x.double().cpu().numpy()
+    ref = _expected_series_rows(batch, pl, src_np, C_, patch, Ws_np, bs_np, Wpe_np, bpe_np)
+    err = O.row_rel_error(got, ref)
+    log(f"  max rel err {err:.3e}")
+    assert err < 1e-5
+    # encoder lifecycle between batches
+    Wn = torch.tensor([0.5, -1.0, 2.0], device="cuda")
+    bn = torch.tensor([0.25], device="cuda")
+    B.vfm_encoder_attach(enc, 1, Wn, bn)
+    B.vfm_encoder_attach(enc, 0, None)
+    x2 = torch.empty_like(x)
+    B.vfm_embed_series(model.cfg, pb.c, enc, src, patch, W_pe, b_pe, x2)
+    torch.cuda.synchronize()
+    Ws_np[1], bs_np[1] = np64(Wn), np64(bn)
+    Ws_np[0], bs_np[0] = None, None
+    got2 = x2.double().cpu().numpy()
+    ref2 = _expected_series_rows(batch, pl, src_np, C_, patch, Ws_np, bs_np, Wpe_np, bpe_np)
+    assert O.row_rel_error(got2, ref2) < 1e-5
+    other = pl["task"][pl["row_req"]] >= 2
+    assert np.array_equal(got2[other], got[other])

@@ -404,3 +404,17 @@ def test_mlp_head_pins():
     W2 = rng.normal(size=(5, 16))
     b2 = rng.normal(size=5)
     assert np.allclose(O.head_mlp(x, np.eye(16), np.zeros(16), W2, b2, act="relu"), O.head(x, W2, b2))
+
+
+def test_channel_combiner_pins():
+    """Linear channel combiner (C channels to one) and the patch embedding it
+    feeds: a hand-worked example, selection of one channel by a unit weight,
+    the channel mean, and patches cut in order."""
+    x = np.array([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]])          # 3 channels, 2 samples
+    assert np.allclose(O.channel_combine(x, [1.0, 0.0, -1.0], 0.5), [1 - 5 + 0.5, 2 - 6 + 0.5])
+    assert np.allclose(O.channel_combine(x, [0.0, 1.0, 0.0]), x[1])
+    assert np.allclose(O.channel_combine(x, [1 / 3] * 3), [3.0, 4.0])
+    assert np.allclose(O.channel_combine(x, [2.0, 0.0, 0.0], np.array([1.0])), [3.0, 5.0])
+    s = np.arange(6.0)                                          # two patches of 3
+    W_pe = np.array([[1.0, 0.0, 0.0], [0.0, 0.0, 1.0]])
+    assert np.allclose(O.patch_embed(s, 3, W_pe, np.array([0.0, 10.0])), [[0.0, 12.0], [3.0, 15.0]])
