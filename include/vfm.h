@@ -55,7 +55,7 @@ typedef enum {
 enum { VFM_F32 = 0, VFM_BF16 = 1 };
 enum { VFM_NORM_LAYER = 0, VFM_NORM_RMS = 1 };
 enum { VFM_MLP_GELU = 0, VFM_MLP_SWIGLU = 1 };
-enum { VFM_ATTN_BIDIR = 0, VFM_ATTN_CAUSAL = 1, VFM_ATTN_DECODE = 2 };
+enum { VFM_ATTN_BIDIR = 0, VFM_ATTN_CAUSAL = 1, VFM_ATTN_DECODE = 2, VFM_ATTN_MIXED = 3 };
 enum { VFM_Q = 0, VFM_K = 1, VFM_V = 2, VFM_O = 3, VFM_GATE = 4, VFM_UP = 5, VFM_DOWN = 6,
        VFM_NPROJ = 7 };
 enum { VFM_POOL_MEAN = 0, VFM_POOL_FIRST = 1, VFM_POOL_LAST = 2 };
@@ -84,7 +84,7 @@ typedef struct vfm_cfg {
   int32_t norm;       /* VFM_NORM_LAYER (encoder) | VFM_NORM_RMS (decoder) */
   int32_t mlp;        /* VFM_MLP_GELU: u = GELU_erf(h W_up^T + b_up)
                          VFM_MLP_SWIGLU: u = SiLU(h W_gate^T) * (h W_up^T) */
-  int32_t attn;       /* VFM_ATTN_BIDIR | VFM_ATTN_CAUSAL | VFM_ATTN_DECODE */
+  int32_t attn;       /* VFM_ATTN_BIDIR | VFM_ATTN_CAUSAL | VFM_ATTN_DECODE | VFM_ATTN_MIXED */
   int32_t has_bias;   /* 1: every backbone linear has a bias */
   float norm_eps;
   float rope_theta;   /* 0: no rotary embedding; else RoPE base (rotate-half) */
@@ -290,6 +290,49 @@ int vfm_embed_series(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_encod
 int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
                       const vfm_batch* batch, float* x, void* k_cache, void* v_cache,
                       int64_t kv_slots, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * a2-a10 over a paged KV cache: the token-based FMs' continuous batching
+ * with long-lived decode iterations (Section 4.2, which also charges their
+ * token-level work in service-time units; Section 6 maps the vFM boundary
+ * onto a vLLM-style runtime, whose KV cache is paged).
+ *
+ * Pages.  The cache keeps the head-major layout of vfm_layer_forward,
+ * [n_heads][n_pages * page_size][head_dim], cut into pages of page_size slots:
+ * token k of request i lives at slot table[i][k / page_size] * page_size +
+ * k % page_size of every head.  Each page of one head is a contiguous run
+ * (page_size * head_dim elements), so decode attention streams whole pages;
+ * a contiguous cache is the case table[i][j] = first_page_i + j.
+ *
+ * Steps.  cfg->attn selects:
+ *   VFM_ATTN_CAUSAL  every request a prompt (ctx 0): causal attention over
+ *                    its own rows, whose K / V are written into its pages.
+ *   VFM_ATTN_DECODE  every request one new token after ctx cached ones.
+ *   VFM_ATTN_MIXED   a continuous-batching step: each request either a
+ *                    prompt (ctx 0, any length) or one decode token (ctx > 0,
+ *                    length 1); a request with ctx > 0 and more than one row
+ *                    (chunked prefill) gives VFM_ERR_UNSUPPORTED.
+ * The new rows' K / V go to slots ctx .. ctx + len - 1 of the request's pages
+ * before attention reads them.
+ * ---------------------------------------------------------------------- */
+typedef struct vfm_kv_pages {
+  void* k;                    /* device [n_heads][n_pages * page_size][head_dim] (dtype) */
+  void* v;                    /* same layout */
+  int64_t n_pages;
+  int32_t page_size;          /* slots per page: a power of two, 16 .. 1024 */
+  int32_t max_pages;          /* columns of the page table */
+  const int32_t* table_host;  /* host [n_req][max_pages], ORIGINAL request order: physical page of
+                                 each logical page; validated against n_pages before any launch */
+  const int32_t* table_dev;   /* device copy of table_host */
+} vfm_kv_pages;
+
+/* Errors as vfm_layer_forward, plus VFM_ERR_SHAPE when a request's
+ * ctx + len tokens need more than max_pages pages or a page id it uses is
+ * outside [0, n_pages), VFM_ERR_ARG for a bad page size or null tables, and
+ * VFM_ERR_UNSUPPORTED for VFM_ATTN_BIDIR or a chunked-prefill request. */
+int vfm_layer_forward_paged(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
+                            const vfm_batch* batch, float* x, const vfm_kv_pages* kv, void* workspace,
+                            size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * a4. Segmented LoRA on one projection: for every plan-order row m of task

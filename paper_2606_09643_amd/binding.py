@@ -22,7 +22,7 @@ VFM_ERR_UNSUPPORTED, VFM_ERR_WORKSPACE, VFM_ERR_HIP = -4, -5, -6
 VFM_F32, VFM_BF16 = 0, 1
 VFM_NORM_LAYER, VFM_NORM_RMS = 0, 1
 VFM_MLP_GELU, VFM_MLP_SWIGLU = 0, 1
-VFM_ATTN_BIDIR, VFM_ATTN_CAUSAL, VFM_ATTN_DECODE = 0, 1, 2
+VFM_ATTN_BIDIR, VFM_ATTN_CAUSAL, VFM_ATTN_DECODE, VFM_ATTN_MIXED = 0, 1, 2, 3
 VFM_POOL_MEAN, VFM_POOL_FIRST, VFM_POOL_LAST = 0, 1, 2
 VFM_EMBED_ROWS, VFM_EMBED_TOKENS, VFM_EMBED_PATCHES = 0, 1, 2
 VFM_ACT_GELU, VFM_ACT_RELU = 0, 1
@@ -37,7 +37,7 @@ EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size
            "vfm_profile_enable", "vfm_profile_read",
            "vfm_bfq_state_size", "vfm_bfq_init", "vfm_bfq_enqueue", "vfm_bfq_next_batch",
            "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach",
-           "vfm_embed_series", "vfm_encoder_attach")
+           "vfm_embed_series", "vfm_encoder_attach", "vfm_layer_forward_paged")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -76,6 +76,11 @@ class vfm_head_table(C.Structure):
                 ("hidden", C.c_int32), ("act", C.c_int32), ("W1", C.c_void_p), ("b1", C.c_void_p)]
 
 
+class vfm_kv_pages(C.Structure):
+    _fields_ = [("k", C.c_void_p), ("v", C.c_void_p), ("n_pages", C.c_int64), ("page_size", C.c_int32),
+                ("max_pages", C.c_int32), ("table_host", C.POINTER(C.c_int32)), ("table_dev", C.c_void_p)]
+
+
 _LIB = None
 
 
@@ -99,6 +104,9 @@ def _lib_handle():
                                           C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
                                           C.c_void_p, C.c_size_t, C.c_void_p]
+        lib.vfm_layer_forward_paged.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_layer_weights),
+                                                C.POINTER(vfm_lora_table), C.POINTER(vfm_batch), C.c_void_p,
+                                                C.POINTER(vfm_kv_pages), C.c_void_p, C.c_size_t, C.c_void_p]
         lib.vfm_lora_apply.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                        C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
@@ -206,6 +214,28 @@ def vfm_layer_forward(cfg, weights, lora, batch, x, k_cache=None, v_cache=None, 
                                          C.byref(batch), _ptr(x), _ptr(k_cache), _ptr(v_cache),
                                          kv_slots, ws_ptr, ws_bytes, _stream(stream))
     _check(st, "vfm_layer_forward")
+
+
+class PagedKV:
+    """One layer's paged K / V pool (device tensors [n_heads, n_pages * page_size,
+    head_dim]) with a page table (host int32 [n_req, max_pages], original
+    request order) and its device copy, as the C struct vfm_kv_pages."""
+
+    def __init__(self, k, v, page_size, table, device="cuda"):
+        self.k, self.v = k, v
+        self.table = np.ascontiguousarray(table, np.int32)
+        self.table_dev = torch.from_numpy(self.table).to(device)
+        self.c = vfm_kv_pages(k.data_ptr(), v.data_ptr(), k.shape[1] // page_size, int(page_size),
+                              self.table.shape[1], self.table.ctypes.data_as(C.POINTER(C.c_int32)),
+                              self.table_dev.data_ptr())
+
+
+def vfm_layer_forward_paged(cfg, weights, lora, batch, x, kv, workspace, stream=None):
+    st = _lib_handle().vfm_layer_forward_paged(C.byref(cfg), C.byref(weights),
+                                               C.byref(lora) if lora is not None else None,
+                                               C.byref(batch), _ptr(x), C.byref(kv.c), workspace.data_ptr(),
+                                               workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "vfm_layer_forward_paged")
 
 
 def vfm_lora_apply(dtype, proj, d_in, d_out, lora, batch, x, y, workspace, stream=None):

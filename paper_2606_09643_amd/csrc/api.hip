@@ -17,7 +17,7 @@ int check_cfg(const vfm_cfg* c) {
   if (c->dtype != VFM_F32 && c->dtype != VFM_BF16) return VFM_ERR_ARG;
   if (c->norm != VFM_NORM_LAYER && c->norm != VFM_NORM_RMS) return VFM_ERR_ARG;
   if (c->mlp != VFM_MLP_GELU && c->mlp != VFM_MLP_SWIGLU) return VFM_ERR_ARG;
-  if (c->attn < VFM_ATTN_BIDIR || c->attn > VFM_ATTN_DECODE) return VFM_ERR_ARG;
+  if (c->attn < VFM_ATTN_BIDIR || c->attn > VFM_ATTN_MIXED) return VFM_ERR_ARG;
   if (c->head_dim != 64 && c->head_dim != 128) return VFM_ERR_UNSUPPORTED;
   if (c->n_heads < 1 || (int64_t)c->n_heads * c->head_dim != c->d_model) return VFM_ERR_SHAPE;
   if (c->d_model % 64 || c->d_model > 8192 || c->d_ff < 64 || c->d_ff % 64) return VFM_ERR_SHAPE;
@@ -179,29 +179,48 @@ extern "C" int vfm_embed_forward(const vfm_cfg* cfg, const vfm_batch* batch, int
                                  (hipStream_t)stream));
 }
 
-extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
-                                 const vfm_lora_table* lora, const vfm_batch* batch, float* x,
-                                 void* k_cache, void* v_cache, int64_t kv_slots, void* workspace,
-                                 size_t ws_bytes, void* stream) {
+namespace {
+
+// Checks shared by the two layer entry points (everything but the cache).
+int check_layer(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
+                const vfm_batch* batch, const float* x, bool have_cache, Plan* pl) {
   VFM_TRY(check_cfg(cfg));
-  Plan pl;
-  VFM_TRY(check_batch(batch, &pl));
-  VFM_TRY(check_lora(lora, pl));
+  VFM_TRY(check_batch(batch, pl));
+  VFM_TRY(check_lora(lora, *pl));
   if (!w || !x) return VFM_ERR_ARG;
   if (!w->norm1_w || !w->norm2_w || !w->w_qkv || !w->w_o || !w->w_up || !w->w_down)
     return VFM_ERR_ARG;
   if (cfg->mlp == VFM_MLP_SWIGLU && !w->w_gate) return VFM_ERR_ARG;
-  const vfm_cfg& c = *cfg;
-  const int d = c.d_model, f = c.d_ff, T = pl.T;
-
-  // KV-cache bounds (host copy of the plan)
-  const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
-  if (c.attn == VFM_ATTN_DECODE) {
-    if (!k_cache || !v_cache) return VFM_ERR_ARG;
-    if (pl.max_seqlen != 1) return VFM_ERR_UNSUPPORTED;
+  if (cfg->attn == VFM_ATTN_DECODE || cfg->attn == VFM_ATTN_MIXED) {
+    if (!have_cache) return VFM_ERR_ARG;
   }
-  if (k_cache || v_cache) {
-    if (!k_cache || !v_cache) return VFM_ERR_ARG;
+  if (cfg->attn == VFM_ATTN_DECODE && pl->max_seqlen != 1) return VFM_ERR_UNSUPPORTED;
+  const PlanOffsets po = plan_offsets(pl->n_req, pl->n_tasks, pl->T);
+  if (cfg->attn == VFM_ATTN_MIXED) {        // prompts (ctx 0) or single decode rows
+    const int32_t* ctx = host_arr(batch, po.ctx);
+    const int32_t* cu = host_arr(batch, po.cu_seqlens);
+    for (int p = 0; p < pl->n_req; ++p)
+      if (ctx[p] > 0 && cu[p + 1] - cu[p] != 1) return VFM_ERR_UNSUPPORTED;
+  }
+  return VFM_OK;
+}
+
+int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_table* lora,
+               const vfm_batch* batch, const Plan& pl, float* x, void* k_cache, void* v_cache,
+               int64_t kv_slots, const KvPages& kp, void* workspace, size_t ws_bytes, void* stream);
+
+}  // namespace
+
+extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
+                                 const vfm_lora_table* lora, const vfm_batch* batch, float* x,
+                                 void* k_cache, void* v_cache, int64_t kv_slots, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  Plan pl;
+  if ((k_cache != nullptr) != (v_cache != nullptr)) return VFM_ERR_ARG;
+  VFM_TRY(check_layer(cfg, w, lora, batch, x, k_cache != nullptr, &pl));
+  // KV-cache bounds (host copy of the plan)
+  if (k_cache) {
+    const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
     const int32_t* ctx = host_arr(batch, po.ctx);
     const int32_t* kvs = host_arr(batch, po.kv_start);
     const int32_t* cu = host_arr(batch, po.cu_seqlens);
@@ -210,6 +229,45 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
       if (end > kv_slots) return VFM_ERR_SHAPE;
     }
   }
+  return layer_impl(*cfg, w, lora, batch, pl, x, k_cache, v_cache, kv_slots, KvPages{nullptr, 0, 0},
+                    workspace, ws_bytes, stream);
+}
+
+extern "C" int vfm_layer_forward_paged(const vfm_cfg* cfg, const vfm_layer_weights* w,
+                                       const vfm_lora_table* lora, const vfm_batch* batch, float* x,
+                                       const vfm_kv_pages* kv, void* workspace, size_t ws_bytes,
+                                       void* stream) {
+  if (!kv || !kv->k || !kv->v || !kv->table_host || !kv->table_dev) return VFM_ERR_ARG;
+  const int ps = kv->page_size;
+  if (ps < 16 || ps > 1024 || (ps & (ps - 1))) return VFM_ERR_ARG;
+  if (kv->n_pages < 1 || kv->max_pages < 1 || kv->n_pages > ((int64_t)1 << 40) / ps) return VFM_ERR_SHAPE;
+  Plan pl;
+  VFM_TRY(check_layer(cfg, w, lora, batch, x, true, &pl));
+  if (cfg->attn == VFM_ATTN_BIDIR) return VFM_ERR_UNSUPPORTED;
+  // every page a request uses (ctx + len tokens) exists
+  const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
+  const int32_t* ctx = host_arr(batch, po.ctx);
+  const int32_t* cu = host_arr(batch, po.cu_seqlens);
+  const int32_t* order = host_arr(batch, po.order);
+  for (int p = 0; p < pl.n_req; ++p) {
+    const int64_t need = ((int64_t)ctx[p] + (cu[p + 1] - cu[p]) + ps - 1) / ps;
+    if (need > kv->max_pages) return VFM_ERR_SHAPE;
+    const int32_t* row = kv->table_host + (int64_t)order[p] * kv->max_pages;
+    for (int64_t j = 0; j < need; ++j)
+      if (row[j] < 0 || row[j] >= kv->n_pages) return VFM_ERR_SHAPE;
+  }
+  int lp = 0;
+  while ((1 << lp) < ps) ++lp;
+  return layer_impl(*cfg, w, lora, batch, pl, x, kv->k, kv->v, kv->n_pages * ps,
+                    KvPages{kv->table_dev, kv->max_pages, lp}, workspace, ws_bytes, stream);
+}
+
+namespace {
+
+int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_table* lora,
+               const vfm_batch* batch, const Plan& pl, float* x, void* k_cache, void* v_cache,
+               int64_t kv_slots, const KvPages& kp, void* workspace, size_t ws_bytes, void* stream) {
+  const int d = c.d_model, f = c.d_ff, T = pl.T;
   const int max_keys = max_keys_of(batch, pl);
   const LayerWs ws = layer_ws(c, pl, lora, max_keys);
   if (!workspace || ws_bytes < ws.total || ((uintptr_t)workspace % ALIGN)) return VFM_ERR_WORKSPACE;
@@ -336,15 +394,15 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
                   3 * d, {VFM_Q, VFM_K, VFM_V}, d));
   // a5: rotary embedding of q and k
   // (with a KV cache the same pass writes each row's rotated k and its v)
-  const bool cache_write = k_cache != nullptr && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL);
+  const bool cache_write = k_cache != nullptr && c.attn != VFM_ATTN_BIDIR;
   const bool rope_writes_kv = c.rope_theta > 0.f && cache_write;
   if (c.rope_theta > 0.f)
     VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta,
                                           rope_writes_kv ? k_cache : nullptr, rope_writes_kv ? v_cache : nullptr,
-                                          kv_slots, s));
+                                          kv_slots, kp, s));
   // a6: attention per request (and the KV-cache write)
   // (timed per kernel inside the launcher)
-  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, rope_writes_kv,
+  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, kp, rope_writes_kv,
                            base + ws.aws, ws.z - ws.aws, max_keys, s));
   // a7: output projection + LoRA_o + residual
   VFM_TRY(project(VFM_PROF_GEMM_O, attn, d, w->w_o, nullptr, w->b_o, d, EPI_RESID, x, d, {VFM_O}, d,
@@ -364,6 +422,8 @@ extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
                   {VFM_DOWN}, d));
   return VFM_OK;
 }
+
+}  // namespace
 
 extern "C" int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t d_out,
                               const vfm_lora_table* lora, const vfm_batch* batch, const void* x,

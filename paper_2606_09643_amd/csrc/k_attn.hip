@@ -102,7 +102,7 @@ __device__ inline void store8<float>(float* p, const float (&v)[8]) {
 template <typename T>
 __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv, int d, int H, int dh,
                                                    float log2_theta, T* __restrict__ kc, T* __restrict__ vc,
-                                                   int64_t kv_slots) {
+                                                   int64_t kv_slots, KvPages kp) {
   __shared__ float cs_s[64], sn_s[64];        // dh / 2 <= 64
   const int r = blockIdx.x;
   const int half = dh >> 1;
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv,
   __syncthreads();
   const int per_head = half / 8;              // 8-pair groups per head
   T* row = qkv + (int64_t)r * 3 * d;
-  const int64_t slot = kc != nullptr ? (int64_t)pl.kv_start[pl.row_req[r]] + pl.pos[r] : 0;
+  const int64_t slot = kc != nullptr ? kv_slot(pl, kp, pl.row_req[r], pl.pos[r]) : 0;
   for (int w = threadIdx.x; w < 2 * H * per_head; w += blockDim.x) {
     const int part = w / (H * per_head);      // q, then k
     const int hh = (w / per_head) % H;
@@ -151,17 +151,18 @@ __global__ __launch_bounds__(256) void rope_kernel(Plan pl, T* __restrict__ qkv,
 }
 
 // ---------------------------------------------------------------------------
-// KV-cache write: row r's k / v go to slot kv_start[p] + pos[r] of every
-// head.  The caches are head-major, [n_heads][kv_slots][head_dim], so one
-// head's keys of one request are a contiguous run.
+// KV-cache write: row r's k / v go to the slot of position pos[r] of its
+// request (kv_start[p] + pos[r], or through the page table) in every head.
+// The caches are head-major, [n_heads][kv_slots][head_dim], so one head's
+// keys of one request (of one page, when paged) are a contiguous run.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void kv_write_kernel(Plan pl, const T* __restrict__ qkv, int d, int dh,
-                                                       int64_t kv_slots, T* __restrict__ kc,
+                                                       int64_t kv_slots, KvPages kp, T* __restrict__ kc,
                                                        T* __restrict__ vc) {
   const int r = blockIdx.x;
   const int p = pl.row_req[r];
-  const int64_t slot = (int64_t)pl.kv_start[p] + pl.pos[r];
+  const int64_t slot = kv_slot(pl, kp, p, pl.pos[r]);
   const T* src = qkv + (int64_t)r * 3 * d;
   for (int c = 8 * threadIdx.x; c < d; c += 8 * 256) {   // 8 elements (16 B bf16) per thread
     const int h = c / dh;
@@ -616,12 +617,28 @@ __global__ __launch_bounds__(256) void attn_prefill_simt_kernel(Plan pl, const T
 // with a single chunk gets its output from the attention kernel directly.
 // Inside a block, each group of LPK lanes walks one key stream; every step
 // issues the K and V loads of UNR keys of the stream before any is used.
+// PAGED: the request's keys sit in pages (KvPages); the block first reads
+// its chunk's page ids (at most DEC_CHUNK / 16) into LDS.  mixed: prompts
+// (ctx 0) of a continuous-batching step are left to the prefill kernels.
 constexpr int DEC_CHUNK = 1024;
+constexpr int DEC_MAX_PAGES = DEC_CHUNK / 16;   // page ids per chunk (pages of >= 16 slots)
 
-template <typename T, int DH, int UNR>
+// The chunk [kbeg, kend)'s page ids into spg; returns the first page index.
+__device__ __forceinline__ int load_chunk_pages(const Plan& pl, const KvPages& kp, int p, int kbeg, int kend,
+                                                int* spg) {
+  const int first = kbeg >> kp.log2_page;
+  const int npg = ((kend - 1) >> kp.log2_page) - first + 1;
+  if ((int)threadIdx.x < npg)
+    spg[threadIdx.x] = kp.table[(int64_t)pl.order[p] * kp.max_pages + first + threadIdx.x];
+  __syncthreads();
+  return first;
+}
+
+template <typename T, int DH, int UNR, bool PAGED>
 __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __restrict__ qkv, int d,
                                                           const T* __restrict__ kc,
                                                           const T* __restrict__ vc, int64_t kv_slots,
+                                                          KvPages kpg, int mixed,
                                                           float* __restrict__ part, int nchunk,
                                                           float scale_log2, T* __restrict__ out) {
   using OT = T;
@@ -629,15 +646,24 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
   constexpr int NG = 256 / LPK;        // key streams per block
   __shared__ float sm[NG], sl[NG];
   __shared__ float so[NG][DH + 1];
+  __shared__ int spg[PAGED ? DEC_MAX_PAGES : 1];
   const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
   const int tid = threadIdx.x;
   const int grp = tid / LPK, sub = tid % LPK;
+  if (mixed && pl.ctx[p] == 0) return;       // a prompt: block-uniform
   const int R = pl.cu_seqlens[p];            // the request's (single) query row
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int kbeg = c * DEC_CHUNK;
   if (kbeg >= nkeys) return;                 // block-uniform
   const int kend = min(kbeg + DEC_CHUNK, nkeys);
-  const int64_t base = (int64_t)pl.kv_start[p];
+  const int pg0 = PAGED ? load_chunk_pages(pl, kpg, p, kbeg, kend, spg) : 0;
+  const int64_t base = PAGED ? 0 : (int64_t)pl.kv_start[p];
+  // element offset of key k of the request from the head's first slot
+  auto koff = [&](int k) -> int64_t {
+    if (!PAGED) return (int64_t)k * DH;
+    const int lp = kpg.log2_page;
+    return (((int64_t)spg[(k >> lp) - pg0] << lp) + (k & ((1 << lp) - 1))) * DH;
+  };
   float q[8];
   load8<T>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8, q);
   float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
@@ -648,8 +674,8 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int k = min(k0 + u * NG, kend - 1);   // clamped: masked below
-      load8<T>(kp + (int64_t)k * DH, kv[u]);
-      load8<T>(vp + (int64_t)k * DH, vv[u]);
+      load8<T>(kp + koff(k), kv[u]);
+      load8<T>(vp + koff(k), vv[u]);
     }
     float sc[UNR];
     float smax = NEG_BIG;
@@ -716,10 +742,11 @@ __device__ __forceinline__ void gload16_untracked(bf16x8& dst, const bf16* p) {
   asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
 }
 
-template <int DH, int UNR>
+template <int DH, int UNR, bool PAGED>
 __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf16* __restrict__ qkv, int d,
                                                                const bf16* __restrict__ kc,
                                                                const bf16* __restrict__ vc, int64_t kv_slots,
+                                                               KvPages kpg, int mixed,
                                                                float* __restrict__ part, int nchunk,
                                                                float scale_log2, bf16* __restrict__ out) {
   using OT = bf16;
@@ -729,15 +756,23 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
   static_assert(UNR % 2 == 0, "keys are weighted in pairs");
   __shared__ float sm[NG], sl[NG];
   __shared__ float so[NG][DH + 1];
+  __shared__ int spg[PAGED ? DEC_MAX_PAGES : 1];
   const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
   const int tid = threadIdx.x;
   const int grp = tid / LPK, sub = tid % LPK;
+  if (mixed && pl.ctx[p] == 0) return;       // a prompt: block-uniform
   const int R = pl.cu_seqlens[p];
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int kbeg = c * DEC_CHUNK;
   if (kbeg >= nkeys) return;                 // block-uniform
   const int kend = min(kbeg + DEC_CHUNK, nkeys);
-  const int64_t base = (int64_t)pl.kv_start[p];
+  const int pg0 = PAGED ? load_chunk_pages(pl, kpg, p, kbeg, kend, spg) : 0;
+  const int64_t base = PAGED ? 0 : (int64_t)pl.kv_start[p];
+  auto koff = [&](int k) -> int64_t {
+    if (!PAGED) return (int64_t)k * DH;
+    const int lp = kpg.log2_page;
+    return (((int64_t)spg[(k >> lp) - pg0] << lp) + (k & ((1 << lp) - 1))) * DH;
+  };
   const bf16x8 q = *reinterpret_cast<const bf16x8*>(qkv + (int64_t)R * 3 * d + h * DH + sub * 8);
   float m_run = NEG_BIG, l_run = 0.f, o[8] = {};
   const bf16* kp = kc + ((int64_t)h * kv_slots + base) * DH + sub * 8;
@@ -749,8 +784,8 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int k = min(k0 + u * NG, kend - 1);
-      gload16_untracked(kb[slot][u], kp + (int64_t)k * DH);
-      gload16_untracked(vb[slot][u], vp + (int64_t)k * DH);
+      gload16_untracked(kb[slot][u], kp + koff(k));
+      gload16_untracked(vb[slot][u], vp + koff(k));
     }
   };
   auto step = [&](int slot, int k0) {
@@ -831,10 +866,11 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
 
 template <typename T, int DH>
 __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const float* __restrict__ part,
-                                                               int nchunk, int d, T* __restrict__ out) {
+                                                               int nchunk, int d, int mixed, T* __restrict__ out) {
   constexpr int MAXC = 64;                   // chunks merged per pass through LDS
   __shared__ float sw[MAXC];
   const int p = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  if (mixed && pl.ctx[p] == 0) return;       // a prompt (prefill kernels)
   const int R = pl.cu_seqlens[p];
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int nc = min((nkeys + DEC_CHUNK - 1) / DEC_CHUNK, nchunk);
@@ -874,76 +910,54 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const fl
 }  // namespace
 
 hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
-                       float theta, void* k_cache, void* v_cache, int64_t kv_slots, hipStream_t s) {
+                       float theta, void* k_cache, void* v_cache, int64_t kv_slots, const KvPages& kp,
+                       hipStream_t s) {
   if (pl.T == 0) return hipSuccess;
   const float l2t = log2f(theta);
   if (dtype == VFM_BF16)
     hipLaunchKernelGGL(rope_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (bf16*)qkv, d, n_heads, head_dim, l2t,
-                       (bf16*)k_cache, (bf16*)v_cache, kv_slots);
+                       (bf16*)k_cache, (bf16*)v_cache, kv_slots, kp);
   else
     hipLaunchKernelGGL(rope_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (float*)qkv, d, n_heads, head_dim, l2t,
-                       (float*)k_cache, (float*)v_cache, kv_slots);
+                       (float*)k_cache, (float*)v_cache, kv_slots, kp);
   return hipGetLastError();
 }
 
 size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys) {
-  if (c.attn != VFM_ATTN_DECODE) return 0;
+  if (c.attn != VFM_ATTN_DECODE && c.attn != VFM_ATTN_MIXED) return 0;
   const int nchunk = (max_keys + DEC_CHUNK - 1) / DEC_CHUNK;
   return (size_t)pl.n_req * c.n_heads * nchunk * (c.head_dim + 2) * sizeof(float);
 }
 
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv, void* out,
-                            void* k_cache, void* v_cache, int64_t kv_slots, bool kv_written, void* ws,
-                            size_t ws_bytes, int max_keys, hipStream_t s) {
+                            void* k_cache, void* v_cache, int64_t kv_slots, const KvPages& kp, bool kv_written,
+                            void* ws, size_t ws_bytes, int max_keys, hipStream_t s) {
   const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
+  const bool mixed = c.attn == VFM_ATTN_MIXED;
   // timing classes: the attention kernel itself is VFM_PROF_ATTN, the cache
   // write and the decode merge VFM_PROF_OTHER
   int pi = -1;
-  if (k_cache && !kv_written && (c.attn == VFM_ATTN_DECODE || c.attn == VFM_ATTN_CAUSAL)) {
+  if (k_cache && !kv_written && c.attn != VFM_ATTN_BIDIR) {
     pi = prof_begin(VFM_PROF_OTHER, s);
     if (dtype == VFM_BF16)
       hipLaunchKernelGGL(kv_write_kernel<bf16>, dim3(pl.T), dim3(256), 0, s, pl, (const bf16*)qkv, d, DH,
-                         kv_slots, (bf16*)k_cache, (bf16*)v_cache);
+                         kv_slots, kp, (bf16*)k_cache, (bf16*)v_cache);
     else
       hipLaunchKernelGGL(kv_write_kernel<float>, dim3(pl.T), dim3(256), 0, s, pl, (const float*)qkv, d, DH,
-                         kv_slots, (float*)k_cache, (float*)v_cache);
+                         kv_slots, kp, (float*)k_cache, (float*)v_cache);
     prof_end(pi, s);
   }
-  if (c.attn == VFM_ATTN_DECODE) {
-    if (ws_bytes < attention_workspace(c, pl, max_keys)) return hipErrorInvalidValue;
-    const int nchunk = (max_keys + DEC_CHUNK - 1) / DEC_CHUNK;
-    float* part = (float*)ws;
-    dim3 grid(H, pl.n_req, nchunk), gm(pl.n_req, H);
-#define DEC(TT, D_)                                                                                    \
-  pi = prof_begin(VFM_PROF_ATTN, s);                                                                   \
-  if (dtype == VFM_BF16)                                                                               \
-    hipLaunchKernelGGL((attn_decode_bf16_kernel<D_, 4>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
-                       d, (const bf16*)k_cache, (const bf16*)v_cache, kv_slots, part, nchunk,       \
-                       scale_log2, (bf16*)out);                                                      \
-  else                                                                                                 \
-    hipLaunchKernelGGL((attn_decode_kernel<float, D_, 4>), grid, dim3(256), 0, s, pl, (const float*)qkv, \
-                       d, (const float*)k_cache, (const float*)v_cache, kv_slots, part, nchunk,     \
-                       scale_log2, (float*)out);                                                     \
-  prof_end(pi, s);                                                                                     \
-  pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
-  hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
-                     nchunk, d, (TT*)out);                                                             \
-  prof_end(pi, s)
-    if (dtype == VFM_BF16) {
-      if (DH == 64) { DEC(bf16, 64); } else { DEC(bf16, 128); }
-    } else {
-      if (DH == 64) { DEC(float, 64); } else { DEC(float, 128); }
-    }
-#undef DEC
-    return hipGetLastError();
-  }
-  pi = prof_begin(VFM_PROF_ATTN, s);
-  dim3 grid(pl.n_qblocks, H);
-  const bool causal = c.attn == VFM_ATTN_CAUSAL;
-  if (dtype == VFM_BF16 && pl.max_seqlen <= 256) {
-    dim3 g2(pl.n_req, H);
-    const int nks = ((pl.max_seqlen + 31) / 32) * 2;   // 16-key sub-tiles, even
+  // Prompts: causal (or bidirectional) attention over each request's own
+  // rows.  In a mixed step this also covers the decode rows, each against
+  // itself only; the decode kernels below overwrite those rows.
+  if (c.attn != VFM_ATTN_DECODE) {
+    pi = prof_begin(VFM_PROF_ATTN, s);
+    dim3 grid(pl.n_qblocks, H);
+    const bool causal = c.attn != VFM_ATTN_BIDIR;
+    if (dtype == VFM_BF16 && pl.max_seqlen <= 256) {
+      dim3 g2(pl.n_req, H);
+      const int nks = ((pl.max_seqlen + 31) / 32) * 2;   // 16-key sub-tiles, even
 #define SHORT(D_, C_, N_)                                                                           \
   hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_, N_>), g2, dim3(256), 0, s, pl, (const bf16*)qkv, \
                      d, (bf16*)out, scale_log2)
@@ -954,25 +968,57 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
     case 10: SHORT(D_, C_, 10); break; case 12: SHORT(D_, C_, 12); break; \
     case 14: SHORT(D_, C_, 14); break; default: SHORT(D_, C_, 16); break; \
   }
-    if (DH == 64) { if (causal) { SHORT_N(64, true); } else { SHORT_N(64, false); } }
-    else { if (causal) { SHORT_N(128, true); } else { SHORT_N(128, false); } }
+      if (DH == 64) { if (causal) { SHORT_N(64, true); } else { SHORT_N(64, false); } }
+      else { if (causal) { SHORT_N(128, true); } else { SHORT_N(128, false); } }
 #undef SHORT_N
 #undef SHORT
-  } else if (dtype == VFM_BF16) {
+    } else if (dtype == VFM_BF16) {
 #define PRE(D_, C_)                                                                            \
   hipLaunchKernelGGL((attn_prefill_bf16_kernel<D_, C_>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
                      d, (bf16*)out, scale_log2)
-    if (DH == 64) { if (causal) PRE(64, true); else PRE(64, false); }
-    else { if (causal) PRE(128, true); else PRE(128, false); }
+      if (DH == 64) { if (causal) PRE(64, true); else PRE(64, false); }
+      else { if (causal) PRE(128, true); else PRE(128, false); }
 #undef PRE
-  } else {
-    if (DH == 64)
-      hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 64>), grid, dim3(256), 0, s, pl,
-                         (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
-    else
-      hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 128>), grid, dim3(256), 0, s, pl,
-                         (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
+    } else {
+      if (DH == 64)
+        hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 64>), grid, dim3(256), 0, s, pl,
+                           (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
+      else
+        hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 128>), grid, dim3(256), 0, s, pl,
+                           (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
+    }
+    prof_end(pi, s);
+    if (!mixed) return hipGetLastError();
   }
-  prof_end(pi, s);
+  // Decode rows: one query against the request's cached keys.
+  if (ws_bytes < attention_workspace(c, pl, max_keys)) return hipErrorInvalidValue;
+  const int nchunk = (max_keys + DEC_CHUNK - 1) / DEC_CHUNK;
+  float* part = (float*)ws;
+  const int mx = mixed ? 1 : 0;
+  dim3 grid(H, pl.n_req, nchunk), gm(pl.n_req, H);
+#define DEC_K(PG, D_)                                                                                     \
+  if (dtype == VFM_BF16)                                                                                   \
+    hipLaunchKernelGGL((attn_decode_bf16_kernel<D_, 4, PG>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
+                       d, (const bf16*)k_cache, (const bf16*)v_cache, kv_slots, kp, mx, part, nchunk,   \
+                       scale_log2, (bf16*)out);                                                          \
+  else                                                                                                     \
+    hipLaunchKernelGGL((attn_decode_kernel<float, D_, 4, PG>), grid, dim3(256), 0, s, pl,                 \
+                       (const float*)qkv, d, (const float*)k_cache, (const float*)v_cache, kv_slots, kp, \
+                       mx, part, nchunk, scale_log2, (float*)out)
+#define DEC(TT, D_)                                                                                    \
+  pi = prof_begin(VFM_PROF_ATTN, s);                                                                   \
+  if (kp.table) { DEC_K(true, D_); } else { DEC_K(false, D_); }                                       \
+  prof_end(pi, s);                                                                                     \
+  pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
+  hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
+                     nchunk, d, mx, (TT*)out);                                                         \
+  prof_end(pi, s)
+  if (dtype == VFM_BF16) {
+    if (DH == 64) { DEC(bf16, 64); } else { DEC(bf16, 128); }
+  } else {
+    if (DH == 64) { DEC(float, 64); } else { DEC(float, 128); }
+  }
+#undef DEC
+#undef DEC_K
   return hipGetLastError();
 }

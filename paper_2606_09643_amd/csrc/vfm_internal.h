@@ -275,19 +275,35 @@ hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
 hipError_t launch_finalize_norm(int dtype, const FinalizeArgs& a, const void* g, const void* b, int kind,
                                 float eps, void* h, hipStream_t s);
 
+// Where the K / V of token k of plan position p live in a head-major cache:
+// slot kv_start[p] + k, or with a page table (original request order,
+// max_pages columns) slot table[order[p]][k >> log2_page] pages in.
+struct KvPages {
+  const int32_t* table;       // device; NULL: contiguous (kv_start)
+  int max_pages, log2_page;
+};
+__device__ inline int64_t kv_slot(const Plan& pl, const KvPages& kp, int p, int k) {
+  if (!kp.table) return (int64_t)pl.kv_start[p] + k;
+  const int pg = kp.table[(int64_t)pl.order[p] * kp.max_pages + (k >> kp.log2_page)];
+  return ((int64_t)pg << kp.log2_page) + (k & ((1 << kp.log2_page) - 1));
+}
+
 // In-place rotary embedding of the q and k parts of qkv [T, 3d]; with
 // k_cache / v_cache (head-major [n_heads, kv_slots, head_dim]) non-null, each
-// row's rotated k and its v are also written to slot kv_start + pos.
+// row's rotated k and its v are also written to its slot (kv_slot of pos).
 hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads, int head_dim,
-                       float theta, void* k_cache, void* v_cache, int64_t kv_slots, hipStream_t s);
+                       float theta, void* k_cache, void* v_cache, int64_t kv_slots, const KvPages& kp,
+                       hipStream_t s);
 
 // Attention per request over qkv [T, 3d] (plan order) into out [T, d].
-// Decode needs attention_workspace() bytes of ws; max_keys = the largest
-// ctx + length over the batch's requests.  kv_written: the rows' K / V are
-// already in the cache (written by the RoPE pass), so no cache write here.
+// Decode and mixed steps need attention_workspace() bytes of ws; max_keys =
+// the largest ctx + length over the batch's requests.  kv_written: the rows'
+// K / V are already in the cache (written by the RoPE pass), so no cache
+// write here.  Mixed steps: prompts (ctx 0) attend causally over their own
+// rows, single-row requests with ctx > 0 over their cached keys.
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv,
-                            void* out, void* k_cache, void* v_cache, int64_t kv_slots, bool kv_written,
-                            void* ws, size_t ws_bytes, int max_keys, hipStream_t s);
+                            void* out, void* k_cache, void* v_cache, int64_t kv_slots, const KvPages& kp,
+                            bool kv_written, void* ws, size_t ws_bytes, int max_keys, hipStream_t s);
 size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys);
 
 // Input rows into the fp32 residual stream (plan order).

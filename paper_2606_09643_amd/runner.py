@@ -99,6 +99,34 @@ class KVCache:
         return take(self.k[li]), take(self.v[li])
 
 
+def paged_from_contiguous(kc, vc, kv_start, n_tok, page_size, rng, spare_pages=0):
+    """A paged copy of a head-major cache: request i's slots kv_start[i] ..
+    kv_start[i] + n_tok[i] - 1 go, in order, to ceil(n_tok[i] / page_size)
+    pages drawn in random order from a pool with `spare_pages` unused ones.
+    Returns (k_pool, v_pool, table [n_req, max_pages] int32)."""
+    n_tok = np.asarray(n_tok, np.int64)
+    need = (n_tok + page_size - 1) // page_size
+    total = int(need.sum()) + int(spare_pages)
+    perm = rng.permutation(total).astype(np.int32)
+    table = np.zeros((len(n_tok), max(int(need.max()), 1)), np.int32)
+    first = np.concatenate([[0], np.cumsum(need)[:-1]])
+    for i in range(len(n_tok)):
+        table[i, :need[i]] = perm[first[i]:first[i] + need[i]]
+    req = np.repeat(np.arange(len(n_tok)), n_tok)
+    pos = np.arange(int(n_tok.sum())) - np.repeat(np.cumsum(n_tok) - n_tok, n_tok)
+    phys = table[req, pos // page_size].astype(np.int64) * page_size + pos % page_size
+    src = np.asarray(kv_start, np.int64)[req] + pos
+    H, _, hd = kc.shape
+    dev = kc.device
+    phys_t, src_t = torch.from_numpy(phys).to(dev), torch.from_numpy(src).to(dev)
+    pools = []
+    for c in (kc, vc):
+        pool = torch.zeros(H, total * page_size, hd, dtype=c.dtype, device=dev)
+        pool[:, phys_t] = c[:, src_t]
+        pools.append(pool)
+    return pools[0], pools[1], table
+
+
 def make_batch(w: wl.Workload, batch: wl.Batch, heads: wl.Heads | None, kv: KVCache | None = None,
                device="cuda") -> B.Batch:
     return B.Batch(batch.task_id, batch.seq_len, w.n_tasks,

@@ -200,3 +200,37 @@ def test_encoder_calls_reject_bad_arguments_before_launching():
     assert att(C.byref(good), -1) == B.VFM_ERR_TASK
     assert att(C.byref(good), 0, fake, fake) == B.VFM_ERR_ARG                        # no bias array
     assert att(None, 0) == B.VFM_ERR_ARG
+
+
+def test_paged_layer_rejects_bad_pages_before_launch():
+    """vfm_layer_forward_paged validates the page size, the page table
+    against the pool and the step kind on the host (nothing is launched when
+    a check fails)."""
+    lib = B.lib()
+    fake = 1 << 20
+    # two decode tokens (ctx 40 and 10) and, for the mixed cases, a prompt
+    host = B.vfm_plan([0, 1], [1, 1], 2, [40, 10], None)
+    bc = _batch_c(host)
+    cfg = B.make_cfg(B.VFM_BF16, 4096, 32, 128, 11008, 1, 1, B.VFM_ATTN_DECODE, 0, 1e-6, 1e4)
+    weights = B.vfm_layer_weights(*([fake] * 13))
+    table = np.array([[3, 1, 2], [0, 0, 0]], np.int32)       # request 0 needs 3 pages of 16, request 1 one
+
+    def run(tab=table, page=16, n_pages=4, c=cfg, batch=bc, k=fake):
+        kv = B.vfm_kv_pages(k, fake, n_pages, page, tab.shape[1],
+                            tab.ctypes.data_as(C.POINTER(C.c_int32)), fake)
+        return lib.vfm_layer_forward_paged(C.byref(c), C.byref(weights), None, C.byref(batch), fake,
+                                           C.byref(kv), fake, 1 << 40, None)
+    assert run(k=None) == B.VFM_ERR_ARG
+    assert run(page=24) == B.VFM_ERR_ARG                       # not a power of two
+    assert run(page=8) == B.VFM_ERR_ARG                        # below 16
+    assert run(n_pages=3) == B.VFM_ERR_SHAPE                   # page 3 is outside the pool
+    assert run(tab=np.array([[3, 1], [0, 0]], np.int32)) == B.VFM_ERR_SHAPE   # 41 tokens need 3 pages
+    assert run(tab=np.array([[3, 1, -1], [0, 0, 0]], np.int32)) == B.VFM_ERR_SHAPE
+    bidir = B.make_cfg(B.VFM_BF16, 4096, 32, 128, 11008, 1, 1, B.VFM_ATTN_BIDIR, 0, 1e-6, 1e4)
+    assert run(c=bidir) == B.VFM_ERR_UNSUPPORTED
+    # mixed steps: a request with cached tokens and more than one new row is chunked prefill
+    mixed = B.make_cfg(B.VFM_BF16, 4096, 32, 128, 11008, 1, 1, B.VFM_ATTN_MIXED, 0, 1e-6, 1e4)
+    chunked = B.vfm_plan([0, 1], [2, 1], 2, [40, 0], None)
+    assert run(c=mixed, batch=_batch_c(chunked)) == B.VFM_ERR_UNSUPPORTED
+    decode_many = B.vfm_plan([0, 1], [1, 5], 2, [0, 0], None)
+    assert run(batch=_batch_c(decode_many)) == B.VFM_ERR_UNSUPPORTED   # decode rows are single

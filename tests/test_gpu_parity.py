@@ -683,3 +683,99 @@ def test_channel_encoder_embed(idx):
     assert O.row_rel_error(got2, ref2) < 1e-5
     other = pl["task"][pl["row_req"]] >= 2
     assert np.array_equal(got2[other], got[other])
+
+
+@pytest.mark.parametrize("page", [16, 64])
+def test_paged_decode_matches_contiguous(page):
+    """A decode layer over a paged cache (pages in random order, spare pages
+    in the pool) gives bit-identical rows to the same layer over the
+    contiguous head-major cache, and writes the new token's K / V into its
+    page.  Contexts 0, 63, 300, 64 and 2048 (three key chunks)."""
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(5)
+    log(f"paged decode, page {page}, ctx {list(batch.ctx)}")
+    fwd.embed()
+    x0 = fwd.x.clone()
+    n_tok = batch.ctx.astype(np.int64) + 1
+    kp, vp, table = R.paged_from_contiguous(kv.k[0], kv.v[0], kv.kv_start, n_tok, page,
+                                            np.random.default_rng(page), spare_pages=7)
+    pkv = B.PagedKV(kp, vp, page, table)
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    x_c = fwd.x.clone()
+    fwd.x.copy_(x0)
+    B.vfm_layer_forward_paged(model.cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, pkv, fwd.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(fwd.x, x_c)
+    for i in range(batch.n_req):
+        c = int(batch.ctx[i])
+        ps = int(table[i, c // page]) * page + c % page
+        cs = int(kv.kv_start[i]) + c
+        assert torch.equal(kp[:, ps], kv.k[0][:, cs]) and torch.equal(vp[:, ps], kv.v[0][:, cs])
+
+
+def _page_rows(pool, table, i, n, page):
+    """Positions 0 .. n-1 of request i from a paged pool, as [n, n_heads * head_dim]."""
+    pos = np.arange(n)
+    phys = table[i, pos // page].astype(np.int64) * page + pos % page
+    rows = pool[:, torch.from_numpy(phys).to(pool.device)]
+    return rows.permute(1, 0, 2).reshape(n, -1)
+
+
+@pytest.mark.parametrize("ctx_long", [300, 2100])
+def test_mixed_prefill_and_decode_step_paged(ctx_long):
+    """One continuous-batching step over a paged cache (7B decoder layer
+    dims, pages of 64 in random order): two prompts (70 and 33 tokens, ctx 0)
+    and three decode tokens (ctx 63, 1100 and a long one) in one batch.  Every
+    row against the oracle (prompts causal over themselves, decode rows over
+    their cached keys plus themselves), and every new row's rotated K and V
+    in its page."""
+    w = wl.WORKLOADS[4]
+    task_id = np.array([3, 0, 3, 63, 5], np.int32)
+    seq_len = np.array([70, 1, 33, 1, 1], np.int32)
+    ctx = np.array([0, 63, 0, ctx_long, 1100], np.int32)
+    batch = wl.Batch(task_id, seq_len, ctx)
+    model = R.Model(w, n_layers=1, b_std=0.1)
+    inp = R.Inputs(w, batch)
+    page = 64
+    n_tok = ctx.astype(np.int64) + seq_len
+    need = (n_tok + page - 1) // page
+    total = int(need.sum()) + 5
+    perm = np.random.default_rng(11).permutation(total).astype(np.int32)
+    table = np.zeros((len(n_tok), int(need.max())), np.int32)
+    first = np.concatenate([[0], np.cumsum(need)[:-1]])
+    for i in range(len(n_tok)):
+        table[i, :need[i]] = perm[first[i]:first[i] + need[i]]
+    g = torch.Generator(device="cuda").manual_seed(13)
+    kp = torch.randn(w.n_heads, total * page, w.head_dim, generator=g, device="cuda").to(torch.bfloat16)
+    vp = torch.randn(w.n_heads, total * page, w.head_dim, generator=g, device="cuda").to(torch.bfloat16)
+    pkv = B.PagedKV(kp, vp, page, table)
+    cfg = R.cfg_for(w)
+    cfg.attn = B.VFM_ATTN_MIXED
+    pb = B.Batch(task_id, seq_len, w.n_tasks, ctx_len=ctx)
+    fwd = R.Forward(model, pb, inp)
+    ws = torch.empty(B.vfm_workspace_size(cfg, pb.c, model.lora_c(0)), dtype=torch.uint8, device="cuda")
+    log(f"mixed step: lens {list(seq_len)} ctx {list(ctx)} T={pb.T}")
+    fwd.embed()
+    x_in = fwd.x.double().cpu().numpy()
+    B.vfm_layer_forward_paged(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, pkv, ws)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    pl = O.plan(task_id, seq_len, w.n_tasks, ctx=ctx)
+    spec = spec_of(w)
+    W_np = oracle_weights(model.layers[0])
+    cu = pl["cu_seqlens"]
+    worst = 0.0
+    for p in range(batch.n_req):
+        sl = slice(int(cu[p]), int(cu[p + 1]))
+        i, t = int(pl["order"][p]), int(pl["task"][p])
+        c, L = int(ctx[i]), int(seq_len[i])
+        kvp = None
+        if c > 0:
+            kvp = (np64(_page_rows(kp, table, i, c, page)), np64(_page_rows(vp, table, i, c, page)))
+        y, k, v = O.layer(spec, W_np, oracle_adapter(model.adapters[0], t), x_in[sl], pos=pl["pos"][sl], kv=kvp)
+        worst = max(worst, O.row_rel_error(got[sl], y))
+        k_new = np64(_page_rows(kp, table, i, c + L, page))[c:]
+        v_new = np64(_page_rows(vp, table, i, c + L, page))[c:]
+        assert O.row_rel_error(k_new, k) < tol(w) and O.row_rel_error(v_new, v) < tol(w)
+    log(f"  max rel err {worst:.3e}")
+    assert worst < tol(w)
