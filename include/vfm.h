@@ -237,6 +237,15 @@ int vfm_head_attach(const vfm_head_table* table, int32_t task, int32_t n_out, co
 int vfm_encoder_attach(const vfm_encoder_table* table, int32_t task, const float* W, const float* b,
                        void* stream);
 
+/* Greedy decoding of token-based FMs: the next token of each request is the
+ * index of its largest head output (a task's LM head over the vocabulary, a
+ * per-task decoder of Section 2.2), taken for every request of the batch in
+ * one launch.  out: device float32 head outputs (vfm_head_forward's layout,
+ * request i at out_off[i], original order); ids: device int32 [n_req],
+ * original order.  Ties go to the lowest index; NaN outputs are never
+ * chosen; a request with no non-NaN output gets -1. */
+int vfm_greedy_tokens(const vfm_batch* batch, const float* out, int32_t* ids, void* stream);
+
 /* Device workspace needed by vfm_layer_forward / vfm_lora_apply /
  * vfm_head_forward for this batch (lora may be NULL). */
 int vfm_workspace_size(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_lora_table* lora,

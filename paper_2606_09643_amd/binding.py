@@ -37,7 +37,9 @@ EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size
            "vfm_profile_enable", "vfm_profile_read",
            "vfm_bfq_state_size", "vfm_bfq_init", "vfm_bfq_enqueue", "vfm_bfq_next_batch",
            "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach",
-           "vfm_embed_series", "vfm_encoder_attach", "vfm_layer_forward_paged")
+           "vfm_embed_series", "vfm_encoder_attach", "vfm_layer_forward_paged", "vfm_greedy_tokens",
+           "vfm_pages_state_size", "vfm_pages_init", "vfm_pages_reserve", "vfm_pages_release",
+           "vfm_pages_table", "vfm_pages_count")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -81,6 +83,11 @@ class vfm_kv_pages(C.Structure):
                 ("max_pages", C.c_int32), ("table_host", C.POINTER(C.c_int32)), ("table_dev", C.c_void_p)]
 
 
+class vfm_pages_config(C.Structure):
+    _fields_ = [("n_pages", C.c_int32), ("page_size", C.c_int32), ("max_seqs", C.c_int32),
+                ("max_pages", C.c_int32)]
+
+
 _LIB = None
 
 
@@ -107,6 +114,13 @@ def _lib_handle():
         lib.vfm_layer_forward_paged.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_layer_weights),
                                                 C.POINTER(vfm_lora_table), C.POINTER(vfm_batch), C.c_void_p,
                                                 C.POINTER(vfm_kv_pages), C.c_void_p, C.c_size_t, C.c_void_p]
+        lib.vfm_greedy_tokens.argtypes = [C.POINTER(vfm_batch), C.c_void_p, C.c_void_p, C.c_void_p]
+        lib.vfm_pages_state_size.argtypes = [C.POINTER(vfm_pages_config), C.POINTER(C.c_size_t)]
+        lib.vfm_pages_init.argtypes = [C.POINTER(vfm_pages_config), C.c_void_p, C.c_size_t]
+        lib.vfm_pages_reserve.argtypes = [C.c_void_p, C.c_int32, C.c_int64]
+        lib.vfm_pages_release.argtypes = [C.c_void_p, C.c_int32]
+        lib.vfm_pages_table.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32]
+        lib.vfm_pages_count.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
         lib.vfm_lora_apply.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                        C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
@@ -303,6 +317,12 @@ class Batch:
     def total_outputs(self):
         return int(self.host[6])
 
+    def out_off(self):
+        """out_off[n_req + 1] of the host plan: first head output of request i (original order)."""
+        n, t = self.n_req, int(self.host[1])
+        o = VFM_PLAN_HEADER + n + n + (n + 1) + (t + 1) + (t + 1) + (n + 1)
+        return self.host[o:o + n + 1]
+
 
 def layer_weights(W: dict) -> vfm_layer_weights:
     return vfm_layer_weights(*[_ptr(W.get(n)) for n, _ in vfm_layer_weights._fields_])
@@ -404,6 +424,49 @@ def vfm_embed_series(cfg, batch, enc, src, patch, W_pe, b_pe, x, stream=None):
 def vfm_encoder_attach(enc, task, W=None, b=None, stream=None):
     st = _lib_handle().vfm_encoder_attach(C.byref(enc.c), int(task), _ptr(W), _ptr(b), _stream(stream))
     _check(st, "vfm_encoder_attach")
+
+
+def vfm_greedy_tokens(batch, out, ids, stream=None):
+    _check(_lib_handle().vfm_greedy_tokens(C.byref(batch), _ptr(out), _ptr(ids), _stream(stream)),
+           "vfm_greedy_tokens")
+
+
+# ---- KV page allocator (host, include/vfm_pages.h) --------------------------
+class PageAllocator:
+    """The library's page allocator on a host state buffer (numpy-owned)."""
+
+    def __init__(self, n_pages, page_size, max_seqs, max_pages):
+        self.cfg = vfm_pages_config(int(n_pages), int(page_size), int(max_seqs), int(max_pages))
+        self.page_size, self.max_pages = int(page_size), int(max_pages)
+        n = C.c_size_t()
+        _check(_lib_handle().vfm_pages_state_size(C.byref(self.cfg), C.byref(n)), "vfm_pages_state_size")
+        self.state = np.zeros((n.value + 7) // 8, np.int64)      # 8-byte aligned
+        _check(_lib_handle().vfm_pages_init(C.byref(self.cfg), self.state.ctypes.data, self.state.nbytes),
+               "vfm_pages_init")
+
+    def reserve(self, seq, n_tokens):
+        _check(_lib_handle().vfm_pages_reserve(self.state.ctypes.data, int(seq), int(n_tokens)),
+               "vfm_pages_reserve")
+
+    def try_reserve(self, seq, n_tokens) -> bool:
+        return _lib_handle().vfm_pages_reserve(self.state.ctypes.data, int(seq), int(n_tokens)) == VFM_OK
+
+    def release(self, seq):
+        _check(_lib_handle().vfm_pages_release(self.state.ctypes.data, int(seq)), "vfm_pages_release")
+
+    def table(self, seqs, max_cols=None):
+        seqs = np.ascontiguousarray(seqs, np.int32)
+        cols = self.max_pages if max_cols is None else int(max_cols)
+        out = np.empty((len(seqs), cols), np.int32)
+        _check(_lib_handle().vfm_pages_table(self.state.ctypes.data, seqs.ctypes.data, len(seqs),
+                                             out.ctypes.data, cols), "vfm_pages_table")
+        return out
+
+    def count(self, seq):
+        h, f = C.c_int32(), C.c_int32()
+        _check(_lib_handle().vfm_pages_count(self.state.ctypes.data, int(seq), C.byref(h), C.byref(f)),
+               "vfm_pages_count")
+        return h.value, f.value
 
 
 # ---- batch-aware fair queueing (host scheduler, include/vfm_bfq.h) --------

@@ -482,3 +482,10 @@ extern "C" int vfm_head_forward(const vfm_cfg* cfg, const void* final_norm_w,
   VFM_HIP(launch_heads(c.dtype, pl, workspace, c.d_model, *heads, out, s));
   return VFM_OK;
 }
+
+extern "C" int vfm_greedy_tokens(const vfm_batch* batch, const float* out, int32_t* ids, void* stream) {
+  Plan pl;
+  VFM_TRY(check_batch(batch, &pl));
+  if (!out || !ids) return VFM_ERR_ARG;
+  return hip_status(launch_greedy(pl, out, ids, (hipStream_t)stream));
+}

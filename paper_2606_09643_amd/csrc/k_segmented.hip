@@ -361,6 +361,46 @@ __global__ __launch_bounds__(256) void heads_f32_kernel(Plan pl, const float* __
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Greedy token selection: one block per request (original order), each
+// thread scans a strided share of the request's outputs, then the wave and
+// the block reduce (value, index) pairs.
+// ---------------------------------------------------------------------------
+__device__ inline bool greedy_better(float v, int i, float bv, int bi) {
+  if (i < 0) return false;
+  if (bi < 0) return true;
+  return v > bv || (v == bv && i < bi);
+}
+
+__global__ __launch_bounds__(256) void greedy_kernel(Plan pl, const float* __restrict__ out,
+                                                     int32_t* __restrict__ ids) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int i = blockIdx.x;
+  const int o0 = pl.out_off[i], n = pl.out_off[i + 1] - o0;
+  float bv = 0.f;
+  int bi = -1;
+  for (int j = threadIdx.x; j < n; j += 256) {
+    const float v = out[o0 + j];
+    if (v == v && greedy_better(v, j, bv, bi)) { bv = v; bi = j; }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(bv, off, 64);
+    const int oi = __shfl_xor(bi, off, 64);
+    if (greedy_better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) { sv[wave] = bv; si[wave] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (greedy_better(sv[w], si[w], bv, bi)) { bv = sv[w]; bi = si[w]; }
+    ids[i] = bi;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s) {
@@ -412,5 +452,10 @@ hipError_t launch_heads(int dtype, const Plan& pl, const void* pooled, int d,
   else
     hipLaunchKernelGGL((heads_f32_kernel<false>), grid, dim3(256), 0, s, pl, (const float*)pooled, d, h,
                        (float*)hid, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_greedy(const Plan& pl, const float* out, int32_t* ids, hipStream_t s) {
+  hipLaunchKernelGGL(greedy_kernel, dim3(pl.n_req), dim3(256), 0, s, pl, out, ids);
   return hipGetLastError();
 }

@@ -319,3 +319,8 @@ hipError_t launch_norm_pool(int dtype, const Plan& pl, const float* x, int d, co
 // Per-task heads on pooled rows: out[out_off[i] + j] = pooled[p] . W_t[j] + b_t[j].
 hipError_t launch_heads(int dtype, const Plan& pl, const void* pooled, int d,
                         const vfm_head_table& h, float* out, hipStream_t s);
+
+// Greedy next token per request: ids[i] = argmax of out[out_off[i] ..
+// out_off[i + 1]) (original order), ties to the lowest index, NaN never
+// chosen, -1 when nothing can be.
+hipError_t launch_greedy(const Plan& pl, const float* out, int32_t* ids, hipStream_t s);

@@ -173,3 +173,167 @@ class Forward:
             self.layer(li, stream)
         self.head(stream)
         return self.out
+
+
+class _Seq:
+    __slots__ = ("rid", "task", "prompt", "max_new", "slot", "cached", "generated", "budget")
+
+    def __init__(self, rid, task, prompt, max_new, page_size):
+        self.rid, self.task = rid, int(task)
+        self.prompt = np.asarray(prompt, np.int32)
+        self.max_new = int(max_new)
+        self.slot = -1
+        self.cached = 0                 # tokens whose K / V are in the pages
+        self.generated = []
+        # pages for every token that will ever be written (the last generated one never is)
+        self.budget = -(-(len(self.prompt) + self.max_new - 1) // page_size)
+
+
+class ContinuousBatcher:
+    """Iteration-level (continuous) batching of a token-based FM over a paged
+    KV cache.  Every step runs ONE mixed batch through all layers: the newly
+    admitted prompts (ctx 0, their whole prompt) and one decode row for each
+    running sequence (ctx = its cached tokens), then the final norm, each
+    request's task head (pooled on its last row) and a greedy pick of its next
+    token.  Pages come from the library's allocator as sequences grow and go
+    back the moment a sequence finishes.
+
+    Admission is FIFO, or BFQ order when a B.BFQ scheduler is given (its
+    batches are taken whole, only when b_max more sequences fit).  A prompt
+    is admitted only when a sequence slot is free, its tokens fit the step's
+    token budget, and the pages it will ever need fit next to those the
+    running sequences may still need, so a running sequence never waits for
+    a page (no preemption).  The host decides only the schedule; every row
+    of the step is computed by the library's kernels."""
+
+    def __init__(self, model: Model, emb, page_size=64, n_pages=1024, max_seqs=256, max_step_tokens=8192,
+                 max_pages=None, bfq=None, record=False, device="cuda"):
+        w = model.w
+        self.m, self.emb, self.device = model, emb, device
+        self.page_size, self.n_pages = int(page_size), int(n_pages)
+        self.max_seqs, self.max_step_tokens = int(max_seqs), int(max_step_tokens)
+        self.max_pages = int(max_pages) if max_pages is not None else self.n_pages
+        self.alloc = B.PageAllocator(self.n_pages, self.page_size, self.max_seqs, self.max_pages)
+        shape = (w.n_heads, self.n_pages * self.page_size, w.head_dim)
+        self.k = [torch.zeros(shape, dtype=w.torch_dtype, device=device) for _ in range(model.n_layers)]
+        self.v = [torch.zeros(shape, dtype=w.torch_dtype, device=device) for _ in range(model.n_layers)]
+        self.cfg = B.vfm_cfg.from_buffer_copy(model.cfg)
+        self.cfg.attn = B.VFM_ATTN_MIXED
+        self.bfq, self.record = bfq, record
+        self.waiting, self.running, self.done = [], [], {}
+        self.requests = {}
+        self.free_slots = list(range(self.max_seqs - 1, -1, -1))
+        self.committed = 0              # pages the running sequences hold or may still take
+        self.ws = torch.empty(0, dtype=torch.uint8, device=device)
+        self.steps = 0
+        self.trace = []                 # per step: [(rid, logits)] when record is set
+
+    def submit(self, rid, task, prompt, max_new, now=0.0):
+        s = _Seq(rid, task, prompt, max_new, self.page_size)
+        if s.budget > self.max_pages or len(s.prompt) < 1 or s.max_new < 1:
+            raise ValueError(f"request {rid}: needs {s.budget} pages (max {self.max_pages}) or is empty")
+        self.requests[rid] = s
+        if self.bfq is not None:
+            self.bfq.enqueue(s.task, rid, now)
+        self.waiting.append(s)
+
+    def _fits(self, s, tokens):
+        return (self.free_slots and tokens + len(s.prompt) <= self.max_step_tokens
+                and self.committed + s.budget <= self.n_pages)
+
+    def _admit_one(self, s):
+        s.slot = self.free_slots.pop()
+        self.committed += s.budget
+        self.waiting.remove(s)
+        self.running.append(s)
+
+    def _admit(self, now):
+        tokens = len(self.running)                   # one decode row per running sequence
+        new = []
+        if self.bfq is None:
+            for s in list(self.waiting):
+                if not self._fits(s, tokens):
+                    break
+                self._admit_one(s)
+                new.append(s)
+                tokens += len(s.prompt)
+            return new
+        while self.waiting:
+            worst = max(len(s.prompt) for s in self.waiting)
+            wb = max(s.budget for s in self.waiting)
+            b = self.bfq.b_max
+            if (len(self.free_slots) < b or tokens + b * worst > self.max_step_tokens
+                    or self.committed + b * wb > self.n_pages):
+                break
+            for rid, _ in self.bfq.next_batch(now):
+                s = self.requests[rid]
+                self._admit_one(s)
+                new.append(s)
+                tokens += len(s.prompt)
+        return new
+
+    def step(self, now=0.0):
+        """One continuous-batching step; returns the ids of the requests that finished."""
+        new = self._admit(now)
+        batch = [s for s in self.running if s not in new] + new
+        if not batch:
+            return []
+        w = self.m.w
+        task = np.array([s.task for s in batch], np.int32)
+        lens = np.array([1 if s.cached else len(s.prompt) for s in batch], np.int32)
+        ctx = np.array([s.cached for s in batch], np.int32)
+        ids = np.concatenate([s.prompt if not s.cached else np.array([s.generated[-1]], np.int32)
+                              for s in batch]).astype(np.int32)
+        for s, c, n in zip(batch, ctx, lens):
+            self.alloc.reserve(s.slot, int(c) + int(n))
+        slots = np.array([s.slot for s in batch], np.int32)
+        table = self.alloc.table(slots, max(int(self.alloc.count(int(x))[0]) for x in slots))
+        table_dev = torch.from_numpy(table).to(self.device)
+        pb = B.Batch(task, lens, w.n_tasks, ctx_len=ctx, n_out=self.m.heads.n_out, device=self.device)
+        need = max(B.vfm_workspace_size(self.cfg, pb.c, self.m.lora_c(i)) for i in range(self.m.n_layers))
+        if need > self.ws.numel():
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        x = torch.empty(pb.T, w.d, dtype=torch.float32, device=self.device)
+        ids_dev = torch.from_numpy(ids).to(self.device)
+        B.vfm_embed_forward(self.cfg, pb.c, B.VFM_EMBED_TOKENS, ids_dev, w.vocab, self.emb, None, x)
+        tp = table.ctypes.data_as(B.C.POINTER(B.C.c_int32))
+        for li in range(self.m.n_layers):
+            kv = B.vfm_kv_pages(self.k[li].data_ptr(), self.v[li].data_ptr(), self.n_pages, self.page_size,
+                                table.shape[1], tp, table_dev.data_ptr())
+            st = B.lib().vfm_layer_forward_paged(B.C.byref(self.cfg), B.C.byref(self.m.c_layers[li]),
+                                                 B.C.byref(self.m.lora[li].c) if self.m.lora[li] else None,
+                                                 B.C.byref(pb.c), x.data_ptr(), B.C.byref(kv),
+                                                 self.ws.data_ptr(), self.ws.numel(), B._stream(None))
+            B._check(st, "vfm_layer_forward_paged")
+        out = torch.empty(max(pb.total_outputs, 1), dtype=torch.float32, device=self.device)
+        fn = self.m.final
+        B.vfm_head_forward(self.cfg, fn["w"], fn.get("b"), self.m.head_tab.c, pb.c, x, out, self.ws)
+        nxt = torch.empty(len(batch), dtype=torch.int32, device=self.device)
+        B.vfm_greedy_tokens(pb.c, out, nxt)
+        nxt_h = nxt.cpu().numpy()                    # waits for the step
+        if self.record:
+            off = pb.out_off()
+            o = out.cpu().numpy()
+            self.trace.append([(s.rid, o[off[i]:off[i + 1]].copy()) for i, s in enumerate(batch)])
+        finished = []
+        for i, s in enumerate(batch):
+            s.cached += int(lens[i])
+            s.generated.append(int(nxt_h[i]))
+            if len(s.generated) == s.max_new:
+                self.alloc.release(s.slot)
+                self.free_slots.append(s.slot)
+                self.committed -= s.budget
+                self.running.remove(s)
+                self.done[s.rid] = list(s.generated)
+                finished.append(s.rid)
+        self.steps += 1
+        return finished
+
+    def run(self, now=0.0):
+        """Steps until every submitted request has finished."""
+        while self.waiting or self.running:
+            before = (len(self.waiting), len(self.running))
+            self.step(now)
+            if not self.running and (len(self.waiting), len(self.running)) == before:
+                raise RuntimeError("a waiting request can never be admitted")
+        return self.done
