@@ -181,6 +181,56 @@ def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
                       f"{elapsed:.1f} s"}
 
 
+def loop_bench(args):
+    """Continuous batching of the 7B decoder workload's model (all layers,
+    128 tasks with rank-16 LoRA on every projection, per-task heads): n
+    requests with prompts of U[64, 512] tokens and U[32, 128] new tokens each,
+    at most 256 running sequences, pages of 64 slots, prompts admitted FIFO up
+    to 8192 tokens per step.  Timed from the first step to the last request
+    finishing, host scheduling and the per-step token read-back included."""
+    import torch
+    from paper_2606_09643_amd import runner as R
+    from paper_2606_09643_amd import workloads as wl
+    w = wl.WORKLOADS[5]
+    model = R.Model(w)
+    one = wl.Batch(np.zeros(1, np.int32), np.ones(1, np.int32), None)
+    _, emb = wl.token_inputs(w, one, "cuda")
+    rng = np.random.default_rng(20260601)
+    n = args.loop
+    tasks = rng.choice(w.n_tasks, size=n, p=wl.zipf_probs(w.n_tasks, w.zipf_s))
+    plen = rng.integers(64, 513, size=n)
+    new = rng.integers(32, 129, size=n)
+    page, max_seqs = 64, 256
+    n_pages = max_seqs * ((512 + 128 + page - 1) // page)
+
+    def make():
+        cb = R.ContinuousBatcher(model, emb, page_size=page, n_pages=n_pages, max_seqs=max_seqs,
+                                 max_step_tokens=8192, max_pages=(512 + 128 + page - 1) // page)
+        for i in range(n):
+            cb.submit(i, int(tasks[i]), rng.integers(0, w.vocab, size=int(plen[i])), int(new[i]))
+        return cb
+    warm = make()                                      # warm-up run (kernels, allocator caches)
+    for _ in range(3):
+        warm.step()
+    del warm
+    cb = make()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    cb.run()
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    gen = int(new.sum())
+    out = {"metric": "continuous-batching generated tokens/s at 1 GPU (paged KV, mixed prefill + decode steps)",
+           "value": gen / sec, "unit": "tokens/s", "n_gpus": 1, "steps": cb.steps,
+           "ms_per_step": sec * 1e3 / cb.steps, "higher_is_better": True, "vs_baseline": None,
+           "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": w.name + " continuous batching", "requests": n,
+                      "prompt_tokens": int(plen.sum()), "generated_tokens": gen, "max_running": max_seqs,
+                      "page_size": page, "max_step_tokens": 8192, "admission": "fifo"},
+           "seconds": sec}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,12 +238,21 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--loop", type=int, default=0,
+                    help="run the continuous-batching loop over this many requests instead of one step")
+    ap.add_argument("--paged", type=int, default=0,
+                    help="decode workloads: read the KV cache through pages of this many slots "
+                         "(random page order) instead of the contiguous cache")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-task forward "
               "shards by request with no cross-GPU exchange, and this build measures one GPU's "
               "share.", file=sys.stderr)
         sys.exit(2)
+
+    if args.loop:
+        loop_bench(args)
+        return
 
     import torch
     from paper_2606_09643_amd import binding as B
@@ -207,6 +266,12 @@ def main():
     kv = R.KVCache(w, batch, w.n_layers) if w.mode == "decode" else None
     pb = R.make_batch(w, batch, model.heads, kv)
     fwd = R.Forward(model, pb, inp, kv)
+    if args.paged:
+        if kv is None:
+            print("--paged applies to decode workloads only", file=sys.stderr)
+            sys.exit(2)
+        fwd.paged = R.page_kv_cache(kv, batch, args.paged)
+        torch.cuda.empty_cache()
     ranks = wl.task_ranks(w)
     work = algorithmic_work(w, batch, ranks, model.heads.n_out if model.heads is not None else None)
     stream = torch.cuda.current_stream()
@@ -255,7 +320,7 @@ def main():
                 "frac": achieved / peak, "traffic": None}
     roof["traffic"] = hbm_traffic(w.name, dom)
     if dom == "attn":
-        kname = "attn_decode_kernel (KV-cache attention)"
+        kname = "attn_decode_kernel (KV-cache attention" + (f", pages of {args.paged})" if args.paged else ")")
     elif w.dtype != "bf16":
         kname = "gemm_f32_kernel (MLP up projection + GELU)"
     elif w.family == "decoder":
@@ -275,13 +340,16 @@ def main():
         "config": {"workload": w.name, "n_req": w.n_req, "tokens": tokens,
                    "n_tasks": w.n_tasks, "distinct_tasks": int(len(np.unique(batch.task_id))),
                    "layers": w.n_layers, "d_model": w.d, "d_ff": w.d_ff, "lora_rank": w.rank,
-                   "lora_targets": list(w.lora_targets)},
+                   "lora_targets": list(w.lora_targets),
+                   "kv_cache": f"paged {args.paged}" if args.paged else "contiguous"},
         "step_tflops": step_tflops,
         "step_roofline_frac": step_tflops / peak_step if w.mode != "decode" else
         (work["step_bytes"] / (ms_step * 1e-3) / 1e9) / PEAK_HBM_GBS,
         "roofline": roof,
     }
-    if not args.no_cpu_baseline:
+    if args.paged:
+        roof["traffic"] = None          # counters were taken on the contiguous cache
+    if not args.no_cpu_baseline and not args.paged:
         out["cpu_baseline"] = cpu_baseline(w, batch, model, inp, kv)
     print(json.dumps(out), flush=True)
 

@@ -299,9 +299,12 @@ class Batch:
     """A planned batch: host plan, its device copy and the C struct."""
 
     def __init__(self, task_id, seq_len, n_tasks, ctx_len=None, kv_start=None, n_out=None,
-                 device="cuda"):
+                 device="cuda", non_blocking=False):
         self.host = vfm_plan(task_id, seq_len, n_tasks, ctx_len, kv_start, n_out)
-        self.dev = torch.from_numpy(self.host).to(device)
+        if non_blocking:     # staged through pinned memory: the host does not wait for the stream
+            self.dev = torch.from_numpy(self.host).pin_memory().to(device, non_blocking=True)
+        else:
+            self.dev = torch.from_numpy(self.host).to(device)
         self.c = vfm_batch(self.host.ctypes.data_as(C.POINTER(C.c_int32)), self.dev.data_ptr(),
                            self.host.size)
 

@@ -127,6 +127,21 @@ def paged_from_contiguous(kc, vc, kv_start, n_tok, page_size, rng, spare_pages=0
     return pools[0], pools[1], table
 
 
+def page_kv_cache(kv: KVCache, batch: wl.Batch, page_size, seed=0):
+    """Moves every layer of a contiguous decode cache into a paged pool
+    (pages in random order), freeing the contiguous copy layer by layer;
+    returns the per-layer B.PagedKV."""
+    n_tok = batch.ctx.astype(np.int64) + batch.seq_len
+    out = []
+    for li in range(len(kv.k)):
+        kp, vp, table = paged_from_contiguous(kv.k[li], kv.v[li], kv.kv_start, n_tok, page_size,
+                                              np.random.default_rng(seed + li))
+        kv.k[li] = kv.v[li] = None
+        torch.cuda.empty_cache()        # the next layer's pool reuses this layer's memory
+        out.append(B.PagedKV(kp, vp, page_size, table))
+    return out
+
+
 def make_batch(w: wl.Workload, batch: wl.Batch, heads: wl.Heads | None, kv: KVCache | None = None,
                device="cuda") -> B.Batch:
     return B.Batch(batch.task_id, batch.seq_len, w.n_tasks,
@@ -141,6 +156,7 @@ class Forward:
     def __init__(self, model: Model, pb: B.Batch, inputs: Inputs, kv: KVCache | None = None,
                  device="cuda"):
         self.m, self.pb, self.inp, self.kv = model, pb, inputs, kv
+        self.paged = None               # per layer B.PagedKV: the layers read a paged cache instead
         w = model.w
         need = max(B.vfm_workspace_size(model.cfg, pb.c, model.lora_c(i)) for i in range(model.n_layers))
         self.ws = torch.empty(need, dtype=torch.uint8, device=device)
@@ -155,6 +171,10 @@ class Forward:
         B.vfm_embed_forward(self.m.cfg, self.pb.c, i.mode, i.src, i.width, i.table, i.bias, self.x, stream)
 
     def layer(self, li, stream=None):
+        if self.paged is not None:
+            B.vfm_layer_forward_paged(self.m.cfg, self.m.c_layers[li], self.m.lora_c(li), self.pb.c, self.x,
+                                      self.paged[li], self.ws, stream)
+            return
         kc = self.kv.k[li] if self.kv is not None else None
         vc = self.kv.v[li] if self.kv is not None else None
         slots = self.kv.slots if self.kv is not None else 0
@@ -176,7 +196,7 @@ class Forward:
 
 
 class _Seq:
-    __slots__ = ("rid", "task", "prompt", "max_new", "slot", "cached", "generated", "budget")
+    __slots__ = ("rid", "task", "prompt", "max_new", "slot", "cached", "generated", "budget", "row")
 
     def __init__(self, rid, task, prompt, max_new, page_size):
         self.rid, self.task = rid, int(task)
@@ -184,7 +204,8 @@ class _Seq:
         self.max_new = int(max_new)
         self.slot = -1
         self.cached = 0                 # tokens whose K / V are in the pages
-        self.generated = []
+        self.generated = []             # (step, index in that step's batch) of each new token
+        self.row = -1                   # index in the latest step's batch
         # pages for every token that will ever be written (the last generated one never is)
         self.budget = -(-(len(self.prompt) + self.max_new - 1) // page_size)
 
@@ -227,6 +248,7 @@ class ContinuousBatcher:
         self.ws = torch.empty(0, dtype=torch.uint8, device=device)
         self.steps = 0
         self.trace = []                 # per step: [(rid, logits)] when record is set
+        self._picks, self._prev_nxt, self._keep = [], None, None
 
     def submit(self, rid, task, prompt, max_new, now=0.0):
         s = _Seq(rid, task, prompt, max_new, self.page_size)
@@ -272,8 +294,19 @@ class ContinuousBatcher:
                 tokens += len(s.prompt)
         return new
 
+    def _h2d(self, arr):
+        """Host array -> device without waiting for the stream (pinned staging)."""
+        return torch.from_numpy(np.ascontiguousarray(arr)).pin_memory().to(self.device, non_blocking=True)
+
     def step(self, now=0.0):
-        """One continuous-batching step; returns the ids of the requests that finished."""
+        """One continuous-batching step; returns the ids of the requests that finished.
+
+        Nothing here waits for the GPU (unless `record` is set): a decode
+        row's input token is gathered on the device from the previous step's
+        greedy picks, the host copies go through pinned memory, and a
+        sequence finishes by its token count, so the host plans step n + 1
+        while the GPU still runs step n.  Token values are read back by
+        `tokens()`."""
         new = self._admit(now)
         batch = [s for s in self.running if s not in new] + new
         if not batch:
@@ -282,19 +315,25 @@ class ContinuousBatcher:
         task = np.array([s.task for s in batch], np.int32)
         lens = np.array([1 if s.cached else len(s.prompt) for s in batch], np.int32)
         ctx = np.array([s.cached for s in batch], np.int32)
-        ids = np.concatenate([s.prompt if not s.cached else np.array([s.generated[-1]], np.int32)
-                              for s in batch]).astype(np.int32)
         for s, c, n in zip(batch, ctx, lens):
             self.alloc.reserve(s.slot, int(c) + int(n))
         slots = np.array([s.slot for s in batch], np.int32)
         table = self.alloc.table(slots, max(int(self.alloc.count(int(x))[0]) for x in slots))
-        table_dev = torch.from_numpy(table).to(self.device)
-        pb = B.Batch(task, lens, w.n_tasks, ctx_len=ctx, n_out=self.m.heads.n_out, device=self.device)
+        table_dev = self._h2d(table)
+        pb = B.Batch(task, lens, w.n_tasks, ctx_len=ctx, n_out=self.m.heads.n_out, device=self.device,
+                     non_blocking=True)
         need = max(B.vfm_workspace_size(self.cfg, pb.c, self.m.lora_c(i)) for i in range(self.m.n_layers))
         if need > self.ws.numel():
             self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
         x = torch.empty(pb.T, w.d, dtype=torch.float32, device=self.device)
-        ids_dev = torch.from_numpy(ids).to(self.device)
+        # input tokens, original order: decode rows' last picks (on device), then the prompts
+        n_dec = len(batch) - len(new)
+        parts = []
+        if n_dec:
+            parts.append(self._prev_nxt[self._h2d(np.array([s.row for s in batch[:n_dec]], np.int64))])
+        if new:
+            parts.append(self._h2d(np.concatenate([s.prompt for s in new]).astype(np.int32)))
+        ids_dev = torch.cat(parts) if len(parts) > 1 else parts[0]
         B.vfm_embed_forward(self.cfg, pb.c, B.VFM_EMBED_TOKENS, ids_dev, w.vocab, self.emb, None, x)
         tp = table.ctypes.data_as(B.C.POINTER(B.C.c_int32))
         for li in range(self.m.n_layers):
@@ -310,7 +349,9 @@ class ContinuousBatcher:
         B.vfm_head_forward(self.cfg, fn["w"], fn.get("b"), self.m.head_tab.c, pb.c, x, out, self.ws)
         nxt = torch.empty(len(batch), dtype=torch.int32, device=self.device)
         B.vfm_greedy_tokens(pb.c, out, nxt)
-        nxt_h = nxt.cpu().numpy()                    # waits for the step
+        self._prev_nxt = nxt
+        self._picks.append(nxt)
+        self._keep = (pb, table, table_dev)            # host arrays the stream may still read
         if self.record:
             off = pb.out_off()
             o = out.cpu().numpy()
@@ -318,16 +359,25 @@ class ContinuousBatcher:
         finished = []
         for i, s in enumerate(batch):
             s.cached += int(lens[i])
-            s.generated.append(int(nxt_h[i]))
+            s.generated.append((self.steps, i))
+            s.row = i
             if len(s.generated) == s.max_new:
                 self.alloc.release(s.slot)
                 self.free_slots.append(s.slot)
                 self.committed -= s.budget
                 self.running.remove(s)
-                self.done[s.rid] = list(s.generated)
+                self.done[s.rid] = s
                 finished.append(s.rid)
         self.steps += 1
         return finished
+
+    def tokens(self):
+        """{request id: generated token ids} of the finished requests (one read-back)."""
+        if not self._picks:
+            return {}
+        flat = torch.cat(self._picks).cpu().numpy()
+        base = np.concatenate([[0], np.cumsum([len(p) for p in self._picks])])
+        return {rid: [int(flat[base[st] + i]) for st, i in s.generated] for rid, s in self.done.items()}
 
     def run(self, now=0.0):
         """Steps until every submitted request has finished."""
@@ -336,4 +386,4 @@ class ContinuousBatcher:
             self.step(now)
             if not self.running and (len(self.waiting), len(self.running)) == before:
                 raise RuntimeError("a waiting request can never be admitted")
-        return self.done
+        return self.tokens()
