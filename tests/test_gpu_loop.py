@@ -87,6 +87,14 @@ def test_continuous_batching_loop(dtype, page, sched):
             assert ref[j][gen[j]] >= ref[j].max() - tol(w) * np.abs(ref[j]).max()
     log(f"  max rel err {worst:.3e}")
     assert worst < tol(w)
+    # the same requests through the asynchronous path (no per-step read-back)
+    # pick the same tokens
+    bfq2 = B.BFQ([1.0, 2.0, 1.0], np.linspace(1.0, 2.0, 3), b_max=2) if sched == "bfq" else None
+    cb2 = R.ContinuousBatcher(model, emb, page_size=page, n_pages=12, max_seqs=3, max_step_tokens=96,
+                              max_pages=6, bfq=bfq2)
+    for rid, ((task, _, n_new), pr) in enumerate(zip(REQUESTS, prompts)):
+        cb2.submit(rid, task, pr, n_new)
+    assert cb2.run() == done and cb2.steps == cb.steps
 
 
 def test_greedy_tokens_ties_nan_and_empty():
