@@ -245,9 +245,11 @@ class PagedKV:
 
 
 def vfm_layer_forward_paged(cfg, weights, lora, batch, x, kv, workspace, stream=None):
+    """kv: a PagedKV, or a vfm_kv_pages struct built by the caller."""
+    kvc = kv.c if isinstance(kv, PagedKV) else kv
     st = _lib_handle().vfm_layer_forward_paged(C.byref(cfg), C.byref(weights),
                                                C.byref(lora) if lora is not None else None,
-                                               C.byref(batch), _ptr(x), C.byref(kv.c), workspace.data_ptr(),
+                                               C.byref(batch), _ptr(x), C.byref(kvc), workspace.data_ptr(),
                                                workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "vfm_layer_forward_paged")
 

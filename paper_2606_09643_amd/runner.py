@@ -335,15 +335,11 @@ class ContinuousBatcher:
             parts.append(self._h2d(np.concatenate([s.prompt for s in new]).astype(np.int32)))
         ids_dev = torch.cat(parts) if len(parts) > 1 else parts[0]
         B.vfm_embed_forward(self.cfg, pb.c, B.VFM_EMBED_TOKENS, ids_dev, w.vocab, self.emb, None, x)
-        tp = table.ctypes.data_as(B.C.POINTER(B.C.c_int32))
+        tp = table.ctypes.data_as(B.C.POINTER(B.C.c_int32))     # one device table for every layer
         for li in range(self.m.n_layers):
             kv = B.vfm_kv_pages(self.k[li].data_ptr(), self.v[li].data_ptr(), self.n_pages, self.page_size,
                                 table.shape[1], tp, table_dev.data_ptr())
-            st = B.lib().vfm_layer_forward_paged(B.C.byref(self.cfg), B.C.byref(self.m.c_layers[li]),
-                                                 B.C.byref(self.m.lora[li].c) if self.m.lora[li] else None,
-                                                 B.C.byref(pb.c), x.data_ptr(), B.C.byref(kv),
-                                                 self.ws.data_ptr(), self.ws.numel(), B._stream(None))
-            B._check(st, "vfm_layer_forward_paged")
+            B.vfm_layer_forward_paged(self.cfg, self.m.c_layers[li], self.m.lora_c(li), pb.c, x, kv, self.ws)
         out = torch.empty(max(pb.total_outputs, 1), dtype=torch.float32, device=self.device)
         fn = self.m.final
         B.vfm_head_forward(self.cfg, fn["w"], fn.get("b"), self.m.head_tab.c, pb.c, x, out, self.ws)
