@@ -65,6 +65,17 @@ int vfm_bfq_enqueue(void* state, int32_t task, int64_t request, double arrival, 
 int vfm_bfq_next_batch(void* state, double now, int64_t* requests, int32_t* tasks, int32_t capacity,
                        int32_t* n);
 
+/* Token-based FMs (Section 4.2: token-level work charged in service-time
+ * units): adds `service` (>= 0, the unit of T) of realised work to task
+ * `task`, e.g. the decode tokens its running sequences produced in one
+ * iteration times the per-token time.  The task's last dispatched request's
+ * finish tag moves by service / w_task (a task with nothing dispatched yet
+ * starts from 0), its queued requests' tags follow (each S = max(F of the
+ * previous one, v at its arrival), F = S + its own service / w), and v is
+ * recomputed.  VFM_ERR_TASK for a task out of range, VFM_ERR_SHAPE for a
+ * negative or non-finite service. */
+int vfm_bfq_charge(void* state, int32_t task, double service);
+
 /* Requests of task `task` waiting in the state. */
 int vfm_bfq_queued(const void* state, int32_t task, int32_t* n);
 

@@ -22,6 +22,9 @@ What it computes, step by step in the paper's order:
   l(b) = T(b) / b (Eq. 3): the dispatched requests (their realised service)
   and then the task's queued ones, each chained as in Eq. 1 from its own
   arrival-time v.
+* Token-based FMs are charged their token-level work in service-time units
+  as it is realised (``charge``): it extends the task's last dispatched
+  request, and the task's queued requests follow.
 
 Readings where the paper is silent (each also a parameter of the C ABI):
 T(b), the service time of a batch of b requests, is a caller-supplied table;
@@ -105,6 +108,23 @@ class BFQ:
             self.f_last[t] = prev
             self.queues[t] = rest
         return [(r.req, r.task) for r in batch]
+
+
+    def charge(self, task, service):
+        """Token-based FMs (Section 4.2: token-level work charged in
+        service-time units): `service` of realised work is added to the
+        task's last dispatched request, whose finish tag moves by
+        service / w; the task's queued requests keep their service lengths
+        and are chained after it as in Eq. 1."""
+        prev = (self.f_disp[task] if self.dispatched[task] else 0.0) + service / self.w[task]
+        self.f_disp[task] = prev
+        self.dispatched[task] = True
+        for r in self.queues[task]:
+            length = r.F - r.S
+            r.S = max(prev, r.va)
+            r.F = r.S + length
+            prev = r.F
+        self.f_last[task] = prev
 
 
 def stfq_order(counts, weights, l=1.0):

@@ -39,7 +39,7 @@ EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size
            "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach",
            "vfm_embed_series", "vfm_encoder_attach", "vfm_layer_forward_paged", "vfm_greedy_tokens",
            "vfm_pages_state_size", "vfm_pages_init", "vfm_pages_reserve", "vfm_pages_release",
-           "vfm_pages_table", "vfm_pages_count")
+           "vfm_pages_table", "vfm_pages_count", "vfm_bfq_charge")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -144,6 +144,7 @@ def _lib_handle():
         lib.vfm_bfq_enqueue.argtypes = [C.c_void_p, C.c_int32, C.c_int64, C.c_double, C.c_double]
         lib.vfm_bfq_next_batch.argtypes = [C.c_void_p, C.c_double, C.c_void_p, C.c_void_p, C.c_int32,
                                            C.POINTER(C.c_int32)]
+        lib.vfm_bfq_charge.argtypes = [C.c_void_p, C.c_int32, C.c_double]
         lib.vfm_bfq_queued.argtypes = [C.c_void_p, C.c_int32, C.POINTER(C.c_int32)]
         lib.vfm_bfq_tags.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_double),
                                      C.POINTER(C.c_double)]
@@ -509,6 +510,10 @@ class BFQ:
                                                 self._task.ctypes.data, self.b_max, C.byref(n)),
                "vfm_bfq_next_batch")
         return [(int(self._req[k]), int(self._task[k])) for k in range(n.value)]
+
+    def charge(self, task, service):
+        _check(_lib_handle().vfm_bfq_charge(self.state.ctypes.data, int(task), float(service)),
+               "vfm_bfq_charge")
 
     def queued(self, task):
         n = C.c_int32()

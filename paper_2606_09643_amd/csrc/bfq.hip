@@ -1,8 +1,9 @@
 // Batch-aware fair queueing (BFQ) on the host: forms the mixed-task batches
 // that the backbone kernels run (paper Section 4.2, "Batch-aware Fair
 // Scheduling": start / finish tags of Eq. 1-2 derived from start-time fair
-// queueing, batch growth bounded by b_max and the requests' deadlines, and
-// the re-tagging of Eq. 3 with the batch-dependent per-request service time).
+// queueing, batch growth bounded by b_max and the requests' deadlines, the
+// re-tagging of Eq. 3 with the batch-dependent per-request service time, and
+// for token-based FMs the token-level work charged in service-time units).
 //
 // State layout in the caller's buffer (all 8-byte fields):
 //   Header | weight[n] | T[b_max + 1] | f_disp[n] | f_last[n] | head[n] |
@@ -185,6 +186,33 @@ extern "C" int vfm_bfq_next_batch(void* state, double now, int64_t* requests, in
   }
   double vmax = 0.0;
   for (int32_t t = 0; t < nt; ++t)
+    if (v.disp[t]) vmax = std::fmax(vmax, v.f_disp[t]);
+  v.h->v = vmax;
+  return VFM_OK;
+}
+
+extern "C" int vfm_bfq_charge(void* state, int32_t task, double service) {
+  if (!live(state)) return VFM_ERR_ARG;
+  const View v = view(state);
+  if (task < 0 || task >= v.h->n_tasks) return VFM_ERR_TASK;
+  if (!(service >= 0.0) || !std::isfinite(service)) return VFM_ERR_SHAPE;
+  // the realised work extends the task's last dispatched request: its finish
+  // tag moves by service / w, and the queued requests' tags follow, chained
+  // as Eq. 1 from their own arrival-time v with their own service lengths
+  const double w = v.weight[task];
+  double prev = (v.disp[task] ? v.f_disp[task] : 0.0) + service / w;
+  v.f_disp[task] = prev;
+  v.disp[task] = 1;
+  for (int64_t j = 0; j < v.count[task]; ++j) {
+    Entry& e = v.at(task, j);
+    const double len = e.F - e.S;
+    e.S = std::fmax(prev, e.va);
+    e.F = e.S + len;
+    prev = e.F;
+  }
+  v.f_last[task] = prev;
+  double vmax = 0.0;
+  for (int32_t t = 0; t < v.h->n_tasks; ++t)
     if (v.disp[t]) vmax = std::fmax(vmax, v.f_disp[t]);
   v.h->v = vmax;
   return VFM_OK;

@@ -220,7 +220,10 @@ class ContinuousBatcher:
     back the moment a sequence finishes.
 
     Admission is FIFO, or BFQ order when a B.BFQ scheduler is given (its
-    batches are taken whole, only when b_max more sequences fit).  A prompt
+    batches are taken whole, only when b_max more sequences fit); with BFQ,
+    every step also charges each task its decode rows times `token_time`
+    (token-level work in service-time units), so tasks whose sequences keep
+    generating fall back in the order of the prompts still waiting.  A prompt
     is admitted only when a sequence slot is free, its tokens fit the step's
     token budget, and the pages it will ever need fit next to those the
     running sequences may still need, so a running sequence never waits for
@@ -228,7 +231,7 @@ class ContinuousBatcher:
     of the step is computed by the library's kernels."""
 
     def __init__(self, model: Model, emb, page_size=64, n_pages=1024, max_seqs=256, max_step_tokens=8192,
-                 max_pages=None, bfq=None, record=False, device="cuda"):
+                 max_pages=None, bfq=None, token_time=1.0, record=False, device="cuda"):
         w = model.w
         self.m, self.emb, self.device = model, emb, device
         self.page_size, self.n_pages = int(page_size), int(n_pages)
@@ -240,7 +243,7 @@ class ContinuousBatcher:
         self.v = [torch.zeros(shape, dtype=w.torch_dtype, device=device) for _ in range(model.n_layers)]
         self.cfg = B.vfm_cfg.from_buffer_copy(model.cfg)
         self.cfg.attn = B.VFM_ATTN_MIXED
-        self.bfq, self.record = bfq, record
+        self.bfq, self.record, self.token_time = bfq, record, float(token_time)
         self.waiting, self.running, self.done = [], [], {}
         self.requests = {}
         self.free_slots = list(range(self.max_seqs - 1, -1, -1))
@@ -352,6 +355,10 @@ class ContinuousBatcher:
             off = pb.out_off()
             o = out.cpu().numpy()
             self.trace.append([(s.rid, o[off[i]:off[i + 1]].copy()) for i, s in enumerate(batch)])
+        if self.bfq is not None and n_dec:
+            per_task = np.bincount(task[:n_dec], minlength=w.n_tasks)
+            for t in np.nonzero(per_task)[0]:
+                self.bfq.charge(int(t), float(per_task[t]) * self.token_time)
         finished = []
         for i, s in enumerate(batch):
             s.cached += int(lens[i])

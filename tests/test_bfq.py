@@ -271,3 +271,88 @@ def test_library_decision_time():
     dt = spent / reps
     print(f"BFQ: {dt * 1e6:.1f} us per batch decision ({n_tasks} tasks, b_max {b_max}, 512 queued)")
     assert dt < 1e-3
+
+
+def test_oracle_token_charge_worked_example():
+    """Token-level work charged in service-time units (Section 4.2,
+    token-based FMs), by hand.  Weights (1, 2), T(1) = 1, b_max 1.  r0 of
+    task 0 and r1 of task 1 arrive at v = 0: r0 S 0 F 1, r1 S 0 F 0.5.  The
+    first batch takes r0 (tie -> lower task) and re-tags it with l(1) = 1:
+    F 1; v = 1.  Task 0 then produces decode tokens worth 3 time units:
+    charge(0, 3) moves its finish tag to 1 + 3/1 = 4, v = 4.  A new request
+    of task 0 (arriving now) gets S = max(4, 4) = 4, F = 5.  A charge of 1
+    unit to task 1 (nothing dispatched yet) moves its queued r1 to
+    S = max(0 + 1/2, v at its arrival = 0) = 0.5, F = 1, so r1 goes first,
+    then task 0's new request."""
+    q = BO.BFQ([1.0, 2.0], [0.0, 1.0], 1)
+    q.enqueue(0, 0, 0.0, INF)
+    q.enqueue(1, 1, 0.0, INF)
+    assert q.next_batch(0.0) == [(0, 0)]
+    assert math.isclose(q.v(), 1.0)
+    q.charge(0, 3.0)
+    assert math.isclose(q.f_disp[0], 4.0) and math.isclose(q.v(), 4.0)
+    q.enqueue(0, 2, 1.0, INF)
+    r2 = q.queues[0][0]
+    assert (r2.S, r2.F) == (4.0, 5.0)
+    q.charge(1, 1.0)
+    r1 = q.queues[1][0]
+    assert (r1.S, r1.F) == (0.5, 1.0)
+    assert q.next_batch(1.0) == [(1, 1)]
+    assert q.next_batch(2.0) == [(2, 0)]
+
+
+def test_oracle_charging_every_token_keeps_weighted_shares():
+    """Two always-backlogged token-based tasks (weights 1 and 3), b_max 1,
+    every dispatched request then charged a variable decode length: the
+    service each task receives (its requests' lengths) follows the weights
+    to within one request's length."""
+    rng = np.random.default_rng(7)
+    q = BO.BFQ([1.0, 3.0], [0.0, 1.0], 1)
+    lens = {}
+    k = 0
+    for _ in range(50):
+        for t in (0, 1):
+            q.enqueue(t, k, 0.0, INF)
+            lens[k] = float(rng.integers(1, 20))
+            k += 1
+    got = [0.0, 0.0]
+    for _ in range(60):
+        (req, t), = q.next_batch(0.0)
+        q.charge(t, lens[req] - 1.0)           # T(1) = 1 already counted at dispatch
+        got[t] += lens[req]
+    assert abs(got[1] / 3.0 - got[0]) <= 20.0
+
+
+def test_library_charge_matches_oracle():
+    """The library's charge gives bit-identical tags and batches to the
+    oracle's on a random mix of arrivals, batches and charges."""
+    rng = np.random.default_rng(11)
+    w = [1.0, 2.0, 0.5, 3.0]
+    T = [0.0] + [1.0 + 0.2 * b for b in range(1, 9)]
+    lib, ref = B.BFQ(w, T, 8), BO.BFQ(w, T, 8)
+    k = 0
+    for step in range(400):
+        now = float(step)
+        for _ in range(int(rng.integers(0, 4))):
+            t = int(rng.integers(0, 4))
+            lib.enqueue(t, k, now, INF)
+            ref.enqueue(t, k, now, INF)
+            k += 1
+        if rng.random() < 0.5:
+            assert lib.next_batch(now) == ref.next_batch(now)
+        t = int(rng.integers(0, 4))
+        s = float(rng.uniform(0.0, 5.0))
+        lib.charge(t, s)
+        ref.charge(t, s)
+        for tt in range(4):
+            for j in range(ref.queued(tt)):
+                r = ref.queues[tt][j]
+                assert lib.tags(tt, j) == (r.S, r.F)
+    lib_state = lib.state.copy()
+    with pytest.raises(B.VfmError):
+        lib.charge(4, 1.0)
+    with pytest.raises(B.VfmError):
+        lib.charge(0, -1.0)
+    with pytest.raises(B.VfmError):
+        lib.charge(0, float("nan"))
+    assert np.array_equal(lib.state, lib_state)
