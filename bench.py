@@ -231,6 +231,60 @@ def loop_bench(args):
     print(json.dumps(out), flush=True)
 
 
+def task_load_bench(args):
+    """Time to load one task into a running ViT-B-shaped backbone: its LoRA
+    factors for every layer (rank 16 on q/k/v/o) and its head (the table's widest),
+    packed as one pinned host blob and copied in one transfer, then attached to
+    the layers' adapter tables and the head table (vfm_lora_attach per layer,
+    vfm_head_attach), on the forward's stream; timed from the first copy to
+    the attached tables being visible to the next forward (stream
+    synchronised), median of 50 loads."""
+    import torch
+    from paper_2606_09643_amd import binding as B
+    from paper_2606_09643_amd import runner as R
+    from paper_2606_09643_amd import workloads as wl
+    w = wl.WORKLOADS[2]
+    model = R.Model(w)
+    r, t = w.rank, 1
+    n_out = int(model.head_tab.c.max_out)        # the widest head of the table
+    # the task's artifact as one pinned blob: every layer's A, B factors, then the head
+    shapes = []
+    for li in range(w.n_layers):
+        for p in w.lora_targets:
+            d_in, d_out = wl.proj_dims(w, p)
+            shapes += [((li, p, "A"), (r, d_in)), ((li, p, "B"), (d_out, r))]
+    shapes += [(("head", "W"), (n_out, w.d)), (("head", "b"), (n_out,))]
+    sizes = [int(np.prod(sh)) for _, sh in shapes]
+    blob_h = torch.randn(sum(sizes), dtype=torch.bfloat16).pin_memory()
+    blob_d = torch.empty_like(blob_h, device="cuda")
+    dev, off = {}, 0
+    for (key, sh), n in zip(shapes, sizes):       # views of the device blob
+        dev[key] = blob_d[off:off + n].view(*sh)
+        off += n
+    stream = torch.cuda.current_stream()
+    times = []
+    nbytes = blob_h.numel() * 2
+    for it in range(60):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        blob_d.copy_(blob_h, non_blocking=True)
+        for li in range(w.n_layers):
+            A = {p: dev[(li, p, "A")] for p in w.lora_targets}
+            Bf = {p: dev[(li, p, "B")] for p in w.lora_targets}
+            B.vfm_lora_attach(model.lora[li], t, r, w.lora_scale, A, Bf, stream)
+        B.vfm_head_attach(model.head_tab, t, n_out, dev[("head", "W")], dev[("head", "b")], stream=stream)
+        torch.cuda.synchronize()
+        if it >= 10:
+            times.append(time.perf_counter() - t0)
+    ms = float(np.median(times)) * 1e3
+    print(json.dumps({"metric": "task load time (LoRA factors of every layer + head, host to attached)",
+                      "value": ms, "unit": "ms", "higher_is_better": False, "n_gpus": 1,
+                      "config": {"workload": w.name, "layers": w.n_layers, "lora_rank": r,
+                                 "lora_targets": list(w.lora_targets), "head_outputs": n_out,
+                                 "bytes": int(nbytes)},
+                      "loads_timed": len(times)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -238,6 +292,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--task-load", action="store_true",
+                    help="time loading one task's adapters and head into the ViT-B-shaped backbone")
     ap.add_argument("--loop", type=int, default=0,
                     help="run the continuous-batching loop over this many requests instead of one step")
     ap.add_argument("--paged", type=int, default=0,
@@ -252,6 +308,9 @@ def main():
 
     if args.loop:
         loop_bench(args)
+        return
+    if args.task_load:
+        task_load_bench(args)
         return
 
     import torch
