@@ -286,10 +286,12 @@ int vfm_embed_series(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_encod
  *   x: device float32 [T, d], plan order (residual stream).
  *   lora: NULL for the bare backbone.
  *   k_cache, v_cache: device [n_heads, kv_slots, head_dim] (dtype), head-major,
- *     rotated keys; used when cfg->attn is VFM_ATTN_DECODE (required) or
- *     VFM_ATTN_CAUSAL (optional, NULL to skip): each row's K/V is written at
- *     slot kv_start + pos of every head.  Head-major keeps one head's keys
- *     of a request contiguous, which is what decode attention streams.
+ *     rotated keys; used when cfg->attn is VFM_ATTN_DECODE or VFM_ATTN_MIXED
+ *     (required) or VFM_ATTN_CAUSAL (optional, NULL to skip): each row's K/V
+ *     is written at slot kv_start + pos of every head.  Head-major keeps one
+ *     head's keys of a request contiguous, which is what decode attention
+ *     streams.  (VFM_ATTN_MIXED steps are described with
+ *     vfm_layer_forward_paged; the contiguous cache works for them too.)
  *   workspace: device, >= vfm_workspace_size bytes, 256-byte aligned.
  * Per layer: h = Norm1(x); [q|k|v] = h W_qkv^T + b (+ per-task LoRA);
  * RoPE; attention per request; x += attn W_o^T + b_o (+ LoRA_o);

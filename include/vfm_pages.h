@@ -49,8 +49,9 @@ int vfm_pages_reserve(void* state, int32_t seq, int64_t n_tokens);
 int vfm_pages_release(void* state, int32_t seq);
 
 /* Page-table rows for a batch: row r (max_cols entries) of `table` gets the
- * pages of sequence seqs[r] in token order, then -1.  VFM_ERR_SHAPE if a
- * sequence holds more than max_cols pages. */
+ * pages of sequence seqs[r] in token order, then -1.  VFM_ERR_TASK for a
+ * sequence slot out of range, VFM_ERR_SHAPE if a sequence holds more than
+ * max_cols pages (nothing is written then). */
 int vfm_pages_table(const void* state, const int32_t* seqs, int32_t n, int32_t* table, int32_t max_cols);
 
 /* Pages held by `seq` (*held) and free in the pool (*free_pages). */
