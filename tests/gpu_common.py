@@ -38,6 +38,25 @@ def expected_embed(w, batch, inp, pl):
     return np.concatenate([src[cu_o[i]:cu_o[i + 1]] for i in pl["order"]])
 
 
+def as_f32(rows):
+    """fp64 rows rounded to fp32 (the GPU residual stream's type), as fp64:
+    the values both sides start from when a GPU call is fed oracle rows."""
+    return np.asarray(rows, np.float64).astype(np.float32).astype(np.float64)
+
+
+def set_rows(x_dev, rows, r0=0):
+    """Writes oracle-side rows (plan order, from row r0) into the GPU's fp32
+    residual stream, so a GPU call and the oracle take the same input and no
+    oracle input comes from the GPU path."""
+    t = torch.from_numpy(np.ascontiguousarray(rows, np.float32)).to(x_dev.device)
+    x_dev[r0:r0 + t.shape[0]].copy_(t)
+
+
+def seeded_rows(n, d, seed):
+    """Standard normal rows from a seeded host generator, rounded to fp32."""
+    return as_f32(np.random.default_rng(seed).standard_normal((n, d)))
+
+
 def oracle_layer_rows(w, W_np, ad, pl, x_plan, reqs, kv=None, li=0):
     """Oracle layer for the chosen plan positions; returns {p: (y, k, v)}.
     kv: the decode KV cache (layer li's cached keys are read from it)."""

@@ -2,9 +2,10 @@
 FM (two layers, d 256, per-task LoRA on every projection and a per-task LM
 head over a 256-token vocabulary) serves requests of ragged prompt lengths
 and output budgets that join and leave the running batch at different
-steps.  Every step's head outputs of every request are checked against the
-oracle's causal forward over the same tokens, and every greedy pick against
-the step's own outputs."""
+steps.  The oracle decodes every request greedily on its own (fp64, from the
+prompt); each step's head outputs of each request are checked against the
+oracle's for as long as the two runs have picked the same tokens, and a
+different pick must be a near-tie of the oracle's outputs."""
 import numpy as np
 import pytest
 import torch
@@ -30,19 +31,27 @@ REQUESTS = [  # (task, prompt length, new tokens)
     (0, 5, 6), (2, 17, 3), (1, 1, 8), (0, 33, 4), (2, 9, 5), (1, 24, 7)]
 
 
-def _oracle_logits(w, model, emb_np, task, tokens, n_prompt):
-    """Head outputs at positions n_prompt - 1 .. len(tokens) - 1 of the
-    oracle's causal forward over `tokens` (the request's task adapters and
-    head)."""
+def _oracle_greedy(w, model, emb_np, task, prompt, n_new):
+    """The oracle's own greedy decode of one request: n_new steps, each a
+    causal forward over the prompt and the oracle's earlier picks (the
+    request's task adapters and head), returning the picks and each step's
+    head outputs at the last position."""
     spec = spec_of(w)
-    x = emb_np[np.asarray(tokens)]
-    pos = np.arange(len(tokens))
-    for li in range(model.n_layers):
-        x, _, _ = O.layer(spec, oracle_weights(model.layers[li]), oracle_adapter(model.adapters[li], task), x,
-                          pos=pos)
-    xn = O.final(spec, np64(model.final["w"]), np64(model.final.get("b")), x)
+    layers = [oracle_weights(model.layers[li]) for li in range(model.n_layers)]
+    ads = [oracle_adapter(model.adapters[li], task) for li in range(model.n_layers)]
+    fw, fb = np64(model.final["w"]), np64(model.final.get("b"))
     W, b = np64(model.heads.W[task]), np64(model.heads.b[task])
-    return [O.head(xn[j], W, b) for j in range(n_prompt - 1, len(tokens))]
+    tokens, picks, outs = list(prompt), [], []
+    for _ in range(n_new):
+        x = emb_np[np.asarray(tokens)]
+        pos = np.arange(len(tokens))
+        for li in range(model.n_layers):
+            x, _, _ = O.layer(spec, layers[li], ads[li], x, pos=pos)
+        logits = O.head(O.final(spec, fw, fb, x)[-1], W, b)
+        outs.append(logits)
+        picks.append(int(np.argmax(logits)))
+        tokens.append(picks[-1])
+    return picks, outs
 
 
 @pytest.mark.parametrize("dtype,page,sched", [("bf16", 16, "fifo"), ("f32", 32, "fifo"), ("bf16", 16, "bfq")])
@@ -72,21 +81,27 @@ def test_continuous_batching_loop(dtype, page, sched):
         for rid, o in step:
             outs[rid].append(o)
     emb_np = np64(emb)
-    worst = 0.0
+    worst, compared = 0.0, 0
     for rid, (task, L, n_new) in enumerate(REQUESTS):
         gen = done[rid]
         assert len(gen) == n_new and len(outs[rid]) == n_new
-        tokens = np.concatenate([prompts[rid], np.asarray(gen[:-1], np.int32)])
-        ref = _oracle_logits(w, model, emb_np, task, tokens, L)
+        ref_picks, ref = _oracle_greedy(w, model, emb_np, task, prompts[rid], n_new)
+        # step j of both runs has the same input tokens while the picks agree
         for j in range(n_new):
             got = outs[rid][j]
             worst = max(worst, O.row_rel_error(got[None], ref[j][None]))
-            # the greedy pick is the first maximum of the step's own outputs
+            compared += 1
+            # the greedy kernel's pick is the first maximum of the step's outputs
             assert gen[j] == int(np.argmax(got))
-            # and a maximum of the oracle's outputs up to the tolerance
-            assert ref[j][gen[j]] >= ref[j].max() - tol(w) * np.abs(ref[j]).max()
-    log(f"  max rel err {worst:.3e}")
+            if gen[j] != ref_picks[j]:
+                # a different pick is only allowed at a near-tie of the oracle's outputs;
+                # past it the two runs decode different tokens
+                assert ref[j][gen[j]] >= ref[j].max() - tol(w) * np.abs(ref[j]).max()
+                break
+    log(f"  {compared} of {sum(n for _, _, n in REQUESTS)} steps compared, max rel err {worst:.3e}")
     assert worst < tol(w)
+    if w.dtype == "f32":
+        assert compared == sum(n for _, _, n in REQUESTS)
     # the same requests through the asynchronous path (no per-step read-back)
     # pick the same tokens
     bfq2 = B.BFQ([1.0, 2.0, 1.0], np.linspace(1.0, 2.0, 3), b_max=2) if sched == "bfq" else None

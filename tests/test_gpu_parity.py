@@ -14,7 +14,8 @@ from oracle import vfm_oracle as O
 from paper_2606_09643_amd import binding as B
 from paper_2606_09643_amd import runner as R
 from paper_2606_09643_amd import workloads as wl
-from tests.gpu_common import (expected_embed, log, oracle_heads, oracle_layer_rows, oracle_plan,
+from tests.gpu_common import (as_f32, expected_embed, log, oracle_heads, oracle_layer_rows, oracle_plan,
+                               seeded_rows, set_rows,
                               pick_requests, tol)
 from tests.helpers import np64, oracle_adapter, oracle_weights, spec_of
 
@@ -77,8 +78,8 @@ def test_layer_parity(idx, b_std):
         ranks[ranks == 0] = 0
     w, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, b_std=b_std, ranks=ranks)
     log(f"layer workload {idx} b_std={b_std} T={pb.T}")
-    fwd.embed()
-    x_in = fwd.x.double().cpu().numpy()
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
     fwd.layer(0)
     torch.cuda.synchronize()
     got = fwd.x.double().cpu().numpy()
@@ -107,13 +108,11 @@ def test_layer_parity(idx, b_std):
 def test_head_parity(idx):
     w, batch, model, inp, kv, pb, fwd, pl = _setup(idx)
     log(f"head workload {idx}")
-    fwd.embed()
-    torch.cuda.synchronize()
-    fwd.x.normal_()
+    x_plan = seeded_rows(pb.T, w.d, 100 + idx)
+    set_rows(fwd.x, x_plan)
     fwd.head()
     torch.cuda.synchronize()
     got = fwd.out.cpu().numpy()
-    x_plan = fwd.x.double().cpu().numpy()
     ref = oracle_heads(w, model, pl, x_plan, model.heads.n_out)
     off = pl["logit_off"]
     worst = max(O.row_rel_error(got[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
@@ -124,12 +123,11 @@ def test_head_parity(idx):
 def test_final_hidden_unpermuted():
     """Decoder prefill returns the final-normed rows in original order."""
     w, batch, model, inp, kv, pb, fwd, pl = _setup(4)
-    fwd.embed()
-    torch.cuda.synchronize()
+    x_plan = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_plan)
     fwd.head()
     torch.cuda.synchronize()
     got = fwd.out.double().cpu().numpy()
-    x_plan = fwd.x.double().cpu().numpy()
     cu, cu_o = pl["cu_seqlens"], pl["cu_orig"]
     fw = np64(model.final["w"])
     for p, i in enumerate(pl["order"]):
@@ -284,8 +282,8 @@ def test_end_to_end_small(idx):
 def test_bench_workload_full_size_sampled():
     """The benchmarked workload (ViT-B-shaped, 64 requests x 197 tokens,
     16 tasks, 12 layers) in the bench's launch configuration: every layer's
-    output on sampled requests against the oracle run on that layer's GPU
-    input, and every request's head outputs."""
+    output on sampled requests against the oracle, both sides starting each
+    layer from the oracle's rows, and those requests' head outputs."""
     w = wl.WORKLOADS[2]
     batch = wl.draw_batch(w)
     model = R.Model(w)
@@ -295,26 +293,29 @@ def test_bench_workload_full_size_sampled():
     pl = oracle_plan(w, batch, model.heads.n_out)
     reqs = pick_requests(pl)
     log(f"full-size bench workload, sampled plan positions {reqs}")
-    fwd.embed()
-    torch.cuda.synchronize()
+    x_or = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_or)
     cu = pl["cu_seqlens"]
     worst = 0.0
     for li in range(w.n_layers):
-        x_in = fwd.x.double().cpu().numpy()
+        res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_or, reqs)
         fwd.layer(li)
         torch.cuda.synchronize()
         got = fwd.x.double().cpu().numpy()
-        res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_in, reqs)
         for p in reqs:
             worst = max(worst, O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]))
+            # both sides take the oracle's rows into the next layer
+            x_or[cu[p]:cu[p + 1]] = as_f32(res[p][0])
+            set_rows(fwd.x, x_or[cu[p]:cu[p + 1]], int(cu[p]))
     log(f"  per-layer max row rel err {worst:.3e}")
     assert worst < tol(w)
     fwd.head()
     torch.cuda.synchronize()
     out = fwd.out.cpu().numpy()
-    ref = oracle_heads(w, model, pl, fwd.x.double().cpu().numpy(), model.heads.n_out)
+    ref = oracle_heads(w, model, pl, x_or, model.heads.n_out)
     off = pl["logit_off"]
-    hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
+    hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None])
+             for i in (int(pl["order"][p]) for p in reqs))
     log(f"  head max rel err {hw:.3e}")
     assert hw < tol(w)
 
@@ -325,8 +326,8 @@ def test_layer_parity_long_prompts():
     case = dict(task_id=[3, 0, 63], seq_len=[300, 1, 513])
     w, batch, model, inp, kv, pb, fwd, pl = _setup(4, n_layers=1, b_std=0.1, case=case)
     log(f"layer workload 4 long prompts T={pb.T}")
-    fwd.embed()
-    x_in = fwd.x.double().cpu().numpy()
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
     fwd.layer(0)
     torch.cuda.synchronize()
     got = fwd.x.double().cpu().numpy()
@@ -354,8 +355,8 @@ def test_large_gemm_many_task_runs():
     w, batch, model, inp, kv, pb, fwd, pl = _setup(4, n_layers=1, b_std=0.1, ranks=ranks, case=case)
     assert pb.T >= 1024, pb.T                      # the large-tile GEMM path
     log(f"layer workload 4, {n} short requests over {len(present)} tasks, T={pb.T}")
-    fwd.embed()
-    x_in = fwd.x.double().cpu().numpy()
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
     fwd.layer(0)
     torch.cuda.synchronize()
     got = fwd.x.double().cpu().numpy()
@@ -371,8 +372,8 @@ def test_large_gemm_many_task_runs():
 def test_full_size_sampled(idx):
     """Each remaining workload at its full batch, in the bench's launch
     configuration: every layer's output on sampled requests against the
-    oracle run on that layer's GPU input, and, when every layer runs, every
-    request's head outputs.  The decoder workloads run their first two layers
+    oracle, both sides starting each layer from the oracle's rows, and, when
+    every layer runs, those requests' head outputs.  The decoder workloads run their first two layers
     (the kernels and launch shapes of all 32 are the same); decode also
     checks the new K / V rows written to the cache."""
     w = wl.WORKLOADS[idx]
@@ -386,19 +387,21 @@ def test_full_size_sampled(idx):
     pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
     reqs = pick_requests(pl, k=4 if idx == 4 else 6)
     log(f"full-size workload {idx}: T={pb.T}, {n_layers} layers, sampled plan positions {reqs}")
-    fwd.embed()
-    torch.cuda.synchronize()
+    x_or = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_or)
     cu = pl["cu_seqlens"]
     worst = 0.0
     for li in range(n_layers):
-        x_in = fwd.x.double().cpu().numpy()
+        res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_or, reqs,
+                                kv=kv, li=li)
         fwd.layer(li)
         torch.cuda.synchronize()
         got = fwd.x.double().cpu().numpy()
-        res = oracle_layer_rows(w, oracle_weights(model.layers[li]), model.adapters[li], pl, x_in, reqs,
-                                kv=kv, li=li)
         for p in reqs:
             worst = max(worst, O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]))
+            # both sides take the oracle's rows into the next layer
+            x_or[cu[p]:cu[p + 1]] = as_f32(res[p][0])
+            set_rows(fwd.x, x_or[cu[p]:cu[p + 1]], int(cu[p]))
             if kv is not None:
                 i = int(pl["order"][p])
                 slot = int(kv.kv_start[i] + batch.ctx[i])
@@ -411,9 +414,10 @@ def test_full_size_sampled(idx):
         fwd.head()
         torch.cuda.synchronize()
         out = fwd.out.cpu().numpy()
-        ref = oracle_heads(w, model, pl, fwd.x.double().cpu().numpy(), model.heads.n_out)
+        ref = oracle_heads(w, model, pl, x_or, model.heads.n_out)
         off = pl["logit_off"]
-        hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None]) for i in range(batch.n_req))
+        hw = max(O.row_rel_error(out[off[i]:off[i + 1]][None], ref[i][None])
+                 for i in (int(pl["order"][p]) for p in reqs))
         log(f"  head max rel err {hw:.3e}")
         assert hw < tol(w)
 
@@ -445,12 +449,12 @@ def test_prefill_writes_kv_cache(rope):
     kc = torch.full((w.n_heads, slots, w.head_dim), sentinel, dtype=torch.bfloat16, device="cuda")
     vc = torch.full_like(kc, sentinel)
     log(f"prefill layer with KV cache, rope={rope}, T={pb.T}, slots={slots}")
-    fwd.embed()
-    x_in = fwd.x.double().cpu().numpy()
+    pl = oracle_plan(w, batch)
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
     B.vfm_layer_forward(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, kc, vc, slots, fwd.ws)
     torch.cuda.synchronize()
     got = fwd.x.double().cpu().numpy()
-    pl = oracle_plan(w, batch)
     spec = spec_of(w)
     if not rope:
         spec["rope_theta"] = 0.0
@@ -481,9 +485,9 @@ def test_attach_and_remove_adapter_between_batches():
     adapter (or the bare backbone), and every other task's rows stay
     bit-identical to the first run.  ViT-B layer, tasks 5, 0, 5, 2, 9, 0."""
     w, batch, model, inp, kv, pb, fwd, pl = _setup(2, n_layers=1, b_std=0.1)
-    fwd.embed()
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
     x0 = fwd.x.clone()
-    x_in = x0.double().cpu().numpy()
     spec = spec_of(w)
     W_np = oracle_weights(model.layers[0])
     cu = pl["cu_seqlens"]
@@ -534,8 +538,11 @@ def test_attach_head_between_batches():
     batch (planned with the new width) gives the oracle's logits for task 2
     and the unchanged ones for the other tasks."""
     w, batch, model, inp, kv, pb, fwd, pl = _setup(2, n_layers=1)
-    out_a = fwd().cpu().numpy()
-    x_fin = fwd.x.double().cpu().numpy()
+    x_fin = seeded_rows(pb.T, w.d, 202)            # the final hidden rows, plan order
+    set_rows(fwd.x, x_fin)
+    fwd.head()
+    torch.cuda.synchronize()
+    out_a = fwd.out.cpu().numpy()
     n_out = model.heads.n_out.copy()
     g = torch.Generator(device="cuda").manual_seed(5)
     Wn = (torch.randn(17, w.d, generator=g, device="cuda") / w.d ** 0.5).to(torch.bfloat16)
@@ -589,8 +596,11 @@ def test_mlp_decoder_heads(idx, act):
         bs.append(hd.b[t])
     tab = B.HeadTable(hd.n_out, Ws, bs, model.head_tab.c.pool, W1s=W1s, b1s=b1s, hidden=H, act=act)
     model.head_tab = tab
-    out = fwd().cpu().numpy()
-    x_fin = fwd.x.double().cpu().numpy()
+    x_fin = seeded_rows(pb.T, w.d, 300 + idx)      # the final hidden rows, plan order
+    set_rows(fwd.x, x_fin)
+    fwd.head()
+    torch.cuda.synchronize()
+    out = fwd.out.cpu().numpy()
     spec = spec_of(w)
     fw = np64(model.final["w"])
     fb = np64(model.final["b"]) if model.final.get("b") is not None else None
@@ -755,12 +765,12 @@ def test_mixed_prefill_and_decode_step_paged(ctx_long):
     fwd = R.Forward(model, pb, inp)
     ws = torch.empty(B.vfm_workspace_size(cfg, pb.c, model.lora_c(0)), dtype=torch.uint8, device="cuda")
     log(f"mixed step: lens {list(seq_len)} ctx {list(ctx)} T={pb.T}")
-    fwd.embed()
-    x_in = fwd.x.double().cpu().numpy()
+    pl = O.plan(task_id, seq_len, w.n_tasks, ctx=ctx)
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
     B.vfm_layer_forward_paged(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, pkv, ws)
     torch.cuda.synchronize()
     got = fwd.x.double().cpu().numpy()
-    pl = O.plan(task_id, seq_len, w.n_tasks, ctx=ctx)
     spec = spec_of(w)
     W_np = oracle_weights(model.layers[0])
     cu = pl["cu_seqlens"]
