@@ -731,44 +731,60 @@ def _page_rows(pool, table, i, n, page):
     return rows.permute(1, 0, 2).reshape(n, -1)
 
 
-@pytest.mark.parametrize("ctx_long", [300, 2100])
-def test_mixed_prefill_and_decode_step_paged(ctx_long):
-    """One continuous-batching step over a paged cache (7B decoder layer
-    dims, pages of 64 in random order): two prompts (70 and 33 tokens, ctx 0)
-    and three decode tokens (ctx 63, 1100 and a long one) in one batch.  Every
-    row against the oracle (prompts causal over themselves, decode rows over
-    their cached keys plus themselves), and every new row's rotated K and V
-    in its page."""
+@pytest.mark.parametrize("ctx_long,layout", [(300, "paged"), (2100, "paged"), (2100, "contiguous"),
+                                             (0, "causal-paged")])
+def test_mixed_step_over_cache(ctx_long, layout):
+    """One continuous-batching step (7B decoder layer dims): two prompts (70
+    and 33 tokens, ctx 0) and three decode tokens (ctx 63, 1100 and a long
+    one) in one batch, over a paged cache (pages of 64 in random order) or
+    the contiguous one (vfm_layer_forward, slots kv_start + k); and a
+    prompts-only causal step over pages.  Every row against the oracle
+    (prompts causal over themselves, decode rows over their cached keys plus
+    themselves), and every new row's rotated K and V in its slots."""
     w = wl.WORKLOADS[4]
     task_id = np.array([3, 0, 3, 63, 5], np.int32)
-    seq_len = np.array([70, 1, 33, 1, 1], np.int32)
-    ctx = np.array([0, 63, 0, ctx_long, 1100], np.int32)
+    if layout == "causal-paged":
+        seq_len = np.array([70, 1, 33, 5, 2], np.int32)
+        ctx = np.zeros(5, np.int32)
+    else:
+        seq_len = np.array([70, 1, 33, 1, 1], np.int32)
+        ctx = np.array([0, 63, 0, ctx_long, 1100], np.int32)
     batch = wl.Batch(task_id, seq_len, ctx)
     model = R.Model(w, n_layers=1, b_std=0.1)
     inp = R.Inputs(w, batch)
-    page = 64
     n_tok = ctx.astype(np.int64) + seq_len
-    need = (n_tok + page - 1) // page
-    total = int(need.sum()) + 5
-    perm = np.random.default_rng(11).permutation(total).astype(np.int32)
-    table = np.zeros((len(n_tok), int(need.max())), np.int32)
-    first = np.concatenate([[0], np.cumsum(need)[:-1]])
-    for i in range(len(n_tok)):
-        table[i, :need[i]] = perm[first[i]:first[i] + need[i]]
+    if layout == "contiguous":
+        # slots kv_start[i] + k: a "page table" of single slots for the oracle's reads
+        page = 1
+        kvs = np.concatenate([[0], np.cumsum(n_tok + 3)[:-1]]).astype(np.int32)
+        total = int((n_tok + 3).sum())
+        table = kvs[:, None] + np.arange(int(n_tok.max()), dtype=np.int32)[None, :]
+    else:
+        page = 64
+        need = (n_tok + page - 1) // page
+        total = int(need.sum()) + 5
+        perm = np.random.default_rng(11).permutation(total).astype(np.int32)
+        table = np.zeros((len(n_tok), int(need.max())), np.int32)
+        first = np.concatenate([[0], np.cumsum(need)[:-1]])
+        for i in range(len(n_tok)):
+            table[i, :need[i]] = perm[first[i]:first[i] + need[i]]
     g = torch.Generator(device="cuda").manual_seed(13)
     kp = torch.randn(w.n_heads, total * page, w.head_dim, generator=g, device="cuda").to(torch.bfloat16)
     vp = torch.randn(w.n_heads, total * page, w.head_dim, generator=g, device="cuda").to(torch.bfloat16)
-    pkv = B.PagedKV(kp, vp, page, table)
     cfg = R.cfg_for(w)
-    cfg.attn = B.VFM_ATTN_MIXED
-    pb = B.Batch(task_id, seq_len, w.n_tasks, ctx_len=ctx)
+    cfg.attn = B.VFM_ATTN_CAUSAL if layout == "causal-paged" else B.VFM_ATTN_MIXED
+    pb = B.Batch(task_id, seq_len, w.n_tasks, ctx_len=ctx, kv_start=kvs if layout == "contiguous" else None)
     fwd = R.Forward(model, pb, inp)
     ws = torch.empty(B.vfm_workspace_size(cfg, pb.c, model.lora_c(0)), dtype=torch.uint8, device="cuda")
-    log(f"mixed step: lens {list(seq_len)} ctx {list(ctx)} T={pb.T}")
+    log(f"{layout} step: lens {list(seq_len)} ctx {list(ctx)} T={pb.T}")
     pl = O.plan(task_id, seq_len, w.n_tasks, ctx=ctx)
     x_in = as_f32(expected_embed(w, batch, inp, pl))
     set_rows(fwd.x, x_in)
-    B.vfm_layer_forward_paged(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, pkv, ws)
+    if layout == "contiguous":
+        B.vfm_layer_forward(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, kp, vp, total, ws)
+    else:
+        B.vfm_layer_forward_paged(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x,
+                                  B.PagedKV(kp, vp, page, table), ws)
     torch.cuda.synchronize()
     got = fwd.x.double().cpu().numpy()
     spec = spec_of(w)
