@@ -185,10 +185,11 @@ def loop_bench(args):
     """Continuous batching of the 7B decoder workload's model (all layers,
     128 tasks with rank-16 LoRA on every projection, per-task heads): n
     requests with prompts of U[64, 512] tokens and U[32, 128] new tokens each,
-    at most 256 running sequences, pages of 64 slots, prompts admitted FIFO up
-    to 8192 tokens per step.  Timed from the first step to the last request
+    at most 256 running sequences, pages of 64 slots, prompts admitted FIFO
+    (or by BFQ with --admission bfq) up to 8192 tokens per step.  Timed from the first step to the last request
     finishing, host scheduling and the per-step token read-back included."""
     import torch
+    from paper_2606_09643_amd import binding as B
     from paper_2606_09643_amd import runner as R
     from paper_2606_09643_amd import workloads as wl
     w = wl.WORKLOADS[5]
@@ -204,8 +205,13 @@ def loop_bench(args):
     n_pages = max_seqs * ((512 + 128 + page - 1) // page)
 
     def make():
+        bfq = None
+        if args.admission == "bfq":
+            # equal weights; T(b): a prompt step's time grows with its prompts (unit: one decode step)
+            bfq = B.BFQ(np.ones(w.n_tasks), [0.0] + [1.0 + 0.25 * b for b in range(1, 17)], b_max=16)
         cb = R.ContinuousBatcher(model, emb, page_size=page, n_pages=n_pages, max_seqs=max_seqs,
-                                 max_step_tokens=8192, max_pages=(512 + 128 + page - 1) // page)
+                                 max_step_tokens=8192, max_pages=(512 + 128 + page - 1) // page, bfq=bfq,
+                                 token_time=1.0 / max_seqs)
         for i in range(n):
             cb.submit(i, int(tasks[i]), rng.integers(0, w.vocab, size=int(plen[i])), int(new[i]))
         return cb
@@ -226,7 +232,7 @@ def loop_bench(args):
            "dtype": "bf16", "data": "synthetic",
            "config": {"workload": w.name + " continuous batching", "requests": n,
                       "prompt_tokens": int(plen.sum()), "generated_tokens": gen, "max_running": max_seqs,
-                      "page_size": page, "max_step_tokens": 8192, "admission": "fifo"},
+                      "page_size": page, "max_step_tokens": 8192, "admission": args.admission},
            "seconds": sec}
     print(json.dumps(out), flush=True)
 
@@ -296,6 +302,8 @@ def main():
                     help="time loading one task's adapters and head into the ViT-B-shaped backbone")
     ap.add_argument("--loop", type=int, default=0,
                     help="run the continuous-batching loop over this many requests instead of one step")
+    ap.add_argument("--admission", choices=("fifo", "bfq"), default="fifo",
+                    help="--loop: admit prompts FIFO or by BFQ (16-request batches, decode tokens charged)")
     ap.add_argument("--paged", type=int, default=0,
                     help="decode workloads: read the KV cache through pages of this many slots "
                          "(random page order) instead of the contiguous cache")

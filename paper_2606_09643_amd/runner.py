@@ -220,7 +220,8 @@ class ContinuousBatcher:
     back the moment a sequence finishes.
 
     Admission is FIFO, or BFQ order when a B.BFQ scheduler is given (its
-    batches are taken whole, only when b_max more sequences fit); with BFQ,
+    batches are taken whole and their requests join in that order as they
+    fit, before any later batch is formed); with BFQ,
     every step also charges each task its decode rows times `token_time`
     (token-level work in service-time units), so tasks whose sequences keep
     generating fall back in the order of the prompts still waiting.  A prompt
@@ -252,6 +253,7 @@ class ContinuousBatcher:
         self.steps = 0
         self.trace = []                 # per step: [(rid, logits)] when record is set
         self._picks, self._prev_nxt, self._keep = [], None, None
+        self._ready = []                # taken from BFQ, not yet admitted (in its order)
 
     def submit(self, rid, task, prompt, max_new, now=0.0):
         s = _Seq(rid, task, prompt, max_new, self.page_size)
@@ -283,18 +285,21 @@ class ContinuousBatcher:
                 new.append(s)
                 tokens += len(s.prompt)
             return new
-        while self.waiting:
-            worst = max(len(s.prompt) for s in self.waiting)
-            wb = max(s.budget for s in self.waiting)
-            b = self.bfq.b_max
-            if (len(self.free_slots) < b or tokens + b * worst > self.max_step_tokens
-                    or self.committed + b * wb > self.n_pages):
+        # BFQ: batches come whole in tag order; their requests join as
+        # they fit (slot, token budget, pages), the rest first in later steps
+        while True:
+            if not self._ready:
+                got = self.bfq.next_batch(now) if self.waiting else []
+                if not got:
+                    break
+                self._ready = [self.requests[rid] for rid, _ in got]
+            s = self._ready[0]
+            if not self._fits(s, tokens):
                 break
-            for rid, _ in self.bfq.next_batch(now):
-                s = self.requests[rid]
-                self._admit_one(s)
-                new.append(s)
-                tokens += len(s.prompt)
+            self._ready.pop(0)
+            self._admit_one(s)
+            new.append(s)
+            tokens += len(s.prompt)
         return new
 
     def _h2d(self, arr):
