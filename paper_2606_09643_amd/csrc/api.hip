@@ -196,7 +196,7 @@ int check_layer(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_t
   }
   if (cfg->attn == VFM_ATTN_DECODE && pl->max_seqlen != 1) return VFM_ERR_UNSUPPORTED;
   const PlanOffsets po = plan_offsets(pl->n_req, pl->n_tasks, pl->T);
-  if (cfg->attn == VFM_ATTN_MIXED) {        // prompts (ctx 0) or single decode rows
+  if (cfg->attn == VFM_ATTN_MIXED && cfg->dtype != VFM_BF16) {   // prompt chunks after cached tokens: bf16
     const int32_t* ctx = host_arr(batch, po.ctx);
     const int32_t* cu = host_arr(batch, po.cu_seqlens);
     for (int p = 0; p < pl->n_req; ++p)
@@ -402,7 +402,14 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
                                           kv_slots, kp, s));
   // a6: attention per request (and the KV-cache write)
   // (timed per kernel inside the launcher)
-  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, kp, rope_writes_kv,
+  bool chunked = false;                      // a prompt chunk after cached tokens
+  if (c.attn == VFM_ATTN_MIXED) {
+    const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
+    const int32_t* ctx = host_arr(batch, po.ctx);
+    const int32_t* cu = host_arr(batch, po.cu_seqlens);
+    for (int p = 0; p < pl.n_req && !chunked; ++p) chunked = ctx[p] > 0 && cu[p + 1] - cu[p] > 1;
+  }
+  VFM_HIP(launch_attention(c.dtype, pl, c, qkv, attn, k_cache, v_cache, kv_slots, kp, rope_writes_kv, chunked,
                            base + ws.aws, ws.z - ws.aws, max_keys, s));
   // a7: output projection + LoRA_o + residual
   VFM_TRY(project(VFM_PROF_GEMM_O, attn, d, w->w_o, nullptr, w->b_o, d, EPI_RESID, x, d, {VFM_O}, d,

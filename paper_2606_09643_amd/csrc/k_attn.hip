@@ -210,10 +210,13 @@ __device__ __forceinline__ int pair_key(int ks, int x) {  // key of row x of sub
 // fragment is one 16-byte read.  Causal: a wave skips key blocks entirely
 // past its queries and masks only the block on its diagonal.
 // ---------------------------------------------------------------------------
-template <int DH, bool CAUSAL>
+template <int DH, bool CAUSAL, bool FROM_CACHE = false>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                                 int d, bf16* __restrict__ out,
-                                                                float scale_log2) {
+                                                                float scale_log2,
+                                                                const bf16* __restrict__ kc = nullptr,
+                                                                const bf16* __restrict__ vc = nullptr,
+                                                                int64_t kv_slots = 0, KvPages kpg = {}) {
   constexpr int KB = 64;          // keys per block step
   constexpr int CH = DH / 8;      // 16-byte chunks per key row
   constexpr int VP = KB + 8;      // V^T row stride (bf16): 36 dwords, conflict-free 16-byte reads
@@ -225,6 +228,12 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
   const int p = upper_index(pl.qblk_off, pl.n_req + 1, b);
   const int R = pl.cu_seqlens[p];
   const int L = pl.cu_seqlens[p + 1] - R;
+  // FROM_CACHE (a prompt chunk after ctx cached tokens): every key, the
+  // cached ones and the chunk's own, is read from the cache, where the RoPE
+  // pass has already put the chunk's rows; query i sits at position ctx + i
+  const int ctx = FROM_CACHE ? pl.ctx[p] : 0;
+  if (FROM_CACHE && (ctx == 0 || L == 1)) return;   // block-uniform: other kernels' requests
+  const int NK = ctx + L;                          // keys of the request
   const int q0 = (b - pl.qblk_off[p]) * 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4;
@@ -245,19 +254,28 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
 
   // staging registers of one key block
   bf16x8 kr[KPT], vr[8];
+  // where key k's K / V row of this head starts
+  auto krow = [&](int k) -> const bf16* {
+    if (FROM_CACHE) return kc + ((int64_t)h * kv_slots + kv_slot(pl, kpg, p, k)) * DH;
+    return base + (int64_t)k * ld + d;
+  };
+  auto vrow = [&](int k) -> const bf16* {
+    if (FROM_CACHE) return vc + ((int64_t)h * kv_slots + kv_slot(pl, kpg, p, k)) * DH;
+    return base + (int64_t)k * ld + 2 * d;
+  };
   auto load = [&](int kb) {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
       kr[i] = bf16x8{};
-      if (kb + key < L) kr[i] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + key) * ld + d + ch * 8);
+      if (kb + key < NK) kr[i] = *reinterpret_cast<const bf16x8*>(krow(kb + key) + ch * 8);
     }
     if (tid < VTILES) {
       const int k8 = (tid / CH) * 8, d8 = (tid % CH) * 8;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         vr[e] = bf16x8{};
-        if (kb + k8 + e < L) vr[e] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + k8 + e) * ld + 2 * d + d8);
+        if (kb + k8 + e < NK) vr[e] = *reinterpret_cast<const bf16x8*>(vrow(kb + k8 + e) + d8);
       }
     }
   };
@@ -279,14 +297,14 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
     }
   };
 
-  const int kend = CAUSAL ? min(L, q0 + 64) : L;
+  const int kend = CAUSAL ? min(NK, ctx + q0 + 64) : NK;
   const int x = lane & 15;
   const int ke = pair_key(0, x), ko = pair_key(1, x);
   int koff_e = ke * DH, koff_o = ko * DH;
   int voff = x * VP + 8 * g;
   asm volatile("" : "+v"(koff_e), "+v"(koff_o), "+v"(voff));
-  const int wq0 = q0 + wave * 16;                 // the wave's first query
-  int lim = CAUSAL ? min(L, qi + 1) : L;          // keys >= lim are masked for this lane
+  const int wq0 = ctx + q0 + wave * 16;           // the wave's first query position
+  int lim = CAUSAL ? min(NK, ctx + qi + 1) : NK;  // keys >= lim are masked for this lane
 
   load(0);
   store();
@@ -298,7 +316,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
     if (!CAUSAL || kb <= wq0 + 15) {
       f32x4 st[4];
       float mb = NEG_BIG;
-      const bool full = kb + KB <= L && (!CAUSAL || kb + KB <= wq0 + 1);
+      const bool full = kb + KB <= NK && (!CAUSAL || kb + KB <= wq0 + 1);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int row0 = (ks & 1) ? ko : ke;
@@ -621,6 +639,12 @@ __global__ __launch_bounds__(256) void attn_prefill_simt_kernel(Plan pl, const T
 // its chunk's page ids (at most DEC_CHUNK / 16) into LDS.  mixed: prompts
 // (ctx 0) of a continuous-batching step are left to the prefill kernels.
 constexpr int DEC_CHUNK = 1024;
+
+// In a mixed step, the requests the decode kernels own: one new row after
+// cached tokens.
+__device__ __forceinline__ bool decode_row(const Plan& pl, int p) {
+  return pl.ctx[p] > 0 && pl.cu_seqlens[p + 1] - pl.cu_seqlens[p] == 1;
+}
 constexpr int DEC_MAX_PAGES = DEC_CHUNK / 16;   // page ids per chunk (pages of >= 16 slots)
 
 // The chunk [kbeg, kend)'s page ids into spg; returns the first page index.
@@ -650,7 +674,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Plan pl, const T* __re
   const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
   const int tid = threadIdx.x;
   const int grp = tid / LPK, sub = tid % LPK;
-  if (mixed && pl.ctx[p] == 0) return;       // a prompt: block-uniform
+  if (mixed && !decode_row(pl, p)) return;   // a prompt or prompt chunk: block-uniform
   const int R = pl.cu_seqlens[p];            // the request's (single) query row
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int kbeg = c * DEC_CHUNK;
@@ -760,7 +784,7 @@ __global__ __launch_bounds__(256) void attn_decode_bf16_kernel(Plan pl, const bf
   const int h = blockIdx.x, p = blockIdx.y, c = blockIdx.z;
   const int tid = threadIdx.x;
   const int grp = tid / LPK, sub = tid % LPK;
-  if (mixed && pl.ctx[p] == 0) return;       // a prompt: block-uniform
+  if (mixed && !decode_row(pl, p)) return;   // a prompt or prompt chunk: block-uniform
   const int R = pl.cu_seqlens[p];
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int kbeg = c * DEC_CHUNK;
@@ -870,7 +894,7 @@ __global__ __launch_bounds__(DH) void attn_decode_merge_kernel(Plan pl, const fl
   constexpr int MAXC = 64;                   // chunks merged per pass through LDS
   __shared__ float sw[MAXC];
   const int p = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
-  if (mixed && pl.ctx[p] == 0) return;       // a prompt (prefill kernels)
+  if (mixed && !decode_row(pl, p)) return;   // a prompt or prompt chunk (prefill kernels)
   const int R = pl.cu_seqlens[p];
   const int nkeys = pl.ctx[p] + (pl.cu_seqlens[p + 1] - R);
   const int nc = min((nkeys + DEC_CHUNK - 1) / DEC_CHUNK, nchunk);
@@ -931,7 +955,7 @@ size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys) {
 
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv, void* out,
                             void* k_cache, void* v_cache, int64_t kv_slots, const KvPages& kp, bool kv_written,
-                            void* ws, size_t ws_bytes, int max_keys, hipStream_t s) {
+                            bool chunked, void* ws, size_t ws_bytes, int max_keys, hipStream_t s) {
   const int d = c.d_model, H = c.n_heads, DH = c.head_dim;
   const float scale_log2 = LOG2E / sqrtf((float)DH);
   const bool mixed = c.attn == VFM_ATTN_MIXED;
@@ -986,6 +1010,17 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
       else
         hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 128>), grid, dim3(256), 0, s, pl,
                            (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
+    }
+    // prompt chunks after cached tokens: their rows again, over every key
+    // of the request read from the cache (the rows above attended to the
+    // chunk alone)
+    if (mixed && chunked && dtype == VFM_BF16) {
+#define CHUNK(D_)                                                                                     \
+  hipLaunchKernelGGL((attn_prefill_bf16_kernel<D_, true, true>), grid, dim3(256), 0, s, pl,           \
+                     (const bf16*)qkv, d, (bf16*)out, scale_log2, (const bf16*)k_cache,              \
+                     (const bf16*)v_cache, kv_slots, kp)
+      if (DH == 64) CHUNK(64); else CHUNK(128);
+#undef CHUNK
     }
     prof_end(pi, s);
     if (!mixed) return hipGetLastError();

@@ -300,10 +300,13 @@ hipError_t launch_rope(int dtype, const Plan& pl, void* qkv, int d, int n_heads,
 // the largest ctx + length over the batch's requests.  kv_written: the rows'
 // K / V are already in the cache (written by the RoPE pass), so no cache
 // write here.  Mixed steps: prompts (ctx 0) attend causally over their own
-// rows, single-row requests with ctx > 0 over their cached keys.
+// rows, single-row requests with ctx > 0 over their cached keys, and (bf16,
+// `chunked` set) prompt chunks with ctx > 0 over the cached keys and their
+// own rows, all read from the cache.
 hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const void* qkv,
                             void* out, void* k_cache, void* v_cache, int64_t kv_slots, const KvPages& kp,
-                            bool kv_written, void* ws, size_t ws_bytes, int max_keys, hipStream_t s);
+                            bool kv_written, bool chunked, void* ws, size_t ws_bytes, int max_keys,
+                            hipStream_t s);
 size_t attention_workspace(const vfm_cfg& c, const Plan& pl, int max_keys);
 
 // Input rows into the fp32 residual stream (plan order).

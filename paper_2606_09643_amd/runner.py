@@ -232,7 +232,7 @@ class ContinuousBatcher:
     of the step is computed by the library's kernels."""
 
     def __init__(self, model: Model, emb, page_size=64, n_pages=1024, max_seqs=256, max_step_tokens=8192,
-                 max_pages=None, bfq=None, token_time=1.0, record=False, device="cuda"):
+                 max_pages=None, bfq=None, token_time=1.0, chunk_prompts=None, record=False, device="cuda"):
         w = model.w
         self.m, self.emb, self.device = model, emb, device
         self.page_size, self.n_pages = int(page_size), int(n_pages)
@@ -245,6 +245,8 @@ class ContinuousBatcher:
         self.cfg = B.vfm_cfg.from_buffer_copy(model.cfg)
         self.cfg.attn = B.VFM_ATTN_MIXED
         self.bfq, self.record, self.token_time = bfq, record, float(token_time)
+        # prompt chunks after cached tokens run on the bf16 path only
+        self.chunk = (w.dtype == "bf16") if chunk_prompts is None else bool(chunk_prompts)
         self.waiting, self.running, self.done = [], [], {}
         self.requests = {}
         self.free_slots = list(range(self.max_seqs - 1, -1, -1))
@@ -265,7 +267,8 @@ class ContinuousBatcher:
         self.waiting.append(s)
 
     def _fits(self, s, tokens):
-        return (self.free_slots and tokens + len(s.prompt) <= self.max_step_tokens
+        first = 1 if self.chunk else len(s.prompt)   # tokens it needs in this step
+        return (self.free_slots and tokens + first <= self.max_step_tokens
                 and self.committed + s.budget <= self.n_pages)
 
     def _admit_one(self, s):
@@ -275,7 +278,12 @@ class ContinuousBatcher:
         self.running.append(s)
 
     def _admit(self, now):
-        tokens = len(self.running)                   # one decode row per running sequence
+        # rows already claimed this step: a decode row per decoding sequence and
+        # the next chunk of every sequence still in its prompt
+        tokens = 0
+        for s in self.running:
+            tokens += 1 if s.cached >= len(s.prompt) else min(len(s.prompt) - s.cached,
+                                                              max(self.max_step_tokens - tokens, 0))
         new = []
         if self.bfq is None:
             for s in list(self.waiting):
@@ -283,7 +291,7 @@ class ContinuousBatcher:
                     break
                 self._admit_one(s)
                 new.append(s)
-                tokens += len(s.prompt)
+                tokens += min(len(s.prompt), self.max_step_tokens - tokens)
             return new
         # BFQ: batches come whole in tag order; their requests join as
         # they fit (slot, token budget, pages), the rest first in later steps
@@ -299,7 +307,7 @@ class ContinuousBatcher:
             self._ready.pop(0)
             self._admit_one(s)
             new.append(s)
-            tokens += len(s.prompt)
+            tokens += min(len(s.prompt), self.max_step_tokens - tokens)
         return new
 
     def _h2d(self, arr):
@@ -316,12 +324,28 @@ class ContinuousBatcher:
         while the GPU still runs step n.  Token values are read back by
         `tokens()`."""
         new = self._admit(now)
-        batch = [s for s in self.running if s not in new] + new
+        old = [s for s in self.running if s not in new]
+        # decoding sequences first (their input is their last pick, on the
+        # device), then the sequences still in their prompt, each with its
+        # next chunk of the step's token budget (the whole rest of the prompt
+        # when prompts are not chunked)
+        dec = [s for s in old if s.cached >= len(s.prompt)]
+        budget = self.max_step_tokens - len(dec)
+        chunks = []
+        for s in [s for s in old if s.cached < len(s.prompt)] + new:
+            n = len(s.prompt) - s.cached
+            if self.chunk:
+                n = min(n, budget)
+            if n <= 0:
+                continue
+            chunks.append((s, n))
+            budget -= n
+        batch = dec + [s for s, _ in chunks]
         if not batch:
             return []
         w = self.m.w
         task = np.array([s.task for s in batch], np.int32)
-        lens = np.array([1 if s.cached else len(s.prompt) for s in batch], np.int32)
+        lens = np.array([1] * len(dec) + [n for _, n in chunks], np.int32)
         ctx = np.array([s.cached for s in batch], np.int32)
         for s, c, n in zip(batch, ctx, lens):
             self.alloc.reserve(s.slot, int(c) + int(n))
@@ -334,13 +358,14 @@ class ContinuousBatcher:
         if need > self.ws.numel():
             self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
         x = torch.empty(pb.T, w.d, dtype=torch.float32, device=self.device)
-        # input tokens, original order: decode rows' last picks (on device), then the prompts
-        n_dec = len(batch) - len(new)
+        # input tokens, original order: decode rows' last picks (on device), then the prompt chunks
+        n_dec = len(dec)
         parts = []
         if n_dec:
-            parts.append(self._prev_nxt[self._h2d(np.array([s.row for s in batch[:n_dec]], np.int64))])
-        if new:
-            parts.append(self._h2d(np.concatenate([s.prompt for s in new]).astype(np.int32)))
+            parts.append(self._prev_nxt[self._h2d(np.array([s.row for s in dec], np.int64))])
+        if chunks:
+            parts.append(self._h2d(np.concatenate([s.prompt[s.cached:s.cached + n] for s, n in chunks])
+                                   .astype(np.int32)))
         ids_dev = torch.cat(parts) if len(parts) > 1 else parts[0]
         B.vfm_embed_forward(self.cfg, pb.c, B.VFM_EMBED_TOKENS, ids_dev, w.vocab, self.emb, None, x)
         tp = table.ctypes.data_as(B.C.POINTER(B.C.c_int32))     # one device table for every layer
@@ -356,19 +381,21 @@ class ContinuousBatcher:
         self._prev_nxt = nxt
         self._picks.append(nxt)
         self._keep = (pb, table, table_dev)            # host arrays the stream may still read
-        if self.record:
-            off = pb.out_off()
-            o = out.cpu().numpy()
-            self.trace.append([(s.rid, o[off[i]:off[i + 1]].copy()) for i, s in enumerate(batch)])
         if self.bfq is not None and n_dec:
             per_task = np.bincount(task[:n_dec], minlength=w.n_tasks)
             for t in np.nonzero(per_task)[0]:
                 self.bfq.charge(int(t), float(per_task[t]) * self.token_time)
-        finished = []
+        o = out.cpu().numpy() if self.record else None
+        off = pb.out_off() if self.record else None
+        rec, finished = [], []
         for i, s in enumerate(batch):
             s.cached += int(lens[i])
+            if s.cached < len(s.prompt):               # a chunk inside the prompt: no token yet
+                continue
             s.generated.append((self.steps, i))
             s.row = i
+            if self.record:
+                rec.append((s.rid, o[off[i]:off[i + 1]].copy()))
             if len(s.generated) == s.max_new:
                 self.alloc.release(s.slot)
                 self.free_slots.append(s.slot)
@@ -376,6 +403,8 @@ class ContinuousBatcher:
                 self.running.remove(s)
                 self.done[s.rid] = s
                 finished.append(s.rid)
+        if self.record:
+            self.trace.append(rec)
         self.steps += 1
         return finished
 

@@ -228,9 +228,9 @@ def test_paged_layer_rejects_bad_pages_before_launch():
     assert run(tab=np.array([[3, 1, -1], [0, 0, 0]], np.int32)) == B.VFM_ERR_SHAPE
     bidir = B.make_cfg(B.VFM_BF16, 4096, 32, 128, 11008, 1, 1, B.VFM_ATTN_BIDIR, 0, 1e-6, 1e4)
     assert run(c=bidir) == B.VFM_ERR_UNSUPPORTED
-    # mixed steps: a request with cached tokens and more than one new row is chunked prefill
-    mixed = B.make_cfg(B.VFM_BF16, 4096, 32, 128, 11008, 1, 1, B.VFM_ATTN_MIXED, 0, 1e-6, 1e4)
+    # mixed steps: a request with cached tokens and more than one new row is a prompt chunk
+    mixed32 = B.make_cfg(B.VFM_F32, 4096, 32, 128, 11008, 1, 1, B.VFM_ATTN_MIXED, 0, 1e-6, 1e4)
     chunked = B.vfm_plan([0, 1], [2, 1], 2, [40, 0], None)
-    assert run(c=mixed, batch=_batch_c(chunked)) == B.VFM_ERR_UNSUPPORTED
+    assert run(c=mixed32, batch=_batch_c(chunked)) == B.VFM_ERR_UNSUPPORTED   # prompt chunks: bf16 only
     decode_many = B.vfm_plan([0, 1], [1, 5], 2, [0, 0], None)
     assert run(batch=_batch_c(decode_many)) == B.VFM_ERR_UNSUPPORTED   # decode rows are single

@@ -46,11 +46,20 @@ def test_fifo_admission_respects_slots_tokens_and_pages():
 
 
 def test_fifo_admission_stops_at_the_first_prompt_that_does_not_fit():
-    cb = _batcher(max_step_tokens=40)
+    cb = _batcher(max_step_tokens=40, chunk_prompts=False)
     for rid, L in enumerate([30, 20, 5]):
         cb.submit(rid, 0, np.zeros(L, np.int32), 2)
     assert [s.rid for s in cb._admit(0.0)] == [0]    # 30 + 20 > 40: FIFO does not skip ahead
     assert [s.rid for s in cb.waiting] == [1, 2]
+
+
+def test_chunked_prompts_join_with_what_is_left_of_the_budget():
+    cb = _batcher(max_step_tokens=40, max_pages=6)
+    for rid, L in enumerate([30, 20, 5]):
+        cb.submit(rid, 0, np.zeros(L, np.int32), 2)
+    # 30 tokens, then 10 of the 20-token prompt; the third has no token left this step
+    assert [s.rid for s in cb._admit(0.0)] == [0, 1]
+    assert [s.rid for s in cb.waiting] == [2]
 
 
 def test_page_commitment_holds_back_prompts():

@@ -54,7 +54,8 @@ def _oracle_greedy(w, model, emb_np, task, prompt, n_new):
     return picks, outs
 
 
-@pytest.mark.parametrize("dtype,page,sched", [("bf16", 16, "fifo"), ("f32", 32, "fifo"), ("bf16", 16, "bfq")])
+@pytest.mark.parametrize("dtype,page,sched", [("bf16", 16, "fifo"), ("f32", 32, "fifo"), ("bf16", 16, "bfq"),
+                                             ("bf16", 16, "fifo-chunked")])
 def test_continuous_batching_loop(dtype, page, sched):
     w = _tiny_decoder(dtype)
     model = R.Model(w, n_layers=2, b_std=0.1)
@@ -66,7 +67,9 @@ def test_continuous_batching_loop(dtype, page, sched):
     if sched == "bfq":
         bfq = B.BFQ([1.0, 2.0, 1.0], np.linspace(1.0, 2.0, 3), b_max=2)
     # three sequence slots and a 12-page pool: requests wait for slots and pages
-    cb = R.ContinuousBatcher(model, emb, page_size=page, n_pages=12, max_seqs=3, max_step_tokens=96,
+    # "-chunked": 20 tokens per step, so the 24- and 33-token prompts are fed in chunks
+    budget = 20 if sched.endswith("chunked") else 96
+    cb = R.ContinuousBatcher(model, emb, page_size=page, n_pages=12, max_seqs=3, max_step_tokens=budget,
                              max_pages=6, bfq=bfq, record=True)
     for rid, ((task, _, n_new), pr) in enumerate(zip(REQUESTS, prompts)):
         cb.submit(rid, task, pr, n_new)
@@ -105,7 +108,7 @@ def test_continuous_batching_loop(dtype, page, sched):
     # the same requests through the asynchronous path (no per-step read-back)
     # pick the same tokens
     bfq2 = B.BFQ([1.0, 2.0, 1.0], np.linspace(1.0, 2.0, 3), b_max=2) if sched == "bfq" else None
-    cb2 = R.ContinuousBatcher(model, emb, page_size=page, n_pages=12, max_seqs=3, max_step_tokens=96,
+    cb2 = R.ContinuousBatcher(model, emb, page_size=page, n_pages=12, max_seqs=3, max_step_tokens=budget,
                               max_pages=6, bfq=bfq2)
     for rid, ((task, _, n_new), pr) in enumerate(zip(REQUESTS, prompts)):
         cb2.submit(rid, task, pr, n_new)

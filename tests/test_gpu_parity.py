@@ -732,13 +732,15 @@ def _page_rows(pool, table, i, n, page):
 
 
 @pytest.mark.parametrize("ctx_long,layout", [(300, "paged"), (2100, "paged"), (2100, "contiguous"),
-                                             (0, "causal-paged")])
+                                             (0, "causal-paged"), (300, "paged-chunked"),
+                                             (2100, "contiguous-chunked")])
 def test_mixed_step_over_cache(ctx_long, layout):
     """One continuous-batching step (7B decoder layer dims): two prompts (70
     and 33 tokens, ctx 0) and three decode tokens (ctx 63, 1100 and a long
     one) in one batch, over a paged cache (pages of 64 in random order) or
-    the contiguous one (vfm_layer_forward, slots kv_start + k); and a
-    prompts-only causal step over pages.  Every row against the oracle
+    the contiguous one (vfm_layer_forward, slots kv_start + k), with and
+    without a 40-row prompt chunk after cached tokens in place of a decode
+    row; and a prompts-only causal step over pages.  Every row against the oracle
     (prompts causal over themselves, decode rows over their cached keys plus
     themselves), and every new row's rotated K and V in its slots."""
     w = wl.WORKLOADS[4]
@@ -747,13 +749,14 @@ def test_mixed_step_over_cache(ctx_long, layout):
         seq_len = np.array([70, 1, 33, 5, 2], np.int32)
         ctx = np.zeros(5, np.int32)
     else:
-        seq_len = np.array([70, 1, 33, 1, 1], np.int32)
+        # "-chunked": request 3 is a 40-row prompt chunk after its ctx cached tokens
+        seq_len = np.array([70, 1, 33, 40 if "chunked" in layout else 1, 1], np.int32)
         ctx = np.array([0, 63, 0, ctx_long, 1100], np.int32)
     batch = wl.Batch(task_id, seq_len, ctx)
     model = R.Model(w, n_layers=1, b_std=0.1)
     inp = R.Inputs(w, batch)
     n_tok = ctx.astype(np.int64) + seq_len
-    if layout == "contiguous":
+    if layout.startswith("contiguous"):
         # slots kv_start[i] + k: a "page table" of single slots for the oracle's reads
         page = 1
         kvs = np.concatenate([[0], np.cumsum(n_tok + 3)[:-1]]).astype(np.int32)
@@ -773,14 +776,15 @@ def test_mixed_step_over_cache(ctx_long, layout):
     vp = torch.randn(w.n_heads, total * page, w.head_dim, generator=g, device="cuda").to(torch.bfloat16)
     cfg = R.cfg_for(w)
     cfg.attn = B.VFM_ATTN_CAUSAL if layout == "causal-paged" else B.VFM_ATTN_MIXED
-    pb = B.Batch(task_id, seq_len, w.n_tasks, ctx_len=ctx, kv_start=kvs if layout == "contiguous" else None)
+    contiguous = layout.startswith("contiguous")
+    pb = B.Batch(task_id, seq_len, w.n_tasks, ctx_len=ctx, kv_start=kvs if contiguous else None)
     fwd = R.Forward(model, pb, inp)
     ws = torch.empty(B.vfm_workspace_size(cfg, pb.c, model.lora_c(0)), dtype=torch.uint8, device="cuda")
     log(f"{layout} step: lens {list(seq_len)} ctx {list(ctx)} T={pb.T}")
     pl = O.plan(task_id, seq_len, w.n_tasks, ctx=ctx)
     x_in = as_f32(expected_embed(w, batch, inp, pl))
     set_rows(fwd.x, x_in)
-    if layout == "contiguous":
+    if contiguous:
         B.vfm_layer_forward(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x, kp, vp, total, ws)
     else:
         B.vfm_layer_forward_paged(cfg, model.c_layers[0], model.lora_c(0), pb.c, fwd.x,
