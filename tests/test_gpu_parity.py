@@ -809,3 +809,33 @@ def test_mixed_step_over_cache(ctx_long, layout):
         assert O.row_rel_error(k_new, k) < tol(w) and O.row_rel_error(v_new, v) < tol(w)
     log(f"  max rel err {worst:.3e}")
     assert worst < tol(w)
+
+
+@pytest.mark.parametrize("idx,seed", [(1, 0), (1, 1), (1, 2), (2, 3), (2, 4), (3, 5), (2, 6)])
+def test_random_batches_layer_parity(idx, seed):
+    """Seeded random batches: 1..12 requests of 1..150 rows, task ids drawn
+    over every task (absent ids included), per-task ranks 0 / 8 / 16: every
+    row of one layer against the oracle, both sides fed the oracle's input
+    rows (small batches take the split-K path, larger ones the tile path)."""
+    w = wl.WORKLOADS[idx]
+    rng = np.random.default_rng(1000 + seed)
+    big = seed == 6                            # at least 1024 rows: the large-tile path
+    n = 12 if big else int(rng.integers(1, 13))
+    case = dict(task_id=rng.integers(0, w.n_tasks, size=n).tolist(),
+                seq_len=rng.integers(90 if big else 1, 151, size=n).tolist())
+    ranks = (8 * rng.integers(0, 3, size=w.n_tasks)).astype(np.int32)
+    if idx == 3:
+        case["seq_len"] = [64] * n             # the time-series workload's patches come in whole series
+    w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, b_std=0.1, ranks=ranks, case=case)
+    log(f"random batch workload {idx} seed {seed}: {n} requests, T={pb.T}, ranks {list(ranks[:8])}")
+    assert not big or pb.T >= B.VFM_SMALL_BATCH_ROWS
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    res = oracle_layer_rows(w, oracle_weights(model.layers[0]), model.adapters[0], pl, x_in, range(batch.n_req))
+    cu = pl["cu_seqlens"]
+    worst = max(O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]) for p in range(batch.n_req))
+    log(f"  max row rel err {worst:.3e}")
+    assert worst < tol(w)
