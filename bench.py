@@ -391,9 +391,11 @@ def main():
     elif w.dtype != "bf16":
         kname = "gemm_f32_kernel (MLP up projection + GELU)"
     elif w.family == "decoder":
-        kname = "gemm_bf16_large_kernel (gate/up projections + SwiGLU, LoRA fused)"
+        kname = "gemm_bf16_large_kernel (gate/up projections + SwiGLU" + (
+            ", LoRA fused)" if {"gate", "up"} & set(w.lora_targets) else ")")
     else:
-        kname = "gemm_bf16_large_kernel (MLP up projection + GELU, LoRA fused)"
+        kname = "gemm_bf16_large_kernel (MLP up projection + GELU" + (
+            ", LoRA fused)" if "up" in w.lora_targets else ")")
     roof.update({"kernel": kname,
                  "avg_launch_ms": avg_ms, "launches": dom_n, "per_launch": per_launch})
 
