@@ -2,16 +2,19 @@
 
 One step = one whole forward of a mixed batch: input rows -> every backbone
 layer (shared projections + per-task LoRA + per-request attention) -> final
-norm, pooling and per-task heads.  Default workload: the ViT-B-shaped encoder
-(12 layers, d 768, 64 requests x 197 tokens, 16 tasks with Zipf(1.1) task ids,
-LoRA rank 16 on q/k/v/o, per-task heads of 10..1000 classes), inputs already
-resident in HBM.
+norm (and, where the workload has them, pooling and per-task heads).  Default
+workload: the Llama-7B-shaped decoder prefill (32 layers, d 4096, SwiGLU
+11008, RoPE, RMSNorm; 32 prompts of U[128, 1024] tokens over 64 tasks with
+Zipf(1.1) task ids, LoRA rank 16 on all seven projections), the largest
+configuration that fits one GPU, with every input resident in HBM.
 
-Prints ONE JSON line.  `value` is tokens/s of the whole step; `roofline` is
-the dominant kernel's achieved rate (algorithmic FLOPs or bytes per launch /
-its average duration from hipEvents recorded around its launches inside the
-timed region) against the MI355X peak; `cpu_baseline` times the fp64 oracle
-on a bounded sample of the same batch on this host's cores.
+Prints ONE JSON line.  `value` is tokens/s of the whole step from the median
+of the timed steps (each step bracketed by its own pair of hipEvents on the
+forward's stream); `roofline` is the dominant kernel's achieved rate
+(algorithmic FLOPs or bytes per launch / its average duration from hipEvents
+recorded around its launches inside the same timed region) against the
+MI355X peak; `cpu_baseline` times the fp64 oracle on a bounded sample of the
+same batch on this host's cores (all of them, then one).
 """
 from __future__ import annotations
 
@@ -108,29 +111,58 @@ def hbm_traffic(workload_name, cls):
 # --------------------------------------------------------------------------
 # CPU baseline: the fp64 oracle on a bounded sample of the same batch
 # --------------------------------------------------------------------------
-def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def _baseline_sample(w, batch, pl):
+    """Requests (original indices) the oracle is timed on, per workload: every
+    request of the tiny encoder, 8 ViT-B requests, 16 time series, the
+    shortest and the longest decoder prompt, 8 decode requests (the first
+    ones in original order)."""
+    n = batch.n_req
+    if w.family == "decoder" and w.mode != "decode":
+        lens = batch.seq_len
+        return sorted({int(np.argmin(lens)), int(np.argmax(lens))})
+    k = {"tiny-encoder-f32": n, "vitb-encoder-bf16": 8, "t5l-timeseries-bf16": 16}.get(w.name, 8)
+    return list(range(min(k, n)))
+
+
+def cpu_baseline(w, batch, model, inp, kv=None):
     """The fp64 oracle on whole requests of the same batch, layer by layer.
 
-    Requests are taken in original order until the oracle time estimated
-    from their first layer reaches about `budget_s`; then every layer and the
-    final norm / head run for those requests.  Each layer's bf16 weights
-    (and, when decoding, the requests' KV slices) are converted to fp64
-    outside the timed region.
+    The sample (_baseline_sample) runs every layer and the final norm / head
+    on all of this host's cores (BLAS threads), then its first layer again
+    on one core; each layer's weights (and, when decoding, the requests' KV
+    slices) are converted to fp64 outside the timed regions.  Also reported:
+    the whole batch's oracle time derived from the sample (scaled by tokens,
+    marked derived) and the CPU model.
     """
     from oracle import vfm_oracle as O
     from tests.gpu_common import expected_embed, oracle_plan
     from tests.helpers import np64, oracle_adapter, oracle_weights, spec_of
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
+        threadpool_limits = None
         cores = os.cpu_count()
     pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
     x_all = expected_embed(w, batch, inp, pl)
     spec = spec_of(w)
     cu = pl["cu_seqlens"]
     inv = np.argsort(pl["order"])
-    xs = {}
+    sample = _baseline_sample(w, batch, pl)
+    x0 = {i: x_all[int(cu[int(inv[i])]):int(cu[int(inv[i]) + 1])] for i in sample}
+    del x_all
+    xs = dict(x0)
 
     def kv_of(li, i):
         if kv is None:
@@ -139,33 +171,25 @@ def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
         kr, vr = kv.rows(li, s0, c)
         return (np64(kr), np64(vr))
 
-    def run_layer(Wn, li, i, kvp):
+    def run_layer(Wn, li, i, x, kvp):
         p = int(inv[i])
         t = int(pl["task"][p])
         sl = slice(int(cu[p]), int(cu[p + 1]))
-        return O.layer(spec, Wn, oracle_adapter(model.adapters[li], t), xs[i], pos=pl["pos"][sl],
+        return O.layer(spec, Wn, oracle_adapter(model.adapters[li], t), x, pos=pl["pos"][sl],
                        kv=kvp)[0]
 
-    W0 = oracle_weights(model.layers[0])
-    sample, est = [], 0.0
-    for i in range(batch.n_req):
-        p = int(inv[i])
-        xs[i] = x_all[int(cu[p]):int(cu[p + 1])]
-        kvp = kv_of(0, i)
-        t0 = time.perf_counter()
-        run_layer(W0, 0, i, kvp)
-        est += (time.perf_counter() - t0) * w.n_layers
-        sample.append(i)
-        if est > budget_s:
-            break
     elapsed = 0.0
+    W0 = None
     for li in range(w.n_layers):
-        Wn = W0 if li == 0 else oracle_weights(model.layers[li])
+        Wn = oracle_weights(model.layers[li])
+        if li == 0:
+            W0 = Wn
         kvs = {i: kv_of(li, i) for i in sample}
         t0 = time.perf_counter()
         for i in sample:
-            xs[i] = run_layer(Wn, li, i, kvs[i])
+            xs[i] = run_layer(Wn, li, i, xs[i], kvs[i])
         elapsed += time.perf_counter() - t0
+        del Wn
     fw, fb = np64(model.final["w"]), np64(model.final["b"])
     t0 = time.perf_counter()
     for i in sample:
@@ -175,10 +199,28 @@ def cpu_baseline(w, batch, model, inp, kv=None, budget_s=20.0):
             O.head(O.pool(xn, w.pool), np64(model.heads.W[t]), np64(model.heads.b[t]))
     elapsed += time.perf_counter() - t0
     tokens = int(sum(xs[i].shape[0] for i in sample))
+    # one core: the sample's first layer, scaled to every layer (derived)
+    single = None
+    if threadpool_limits is not None:
+        kvs = {i: kv_of(0, i) for i in sample}
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            for i in sample:
+                run_layer(W0, 0, i, x0[i], kvs[i])
+            t1 = time.perf_counter() - t0
+        single = {"value": tokens / (t1 * w.n_layers), "unit": "tokens/s", "cores": 1,
+                  "layer_seconds": t1, "derived": f"layer 0 of the same sample timed on one core, "
+                                                  f"scaled to {w.n_layers} layers"}
+    total_tokens = int(batch.total_rows)
     return {"value": tokens / elapsed, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {len(sample)} of {batch.n_req} requests (original order), "
-                      f"{tokens} tokens, all {w.n_layers} layers + final norm/head, fp64 numpy, "
-                      f"{elapsed:.1f} s"}
+            "cpu_model": _cpu_model(),
+            "sample": f"requests {sample} of {batch.n_req} (original order), {tokens} tokens, "
+                      f"all {w.n_layers} layers + final norm" + ("/head" if model.heads is not None else "")
+                      + f", fp64 numpy, {elapsed:.1f} s",
+            "seconds": elapsed,
+            "single_core": single,
+            "full_batch_seconds_derived": elapsed * total_tokens / tokens,
+            "full_batch_note": f"derived: the sample's time scaled by tokens ({total_tokens} / {tokens})"}
 
 
 def loop_bench(args):
@@ -296,7 +338,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=4,
+                    help="1 tiny fp32 encoder, 2 ViT-B, 3 time-series encoder, "
+                         "4 7B decoder prefill (default), 5 7B decoder decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--task-load", action="store_true",
                     help="time loading one task's adapters and head into the ViT-B-shaped backbone")
@@ -355,20 +399,26 @@ def main():
         fwd(stream)
     torch.cuda.synchronize()
 
-    # the dominant kernel class is timed with hipEvents inside the timed region
+    # Timed region: exactly `steps` forwards, each bracketed by its own pair
+    # of events on the forward's stream; the dominant kernel class is timed
+    # with hipEvents around each of its launches inside the same region (the
+    # library records them on the stream it launches on).
     dom = "attn" if w.mode == "decode" else "gemm_up"
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
     B.vfm_profile_enable([dom])
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for _ in range(args.steps):
+    t_wall = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record(stream)
         fwd(stream)
-    t_end.record(stream)
+        e1.record(stream)
     torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t_wall
     prof = B.vfm_profile_read()
     B.vfm_profile_enable([])
-    ms_step = t_start.elapsed_time(t_end) / args.steps
+    step_ms = np.array([e0.elapsed_time(e1) for e0, e1 in ev])
+    ms_step = float(np.median(step_ms))
     tokens = batch.total_rows
     value = tokens / (ms_step * 1e-3)
 
@@ -411,6 +461,8 @@ def main():
                    "layers": w.n_layers, "d_model": w.d, "d_ff": w.d_ff, "lora_rank": w.rank,
                    "lora_targets": list(w.lora_targets),
                    "kv_cache": f"paged {args.paged}" if args.paged else "contiguous"},
+        "ms_per_step_mean": float(step_ms.mean()), "ms_per_step_min": float(step_ms.min()),
+        "ms_per_step_max": float(step_ms.max()), "timed_wall_s": wall_s,
         "step_tflops": step_tflops,
         "step_roofline_frac": step_tflops / peak_step if w.mode != "decode" else
         (work["step_bytes"] / (ms_step * 1e-3) / 1e9) / PEAK_HBM_GBS,

@@ -283,6 +283,10 @@ int vfm_embed_series(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_encod
 
 /* ------------------------------------------------------------------------
  * a2-a10. One backbone layer over the whole mixed batch, in place on x.
+ * The shared projections run once over the rows of every task and each
+ * task's adapter difference is added on its own rows only (Section 4.2, the
+ * adapter handling in the last paragraph of "Batch-aware Fair Scheduling";
+ * example (c) of Fig. 5); attention stays within each request.
  *   x: device float32 [T, d], plan order (residual stream).
  *   lora: NULL for the bare backbone.
  *   k_cache, v_cache: device [n_heads, kv_slots, head_dim] (dtype), head-major,
@@ -297,6 +301,14 @@ int vfm_embed_series(const vfm_cfg* cfg, const vfm_batch* batch, const vfm_encod
  * RoPE; attention per request; x += attn W_o^T + b_o (+ LoRA_o);
  * h2 = Norm2(x); u = MLP(h2) (+ LoRA on gate/up); x += u W_down^T + b_down
  * (+ LoRA_down).
+ * Errors: the checks listed in the file header; VFM_ERR_ARG for a missing
+ * weight or (decode / mixed) a missing cache; VFM_ERR_SHAPE when a request's
+ * cache slots kv_start + ctx + len exceed kv_slots; VFM_ERR_UNSUPPORTED for a
+ * VFM_ATTN_DECODE request of more than one row, for a VFM_ATTN_BIDIR or
+ * VFM_ATTN_CAUSAL request with ctx > 0 (those steps attend over the
+ * request's own rows only), and for a prompt chunk in an fp32 mixed step;
+ * VFM_ERR_WORKSPACE for a workspace below vfm_workspace_size or not 256-byte
+ * aligned.
  * ---------------------------------------------------------------------- */
 int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
                       const vfm_batch* batch, float* x, void* k_cache, void* v_cache,
@@ -319,10 +331,12 @@ int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_
  *   VFM_ATTN_CAUSAL  every request a prompt (ctx 0): causal attention over
  *                    its own rows, whose K / V are written into its pages.
  *   VFM_ATTN_DECODE  every request one new token after ctx cached ones.
- *   VFM_ATTN_MIXED   a continuous-batching step: each request either a
- *                    prompt (ctx 0, any length) or one decode token (ctx > 0,
- *                    length 1); a request with ctx > 0 and more than one row
- *                    (chunked prefill) gives VFM_ERR_UNSUPPORTED.
+ *   VFM_ATTN_MIXED   a continuous-batching step: each request is a prompt
+ *                    (ctx 0, any length), one decode token (ctx > 0, length
+ *                    1) or, in bf16, a prompt chunk after cached tokens
+ *                    (ctx > 0, several rows: each row attends causally to the
+ *                    ctx cached keys and the chunk's earlier rows).  An fp32
+ *                    step with such a chunk gives VFM_ERR_UNSUPPORTED.
  * The new rows' K / V go to slots ctx .. ctx + len - 1 of the request's pages
  * before attention reads them.
  * ---------------------------------------------------------------------- */
@@ -340,7 +354,9 @@ typedef struct vfm_kv_pages {
 /* Errors as vfm_layer_forward, plus VFM_ERR_SHAPE when a request's
  * ctx + len tokens need more than max_pages pages or a page id it uses is
  * outside [0, n_pages), VFM_ERR_ARG for a bad page size or null tables, and
- * VFM_ERR_UNSUPPORTED for VFM_ATTN_BIDIR or a chunked-prefill request. */
+ * VFM_ERR_UNSUPPORTED for VFM_ATTN_BIDIR, for a VFM_ATTN_CAUSAL request with
+ * ctx > 0, and for a prompt chunk (ctx > 0, more than one row) in an fp32
+ * VFM_ATTN_MIXED step (bf16 accepts it). */
 int vfm_layer_forward_paged(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
                             const vfm_batch* batch, float* x, const vfm_kv_pages* kv, void* workspace,
                             size_t ws_bytes, void* stream);
@@ -348,22 +364,35 @@ int vfm_layer_forward_paged(const vfm_cfg* cfg, const vfm_layer_weights* w, cons
 /* ------------------------------------------------------------------------
  * a4. Segmented LoRA on one projection: for every plan-order row m of task
  * t with rank_t > 0,  y[m, :] += scale_t * (x[m, :] A_{t,proj}^T) B_{t,proj}^T.
+ * This is the per-task adapter difference on its own (LoRA, Section 2.2;
+ * applied per task segment of the shared batch, Section 4.2 adapter
+ * handling).  Rows of rank-0 tasks are left untouched.
  *   x: device [T, d_in] (dtype), plan order.  y: device float32 [T, d_out].
  *   d_in a multiple of 64, d_out a multiple of 4 (else VFM_ERR_SHAPE).
  *   workspace: device, >= T * rpad * sizeof(dtype) bytes (rpad = 32 if
  *   max_rank <= 32, else 64), 256-byte aligned.
+ * Errors: VFM_ERR_ARG for a bad dtype / projection, null pointers or a
+ * projection without adapters in the table; VFM_ERR_SHAPE as above and for a
+ * table of another task count; VFM_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
 int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t d_out,
                    const vfm_lora_table* lora, const vfm_batch* batch, const void* x, float* y,
                    void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * a11-a12. Final norm, pooling and per-task heads.
+ * a11-a12. Final norm, pooling and per-task heads: each request ends in its
+ * own task's decoder head on the shared backbone's output (Section 2.2
+ * decoders; Section 4.1 task extensions; Table 1 add_decoder).
  *   x: device float32 [T, d] plan order (the last layer's output).
  *   heads != NULL: out = device float32 [total_outputs]; request i's
  *     outputs W_t pool(Norm(x_i)) + b_t start at out_off[i] (original order).
  *   heads == NULL: out = device float32 [T, d], the final-normed rows in
  *     original order.
+ *   workspace: device, >= vfm_workspace_size bytes, 256-byte aligned (holds
+ *     the pooled rows and MLP heads' hidden rows).
+ * Errors: VFM_ERR_ARG for null pointers, a head table of another task count,
+ * a bad pooling mode or activation; VFM_ERR_SHAPE for a bad hidden width;
+ * VFM_ERR_UNSUPPORTED for d * sizeof(dtype) above 64 KB; VFM_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
 int vfm_head_forward(const vfm_cfg* cfg, const void* final_norm_w, const void* final_norm_b,
                      const vfm_head_table* heads, const vfm_batch* batch, const float* x,

@@ -196,6 +196,13 @@ int check_layer(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_t
   }
   if (cfg->attn == VFM_ATTN_DECODE && pl->max_seqlen != 1) return VFM_ERR_UNSUPPORTED;
   const PlanOffsets po = plan_offsets(pl->n_req, pl->n_tasks, pl->T);
+  if (cfg->attn == VFM_ATTN_BIDIR || cfg->attn == VFM_ATTN_CAUSAL) {
+    // these steps attend over a request's own rows only: cached tokens
+    // before them would be ignored, so a request with ctx > 0 is refused
+    const int32_t* ctx = host_arr(batch, po.ctx);
+    for (int p = 0; p < pl->n_req; ++p)
+      if (ctx[p] > 0) return VFM_ERR_UNSUPPORTED;
+  }
   if (cfg->attn == VFM_ATTN_MIXED && cfg->dtype != VFM_BF16) {   // prompt chunks after cached tokens: bf16
     const int32_t* ctx = host_arr(batch, po.ctx);
     const int32_t* cu = host_arr(batch, po.cu_seqlens);

@@ -234,3 +234,39 @@ def test_paged_layer_rejects_bad_pages_before_launch():
     assert run(c=mixed32, batch=_batch_c(chunked)) == B.VFM_ERR_UNSUPPORTED   # prompt chunks: bf16 only
     decode_many = B.vfm_plan([0, 1], [1, 5], 2, [0, 0], None)
     assert run(batch=_batch_c(decode_many)) == B.VFM_ERR_UNSUPPORTED   # decode rows are single
+
+
+def test_prompt_steps_refuse_cached_context():
+    """Bidirectional and causal steps attend over a request's own rows only,
+    so a request that brings cached tokens (ctx > 0) is refused on the host
+    (contiguous and paged entry points alike) instead of ignoring them; the
+    same batch is accepted as a mixed step."""
+    lib = B.lib()
+    fake = 1 << 20
+    weights = B.vfm_layer_weights(*([fake] * 13))
+    host = B.vfm_plan([0, 1], [3, 2], 2, [0, 17], None)        # request 1: a chunk after 17 tokens
+    bc = _batch_c(host)
+    zero = _batch_c(B.vfm_plan([0, 1], [3, 2], 2, [0, 0], None))
+    table = np.array([[0], [1]], np.int32)
+
+    def cfg(attn):
+        return B.make_cfg(B.VFM_BF16, 4096, 32, 128, 11008, 1, 1, attn, 0, 1e-6, 1e4)
+
+    def plain(c, batch, kc=fake):
+        return lib.vfm_layer_forward(C.byref(c), C.byref(weights), None, C.byref(batch), fake,
+                                     kc, kc, 1 << 20, fake, 1 << 40, None)
+
+    def paged(c, batch):
+        kv = B.vfm_kv_pages(fake, fake, 4, 64, 1, table.ctypes.data_as(C.POINTER(C.c_int32)), fake)
+        return lib.vfm_layer_forward_paged(C.byref(c), C.byref(weights), None, C.byref(batch), fake,
+                                           C.byref(kv), fake, 1 << 40, None)
+
+    for attn in (B.VFM_ATTN_BIDIR, B.VFM_ATTN_CAUSAL):
+        assert plain(cfg(attn), bc) == B.VFM_ERR_UNSUPPORTED
+        assert plain(cfg(attn), bc, kc=None) == B.VFM_ERR_UNSUPPORTED
+    assert paged(cfg(B.VFM_ATTN_CAUSAL), bc) == B.VFM_ERR_UNSUPPORTED
+    # without cached tokens the same shapes pass this check and stop at the
+    # workspace check that follows it (a null workspace; nothing launched)
+    c = cfg(B.VFM_ATTN_CAUSAL)
+    assert lib.vfm_layer_forward(C.byref(c), C.byref(weights), None, C.byref(zero), fake,
+                                 None, None, 0, None, 0, None) == B.VFM_ERR_WORKSPACE

@@ -334,6 +334,31 @@ def test_decode_step_equals_last_prefill_row():
     assert np.allclose(k1, k[L:], atol=1e-12) and np.allclose(v1, v[L:], atol=1e-12)
 
 
+@pytest.mark.parametrize("L,m", [(12, 5), (7, 1), (1, 9), (20, 13)])
+def test_prefill_chunk_equals_rows_of_full_prefill(L, m):
+    """A prompt chunk of m rows after L cached tokens (the chunked-prefill
+    step) equals rows L .. L+m-1 of the whole (L+m)-token prefill: each chunk
+    row attends causally to the cached keys and the chunk's earlier rows.
+    Pins the multi-row branch of the cached-key attention (q_offset > 0,
+    causal mask inside the chunk), not only its one-row decode case."""
+    w = _tiny("decoder")
+    W = oracle_weights(wl.backbone_layer(w, 0))
+    ad = oracle_adapter(wl.adapters_layer(w, 0, b_std=0.3), 2)
+    x = _rng(40 + L + m).normal(size=(L + m, w.d))
+    full, k, v = O.layer(spec_of(w), W, ad, x, pos=np.arange(L + m))
+    chunk, kc, vc = O.layer(spec_of(w), W, ad, x[L:], pos=np.arange(L, L + m), kv=(k[:L], v[:L]))
+    assert np.abs(chunk - full[L:]).max() <= 1e-12 * np.abs(full[L:]).max()
+    assert np.abs(kc - k[L:]).max() <= 1e-12 * np.abs(k[L:]).max()
+    assert np.abs(vc - v[L:]).max() <= 1e-12 * np.abs(v[L:]).max()
+    # a wrong mask inside the chunk (every chunk row seeing the whole chunk) is caught
+    q_full = O.rope(O.linear(O.rms_norm(x, W["norm1_w"], w.norm_eps), W["w_qkv"][:w.d]),
+                    np.arange(L + m), w.n_heads, w.head_dim, w.rope_theta)
+    if m > 1:
+        leak = O.attention(q_full[L:], k, v, w.n_heads, w.head_dim, causal=False)
+        ok = O.attention(q_full[L:], k, v, w.n_heads, w.head_dim, causal=True, q_offset=L)
+        assert np.abs(leak - ok).max() > 1e-3
+
+
 # --------------------------------------------------------------------------
 # the method's re-association equals the per-request definition
 # --------------------------------------------------------------------------
