@@ -315,6 +315,35 @@ int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_
                       int64_t kv_slots, void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * vfm_layer_forward without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops
+ * and harnesses that forbid allocation.  Same arguments (minus workspace),
+ * same kernels, same results and errors as vfm_layer_forward.
+ *
+ * The workspace is instead a fixed array of VFM_NOALLOC_SCRATCH_BYTES inside
+ * the library, one per GPU, held by each GPU the library runs on until the
+ * process ends.  A batch whose workspace (vfm_workspace_size) exceeds it is
+ * refused on the host with VFM_ERR_WORKSPACE (the decode step of 256 rows of
+ * a 4096-wide, 11008-MLP decoder needs about 105 MiB; a 12 608-row ViT-B
+ * batch about 117 MiB).  The call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine): the array's device address is looked up once
+ * per device, on the first call with that device current.  stream must
+ * belong to the current device (VFM_ERR_ARG otherwise).
+ *
+ * Every call on one GPU uses that GPU's one array: calls that overlap on a
+ * GPU (two streams, or two host threads) race and must be serialised by the
+ * caller; calls in stream order on one stream are safe.  The array keeps the
+ * last call's contents; no call reads what an earlier one left.  As with
+ * every entry point, timing events are recorded only while vfm_profile_enable
+ * has a class enabled (a benchmark facility), so leave it disabled here.
+ * ---------------------------------------------------------------------- */
+#define VFM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+int vfm_layer_forward_noalloc(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
+                              const vfm_batch* batch, float* x, void* k_cache, void* v_cache,
+                              int64_t kv_slots, void* stream);
+
+/* ------------------------------------------------------------------------
  * a2-a10 over a paged KV cache: the token-based FMs' continuous batching
  * with long-lived decode iterations (Section 4.2, which also charges their
  * token-level work in service-time units; Section 6 maps the vFM boundary

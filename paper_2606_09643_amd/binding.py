@@ -30,6 +30,7 @@ VFM_NPROJ = 7
 VFM_PLAN_HEADER = 16
 VFM_ROW_TILE = 64
 VFM_SMALL_BATCH_ROWS = 1024
+VFM_NOALLOC_SCRATCH_BYTES = 128 << 20
 PROJ = ("q", "k", "v", "o", "gate", "up", "down")
 
 EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size",
@@ -39,7 +40,8 @@ EXPORTS = ("vfm_status_string", "vfm_plan_size", "vfm_plan", "vfm_workspace_size
            "vfm_bfq_queued", "vfm_bfq_tags", "vfm_lora_attach", "vfm_head_attach",
            "vfm_embed_series", "vfm_encoder_attach", "vfm_layer_forward_paged", "vfm_greedy_tokens",
            "vfm_pages_state_size", "vfm_pages_init", "vfm_pages_reserve", "vfm_pages_release",
-           "vfm_pages_table", "vfm_pages_count", "vfm_bfq_charge")
+           "vfm_pages_table", "vfm_pages_count", "vfm_bfq_charge",
+           "vfm_layer_forward_noalloc")
 PROF_CLASSES = ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down", "attn", "norm", "shrink", "other")
 
 
@@ -111,6 +113,9 @@ def _lib_handle():
                                           C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
                                           C.c_void_p, C.c_size_t, C.c_void_p]
+        lib.vfm_layer_forward_noalloc.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_layer_weights),
+                                                  C.POINTER(vfm_lora_table), C.POINTER(vfm_batch),
+                                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]
         lib.vfm_layer_forward_paged.argtypes = [C.POINTER(vfm_cfg), C.POINTER(vfm_layer_weights),
                                                 C.POINTER(vfm_lora_table), C.POINTER(vfm_batch), C.c_void_p,
                                                 C.POINTER(vfm_kv_pages), C.c_void_p, C.c_size_t, C.c_void_p]
@@ -229,6 +234,15 @@ def vfm_layer_forward(cfg, weights, lora, batch, x, k_cache=None, v_cache=None, 
                                          C.byref(batch), _ptr(x), _ptr(k_cache), _ptr(v_cache),
                                          kv_slots, ws_ptr, ws_bytes, _stream(stream))
     _check(st, "vfm_layer_forward")
+
+
+def vfm_layer_forward_noalloc(cfg, weights, lora, batch, x, k_cache=None, v_cache=None, kv_slots=0,
+                              stream=None):
+    st = _lib_handle().vfm_layer_forward_noalloc(C.byref(cfg), C.byref(weights),
+                                                 C.byref(lora) if lora is not None else None,
+                                                 C.byref(batch), _ptr(x), _ptr(k_cache), _ptr(v_cache),
+                                                 kv_slots, _stream(stream))
+    _check(st, "vfm_layer_forward_noalloc")
 
 
 class PagedKV:

@@ -2,6 +2,7 @@
 // sequence of one backbone layer over a mixed-task batch.
 #include <algorithm>
 #include <initializer_list>
+#include <mutex>
 
 #include "vfm_internal.h"
 
@@ -218,26 +219,94 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
 
 }  // namespace
 
+namespace {
+
+// Checks of the contiguous-cache layer call: check_layer plus the cache's
+// bounds (host copy of the plan).
+int check_layer_contiguous(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_lora_table* lora,
+                           const vfm_batch* batch, const float* x, const void* k_cache,
+                           const void* v_cache, int64_t kv_slots, Plan* pl) {
+  if ((k_cache != nullptr) != (v_cache != nullptr)) return VFM_ERR_ARG;
+  VFM_TRY(check_layer(cfg, w, lora, batch, x, k_cache != nullptr, pl));
+  if (k_cache) {
+    const PlanOffsets po = plan_offsets(pl->n_req, pl->n_tasks, pl->T);
+    const int32_t* ctx = host_arr(batch, po.ctx);
+    const int32_t* kvs = host_arr(batch, po.kv_start);
+    const int32_t* cu = host_arr(batch, po.cu_seqlens);
+    for (int p = 0; p < pl->n_req; ++p) {
+      const int64_t end = (int64_t)kvs[p] + ctx[p] + (cu[p + 1] - cu[p]);
+      if (end > kv_slots) return VFM_ERR_SHAPE;
+    }
+  }
+  return VFM_OK;
+}
+
+}  // namespace
+
 extern "C" int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w,
                                  const vfm_lora_table* lora, const vfm_batch* batch, float* x,
                                  void* k_cache, void* v_cache, int64_t kv_slots, void* workspace,
                                  size_t ws_bytes, void* stream) {
   Plan pl;
-  if ((k_cache != nullptr) != (v_cache != nullptr)) return VFM_ERR_ARG;
-  VFM_TRY(check_layer(cfg, w, lora, batch, x, k_cache != nullptr, &pl));
-  // KV-cache bounds (host copy of the plan)
-  if (k_cache) {
-    const PlanOffsets po = plan_offsets(pl.n_req, pl.n_tasks, pl.T);
-    const int32_t* ctx = host_arr(batch, po.ctx);
-    const int32_t* kvs = host_arr(batch, po.kv_start);
-    const int32_t* cu = host_arr(batch, po.cu_seqlens);
-    for (int p = 0; p < pl.n_req; ++p) {
-      const int64_t end = (int64_t)kvs[p] + ctx[p] + (cu[p + 1] - cu[p]);
-      if (end > kv_slots) return VFM_ERR_SHAPE;
-    }
-  }
+  VFM_TRY(check_layer_contiguous(cfg, w, lora, batch, x, k_cache, v_cache, kv_slots, &pl));
   return layer_impl(*cfg, w, lora, batch, pl, x, k_cache, v_cache, kv_slots, KvPages{nullptr, 0, 0},
                     workspace, ws_bytes, stream);
+}
+
+// ---- the allocation-free layer call ----------------------------------------
+namespace {
+
+// Workspace of vfm_layer_forward_noalloc.  Every GPU the library runs on
+// holds its own copy of this array, at its own address, until the process
+// ends.  In host code `scratch` names a host-side stand-in, not the device
+// memory: host code uses only the device address hipGetSymbolAddress returns
+// for the current device (kept per device below), never the name itself.
+static __device__ __align__(256) unsigned char scratch[VFM_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, looked up once per
+// device (with that device current) on its first call.  The stream must
+// belong to the current device, since the address is that device's.
+int scratch_of_current_device(hipStream_t s, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return VFM_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return VFM_ERR_UNSUPPORTED;
+  if (s != nullptr) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(s, &sdev) != hipSuccess) return VFM_ERR_HIP;
+    if (sdev != dev) return VFM_ERR_ARG;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return VFM_ERR_HIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return VFM_OK;
+}
+
+}  // namespace
+
+extern "C" int vfm_layer_forward_noalloc(const vfm_cfg* cfg, const vfm_layer_weights* w,
+                                         const vfm_lora_table* lora, const vfm_batch* batch, float* x,
+                                         void* k_cache, void* v_cache, int64_t kv_slots, void* stream) {
+  Plan pl;
+  VFM_TRY(check_layer_contiguous(cfg, w, lora, batch, x, k_cache, v_cache, kv_slots, &pl));
+  // the batch's workspace must fit the fixed scratch array (checked on the
+  // host, before the device is touched)
+  if (layer_ws(*cfg, pl, lora, max_keys_of(batch, pl)).total > VFM_NOALLOC_SCRATCH_BYTES)
+    return VFM_ERR_WORKSPACE;
+  void* ws = nullptr;
+  VFM_TRY(scratch_of_current_device((hipStream_t)stream, &ws));
+  // nothing in the scratch array needs to start at zero: every kernel writes
+  // the workspace regions it reads in the same call (stale bytes of an
+  // earlier call are never read)
+  return layer_impl(*cfg, w, lora, batch, pl, x, k_cache, v_cache, kv_slots, KvPages{nullptr, 0, 0}, ws,
+                    VFM_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 extern "C" int vfm_layer_forward_paged(const vfm_cfg* cfg, const vfm_layer_weights* w,

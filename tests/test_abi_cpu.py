@@ -141,6 +141,8 @@ def test_binding_constants_match_header():
     defs = dict(re.findall(r"#define\s+(VFM_\w+)\s+(\d+)", src))
     for name in ("VFM_PLAN_HEADER", "VFM_ROW_TILE", "VFM_SMALL_BATCH_ROWS"):
         assert int(defs[name]) == getattr(B, name), name
+    mib = re.search(r"#define\s+VFM_NOALLOC_SCRATCH_BYTES\s+\(\(size_t\)(\d+) << 20\)", src)
+    assert mib and int(mib.group(1)) << 20 == B.VFM_NOALLOC_SCRATCH_BYTES
 
 
 def test_attach_rejects_bad_arguments_before_launching():
