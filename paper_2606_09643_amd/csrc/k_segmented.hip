@@ -143,6 +143,48 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
   }
 }
 
+// fp32 shrink: one block per (16-row group of a segmented tile, projection);
+// thread (row r, column jj) accumulates U[r, jj + 16 q] for q < rpad / 16
+// over the whole of K with 16-byte loads (the row's loads are shared by its
+// 16 threads through L1).  No LDS, no barrier.
+__global__ __launch_bounds__(256) void shrink_f32_stream_kernel(Plan pl, ShrinkArgs a) {
+  __shared__ int tslot;
+  const int tile = blockIdx.x >> 2, grp = blockIdx.x & 3, p = blockIdx.y;
+  const int t = block_tile_task(pl, tile, &tslot);
+  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE + grp * 16;
+  const int r1 = min(pl.seg_row[t] + (tile - pl.rtile_off[t] + 1) * VFM_ROW_TILE, pl.seg_row[t + 1]);
+  if (r0 >= r1) return;
+  const int r = threadIdx.x >> 4, jj = threadIdx.x & 15;
+  const int m = r0 + r;
+  const int rank = min(a.rank[t], a.rpad) & ~7;
+  const int nq = a.rpad / 16;                         // outputs per thread (2 or 4)
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (rank > 0 && m < r1) {
+    const float* xr = (const float*)a.X + (int64_t)m * a.ldx;
+    const float* At = (const float*)a.A[p][t];
+    for (int k = 0; k < a.K; k += 4) {
+      const float4 xv = *reinterpret_cast<const float4*>(xr + k);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = jj + 16 * q;
+        if (q < nq && j < rank) {
+          const float4 av = *reinterpret_cast<const float4*>(At + (int64_t)j * a.K + k);
+          acc[q] = fmaf(xv.x, av.x, acc[q]);
+          acc[q] = fmaf(xv.y, av.y, acc[q]);
+          acc[q] = fmaf(xv.z, av.z, acc[q]);
+          acc[q] = fmaf(xv.w, av.w, acc[q]);
+        }
+      }
+    }
+  }
+  if (m >= r1) return;
+  const float sc = a.scale[t];
+  float* U = (float*)a.U;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (q < nq) U[(int64_t)m * a.ldu + a.ucol[p] + jj + 16 * q] = acc[q] * sc;
+}
+
 __global__ __launch_bounds__(256) void shrink_f32_kernel(Plan pl, ShrinkArgs a) {
   // One block per (row tile, projection).  K is walked in 32-column chunks
   // staged in LDS (the tile's rows and the task's A rows); thread (row i,
@@ -414,6 +456,9 @@ hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hi
       if (a.n_proj == 1) SHR(1, 4); else if (a.n_proj == 2) SHR(2, 4); else SHR(3, 4);
     }
 #undef SHR
+  } else if (a.K % 4 == 0) {
+    dim3 grid(4 * pl.n_rtiles, a.n_proj);
+    hipLaunchKernelGGL(shrink_f32_stream_kernel, grid, dim3(256), 0, s, pl, a);
   } else {
     dim3 grid(pl.n_rtiles, a.n_proj);
     hipLaunchKernelGGL(shrink_f32_kernel, grid, dim3(256), 0, s, pl, a);

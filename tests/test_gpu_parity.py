@@ -372,12 +372,11 @@ def test_large_gemm_many_task_runs():
 def test_full_size_sampled(idx):
     """Each remaining workload at its full batch, in the bench's launch
     configuration: every layer's output on sampled requests against the
-    oracle, both sides starting each layer from the oracle's rows, and, when
-    every layer runs, those requests' head outputs.  The decoder workloads run their first two layers
-    (the kernels and launch shapes of all 32 are the same); decode also
-    checks the new K / V rows written to the cache."""
+    oracle, both sides starting each layer from the oracle's rows (parity
+    call by call, through all 24 / 32 layers), and those requests' head
+    outputs; decode also checks the new K / V rows written to the cache."""
     w = wl.WORKLOADS[idx]
-    n_layers = w.n_layers if w.family != "decoder" else 2
+    n_layers = w.n_layers
     batch = wl.draw_batch(w)
     model = R.Model(w, n_layers=n_layers)
     inp = R.Inputs(w, batch)
@@ -385,7 +384,15 @@ def test_full_size_sampled(idx):
     pb = R.make_batch(w, batch, model.heads, kv)
     fwd = R.Forward(model, pb, inp, kv)
     pl = oracle_plan(w, batch, model.heads.n_out if model.heads is not None else None)
-    reqs = pick_requests(pl, k=4 if idx == 4 else 6)
+    if idx == 4:      # the shortest prompt and a 300..512-token one at a task boundary (oracle cost)
+        lens = np.diff(pl["cu_seqlens"])
+        seg = pl["seg_req"]
+        bound = sorted({int(seg[t]) for t in range(w.n_tasks) if seg[t + 1] > seg[t]} |
+                       {int(seg[t + 1]) - 1 for t in range(w.n_tasks) if seg[t + 1] > seg[t]})
+        mid = [p for p in bound if 300 <= lens[p] <= 512] or [int(np.argsort(lens)[len(lens) // 2])]
+        reqs = [int(np.argmin(lens)), mid[0]]
+    else:
+        reqs = pick_requests(pl, k=6)
     log(f"full-size workload {idx}: T={pb.T}, {n_layers} layers, sampled plan positions {reqs}")
     x_or = as_f32(expected_embed(w, batch, inp, pl))
     set_rows(fwd.x, x_or)
