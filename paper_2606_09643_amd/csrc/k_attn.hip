@@ -202,14 +202,58 @@ __device__ __forceinline__ int pair_key(int ks, int x) {  // key of row x of sub
 
 // ---------------------------------------------------------------------------
 // Prefill attention, bf16, MFMA: one block = 64 queries of one request and
-// one head, 4 waves x 16 queries, online softmax over 64-key blocks.  K (rows
-// swizzled) and V^T (through 8x8 register transposes) of a key block are
-// staged in LDS; the next block's K / V are loaded into registers while the
-// current one is computed.  Score sub-tiles take the keys of each 32-key pair
-// in the pair_key order, so a lane's P^T keys are contiguous and each V^T
-// fragment is one 16-byte read.  Causal: a wave skips key blocks entirely
-// past its queries and masks only the block on its diagonal.
+// one head, 4 waves x 16 queries, online softmax over 64-key blocks.  K and V
+// of a key block are staged in LDS row-major, as loaded (rows swizzled); the
+// next block's K / V are loaded into registers while the current one is
+// computed.  Score sub-tiles take the keys of each 32-key pair in the
+// pair_key order, so a lane's P^T keys are contiguous; the V^T operand of
+// O^T = V^T P^T is read from the row-major V tile with gfx950's transposing
+// LDS read (ds_read_b64_tr_b16, vtr_frag), so V is never transposed in
+// registers.  Causal: a wave skips key blocks entirely past its queries and
+// masks only the block on its diagonal.
 // ---------------------------------------------------------------------------
+// V tile row-major in LDS ([64 keys][DH] bf16) with 32-byte segments
+// swizzled per row: segment s of key row r sits at s ^ vswz(r).  vswz makes
+// the transposing reads below bank-conflict free (each 32-lane half of a read
+// touches 8 rows, one 32-byte segment each, spread over all 64 banks) and is
+// a permutation within the row, so the row stores stay conflict-free too.
+template <int DH>
+__device__ __forceinline__ int vswz(int r) {
+  return DH == 128 ? ((r & 3) | (((r >> 3) & 1) << 2)) : (((r >> 1) & 1) | (((r >> 3) & 1) << 1));
+}
+// physical 16-byte chunk of logical chunk ch (head dims 8 ch .. 8 ch + 7) of row r
+template <int DH>
+__device__ __forceinline__ int vswz_chunk(int r, int ch) {
+  return (((ch >> 1) ^ vswz<DH>(r)) << 1) | (ch & 1);
+}
+// ds_read_b64_tr_b16 (gfx950): within each group of 16 lanes, lane k brings
+// the 4 consecutive 16-bit values D_k at its address and lane i receives
+// D_{4j + i/4}[i % 4] for j = 0..3 (its lane layout, checked on the device).
+// The A operand of v_mfma_f32_16x16x32_bf16 for V^T (lane l: head dim
+// 16 ds + l % 16, keys 8 (l / 16) .. + 7 of the 32-key half u) is then two
+// such reads: lane l points at key row 32 u + 8 (l / 16) + (l % 16) / 4 + 4 h
+// (h = 0, 1: keys 0..3 and 4..7), dims 16 ds + 4 (l % 4) .. + 3.  With the
+// row swizzle above the lane's segment term, vswz of that row, depends on
+// the lane only, so one base offset serves every (u, h, ds).
+template <int DH>
+__device__ __forceinline__ int vtr_lane_offset(int lane) {
+  const int g = lane >> 4, kq = lane & 15;
+  const int row = 8 * g + (kq >> 2);        // + 32 u + 4 h, which leave vswz unchanged
+  return row * DH * 2 + (vswz<DH>(row) << 5) + (kq & 3) * 8;
+}
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+template <int DH>
+__device__ __forceinline__ bf16x8 vtr_frag(const bf16* Vs, int vbase, int u, int ds) {
+  const char* p = reinterpret_cast<const char*>(Vs) + (vbase ^ (ds << 5)) + u * 32 * DH * 2;
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * DH * 2));
+  bf16x8 f;
+  __builtin_memcpy(&f, &lo, 8);
+  __builtin_memcpy(reinterpret_cast<char*>(&f) + 8, &hi, 8);
+  return f;
+}
+
 template <int DH, bool CAUSAL, bool FROM_CACHE = false>
 __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                                 int d, bf16* __restrict__ out,
@@ -219,11 +263,9 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
                                                                 int64_t kv_slots = 0, KvPages kpg = {}) {
   constexpr int KB = 64;          // keys per block step
   constexpr int CH = DH / 8;      // 16-byte chunks per key row
-  constexpr int VP = KB + 8;      // V^T row stride (bf16): 36 dwords, conflict-free 16-byte reads
-  constexpr int KPT = KB * CH / 256;          // K chunks per thread
-  constexpr int VTILES = (KB / 8) * CH;       // 8x8 V tiles per key block (<= 256)
+  constexpr int KPT = KB * CH / 256;          // K (and V) chunks per thread
   __shared__ __attribute__((aligned(16))) bf16 Ks[KB * DH];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[KB * DH];
   const int b = blockIdx.x, h = blockIdx.y;
   const int p = upper_index(pl.qblk_off, pl.n_req + 1, b);
   const int R = pl.cu_seqlens[p];
@@ -253,7 +295,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
   float m_run = NEG_BIG, l_run = 0.f;
 
   // staging registers of one key block
-  bf16x8 kr[KPT], vr[8];
+  bf16x8 kr[KPT], vr[KPT];
   // where key k's K / V row of this head starts
   auto krow = [&](int k) -> const bf16* {
     if (FROM_CACHE) return kc + ((int64_t)h * kv_slots + kv_slot(pl, kpg, p, k)) * DH;
@@ -270,13 +312,11 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
       kr[i] = bf16x8{};
       if (kb + key < NK) kr[i] = *reinterpret_cast<const bf16x8*>(krow(kb + key) + ch * 8);
     }
-    if (tid < VTILES) {
-      const int k8 = (tid / CH) * 8, d8 = (tid % CH) * 8;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        vr[e] = bf16x8{};
-        if (kb + k8 + e < NK) vr[e] = *reinterpret_cast<const bf16x8*>(vrow(kb + k8 + e) + d8);
-      }
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      vr[i] = bf16x8{};
+      if (kb + key < NK) vr[i] = *reinterpret_cast<const bf16x8*>(vrow(kb + key) + ch * 8);
     }
   };
   auto store = [&]() {
@@ -285,15 +325,10 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
       *reinterpret_cast<bf16x8*>(&Ks[key * DH + sswz<DH>(key, ch) * 8]) = kr[i];
     }
-    if (tid < VTILES) {
-      const int k8 = (tid / CH) * 8, d8 = (tid % CH) * 8;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        bf16x8 col;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) col[e] = vr[e][j];
-        *reinterpret_cast<bf16x8*>(&Vt[(d8 + j) * VP + k8]) = col;
-      }
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      *reinterpret_cast<bf16x8*>(&Vs[key * DH + vswz_chunk<DH>(key, ch) * 8]) = vr[i];
     }
   };
 
@@ -301,8 +336,8 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
   const int x = lane & 15;
   const int ke = pair_key(0, x), ko = pair_key(1, x);
   int koff_e = ke * DH, koff_o = ko * DH;
-  int voff = x * VP + 8 * g;
-  asm volatile("" : "+v"(koff_e), "+v"(koff_o), "+v"(voff));
+  const int vbase = vtr_lane_offset<DH>(lane);  // bytes, key row 8g + (x >> 2) of the tile
+  asm volatile("" : "+v"(koff_e), "+v"(koff_o));
   const int wq0 = ctx + q0 + wave * 16;           // the wave's first query position
   int lim = CAUSAL ? min(NK, ctx + qi + 1) : NK;  // keys >= lim are masked for this lane
 
@@ -343,7 +378,6 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
       float lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < DH / 16; ++i) o[i] *= alpha;
-      const bf16* vb = Vt + voff;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         f32x4 e0, e1;
@@ -356,7 +390,7 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
         const bf16x8 pf = pack8(e0, e1);
 #pragma unroll
         for (int ds = 0; ds < DH / 16; ++ds) {
-          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + ds * 16 * VP + 32 * u);
+          const bf16x8 vf = vtr_frag<DH>(Vs, vbase, u, ds);
           o[ds] = mfma16(vf, pf, o[ds]);
         }
       }
