@@ -420,11 +420,11 @@ __global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const b
 
 // ---------------------------------------------------------------------------
 // Prefill attention for requests of at most 256 tokens (bf16, MFMA).
-// One block per (request, head): K and V^T of the whole request are staged in
-// LDS once (V^T through 8x8 register transposes), then each wave takes
-// 16-query groups; with all keys resident the softmax is one pass (max,
-// exp, sum) with no rescaling.  Keys are padded to a multiple of 32 with
-// zeros and masked.
+// One block per (request, head): K and V of the whole request are staged in
+// LDS once, row-major (V^T fragments come from the transposing LDS read, as
+// in the flash kernel), then each wave takes 16-query groups; with all keys
+// resident the softmax is one pass (max, exp, sum) with no rescaling.  Keys
+// are padded to a multiple of 32 with zeros and masked.
 // ---------------------------------------------------------------------------
 template <int DH, bool CAUSAL, int NKS>
 __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
@@ -433,9 +433,8 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
   // NKS 16-key sub-tiles cover every request of the batch (NKS * 16 >= L)
   constexpr int LMAX = NKS * 16;
   constexpr int CH = DH / 8;      // 16-byte chunks per key row
-  constexpr int VP = LMAX + 8;    // V^T row stride (bf16)
   __shared__ __attribute__((aligned(16))) bf16 Ks[LMAX * DH];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[DH * VP];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[LMAX * DH];
   const int p = blockIdx.x, h = blockIdx.y;
   const int R = pl.cu_seqlens[p];
   const int L = pl.cu_seqlens[p + 1] - R;
@@ -444,45 +443,27 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
   const int64_t ld = 3 * (int64_t)d;
   const bf16* base = qkv + (int64_t)R * ld + h * DH;
 
-  // Stage K and V^T.  Every global load of a thread is issued before its
+  // Stage K and V.  Every global load of a thread is issued before its
   // first LDS store, so the block pays the load latency once.
   {
-    constexpr int KPT = (LMAX * CH + 255) / 256;  // K chunks per thread
-    bf16x8 kr[KPT];
+    constexpr int KPT = (LMAX * CH + 255) / 256;  // K (and V) chunks per thread
+    bf16x8 kr[KPT], vr[KPT];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
       kr[i] = bf16x8{};
-      if (key < L && c < LMAX * CH) kr[i] = *reinterpret_cast<const bf16x8*>(base + (int64_t)key * ld + d + ch * 8);
-    }
-    constexpr int VPT = ((LMAX / 8) * CH + 255) / 256;  // 8x8 V tiles per thread
-    bf16x8 vr[VPT][8];
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int tile = tid + 256 * i, kb = (tile / CH) * 8, db = (tile % CH) * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        vr[i][e] = bf16x8{};
-        if (kb + e < L && tile < (LMAX / 8) * CH)
-          vr[i][e] = *reinterpret_cast<const bf16x8*>(base + (int64_t)(kb + e) * ld + 2 * d + db);
+      vr[i] = bf16x8{};
+      if (key < L && c < LMAX * CH) {
+        kr[i] = *reinterpret_cast<const bf16x8*>(base + (int64_t)key * ld + d + ch * 8);
+        vr[i] = *reinterpret_cast<const bf16x8*>(base + (int64_t)key * ld + 2 * d + ch * 8);
       }
     }
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int c = tid + 256 * i, key = c / CH, ch = c % CH;
-      if (c < LMAX * CH) *reinterpret_cast<bf16x8*>(&Ks[key * DH + sswz<DH>(key, ch) * 8]) = kr[i];
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int tile = tid + 256 * i, kb = (tile / CH) * 8, db = (tile % CH) * 8;
-      if (tile < (LMAX / 8) * CH) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          bf16x8 col;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) col[e] = vr[i][e][j];
-          *reinterpret_cast<bf16x8*>(&Vt[(db + j) * VP + kb]) = col;
-        }
+      if (c < LMAX * CH) {
+        *reinterpret_cast<bf16x8*>(&Ks[key * DH + sswz<DH>(key, ch) * 8]) = kr[i];
+        *reinterpret_cast<bf16x8*>(&Vs[key * DH + vswz_chunk<DH>(key, ch) * 8]) = vr[i];
       }
     }
   }
@@ -558,9 +539,8 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     f32x4 o[DH / 16];
 #pragma unroll
     for (int i = 0; i < DH / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    int voff = (lane & 15) * VP + 8 * g;
-    asm volatile("" : "+v"(voff));
-    const bf16* vbase = Vt + voff;
+    int vbase = vtr_lane_offset<DH>(lane);
+    asm volatile("" : "+v"(vbase));
 #pragma unroll
     for (int u = 0; u < NKS / 2; ++u) {
       f32x4 e0, e1;
@@ -573,7 +553,7 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
       const bf16x8 pf = pack8(e0, e1);
 #pragma unroll
       for (int ds = 0; ds < DH / 16; ++ds) {
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vbase + ds * 16 * VP + 32 * u);
+        const bf16x8 vf = vtr_frag<DH>(Vs, vbase, u, ds);
         o[ds] = mfma16(vf, pf, o[ds]);
       }
     }
