@@ -91,8 +91,7 @@ LayerWs layer_ws(const vfm_cfg& c, const Plan& pl, const vfm_lora_table* l, int 
   w.kchunks = 0;
   if (use_skinny(c, pl)) {
     // fp32 split partials of the largest projection group
-    // (the LoRA expand adds one more slice)
-    auto zbytes = [&](int N, int K) { return (size_t)(skinny_splits(N, K) + 1) * T * N * 4; };
+    auto zbytes = [&](int N, int K) { return (size_t)skinny_splits(N, K) * T * N * 4; };
     const int n_up = c.mlp == VFM_MLP_SWIGLU ? 2 * f : f;
     const size_t zmax = std::max(std::max(zbytes(3 * d, d), zbytes(d, d)),
                                  std::max(zbytes(n_up, d), zbytes(d, f)));
@@ -410,8 +409,9 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
       VFM_TIMED(cls, launch_gemm(c.dtype, g, s));
       return VFM_OK;
     }
-    // small batch: split-K shrink + reduce, split-K GEMM into partial
-    // slices, the LoRA expand as one more slice, then the streaming sum
+    // small batch: split-K shrink, split-K GEMM into partial slices, then
+    // the streaming sum, which also reduces the shrink partials and adds
+    // each row's LoRA difference
     const bool sw = epi == EPI_SWIGLU;
     const int nz = sw ? 2 * N : N;
     SkinnyArgs k = {};
@@ -422,35 +422,31 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
     fa.Z = Z; fa.nslices = k.nsplit; fa.M = T; fa.N = N; fa.epi = epi; fa.bias = bias;
     fa.out = out; fa.ldo = ldo;
     if (any) {
+      // the split shrink writes fp32 partials; the finalize pass sums them
+      // into each row's U and adds U B_t^T to the row's columns
       ShrinkSplitArgs a = {};
       a.X = X; a.ldx = K; a.K = K; a.P = P; a.ldp = ldu; a.rpad = rpad;
       a.kchunks = shrink_chunks(K); a.rank = lora->rank;
-      LoraReduceArgs ra = {};
-      ra.P = P; ra.ldp = ldu; ra.kchunks = a.kchunks; ra.U = (bf16*)U; ra.ldu = ldu;
-      ra.rpad = rpad; ra.scale = lora->scale;
       for (int p : projs) {
         if (!has(p)) continue;
         a.A[a.n_proj] = lora->A[p];
         a.ucol[a.n_proj] = p * rpad;
-        ra.ucol[a.n_proj] = p * rpad;
         a.n_proj++;
       }
-      ra.n_slots = a.n_proj;
       VFM_TIMED(VFM_PROF_SHRINK, launch_shrink_split(pl, a, s));
-      VFM_TIMED(VFM_PROF_SHRINK, launch_lora_reduce(pl, ra, s));
-      ExpandZArgs ea = {};
-      ea.U = (const bf16*)U; ea.ldu = ldu;
+      FinLora& fl = fa.lora;
+      fl.enabled = 1;
+      fl.P = P; fl.ldp = ldu; fl.cstride = (int64_t)T * ldu; fl.kchunks = a.kchunks;
       int i = 0;
       for (int p : projs) {
-        if (has(p)) ea.B[i] = lora->B[p];
-        ea.ucol[i] = p * rpad;
+        fl.ucol[i] = p * rpad;
+        fl.B[i] = has(p) ? lora->B[p] : nullptr;
         ++i;
       }
-      ea.slot_width = sw ? N : slot_width;
-      ea.rank = lora->rank; ea.max_rank = lora->max_rank;
-      ea.L = Z + (size_t)k.nsplit * T * nz; ea.NZ = nz;
-      VFM_TIMED(VFM_PROF_SHRINK, launch_lora_expand_z(pl, ea, s));
-      fa.nslices = k.nsplit + 1;
+      fl.n_slots = i; fl.rpad = rpad;
+      fl.slot_width = sw ? N : slot_width;
+      fl.scale = lora->scale; fl.rank = lora->rank; fl.max_rank = lora->max_rank;
+      fl.row_task = pl.row_task;
     }
     const int pi = prof_begin(cls, s);
     hipError_t e = launch_gemm_skinny(k, s);

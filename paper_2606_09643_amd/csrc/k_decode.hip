@@ -14,12 +14,11 @@
 //   shrink_split   P[c, m, slot + j] = sum over K chunk c of X[m, k] A_t[j, k]:
 //                  one block per (task row tile, K chunk), so a task's A
 //                  factors are read once, by many blocks at a time.
-//   lora_reduce    U = bf16(s_t * sum_c P), one pass over the partials
-//   lora_expand_z  one more partial slice Z[ns] = U B_t^T: one block per
-//                  (task row tile, 256 columns) on the MFMA, so B_t is read
-//                  once per column for all of the task's rows in the tile
-//   finalize       y = sum of the slices + bias, then the activation or
-//                  residual epilogue, streamed one thread per 4 outputs.
+//   finalize       per row: U = bf16(s_t * sum_c P) rebuilt in LDS, then
+//                  y = sum of the slices + U B_t^T + bias and the activation
+//                  or residual epilogue, streamed one thread per 4 outputs
+//                  (B_t rows read straight from the task's factor: the
+//                  per-task adapter gather).
 #include <algorithm>
 
 #include "vfm_internal.h"
@@ -255,123 +254,35 @@ __global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitA
 }
 
 // ---------------------------------------------------------------------------
-// LoRA reduce: U[m, ucol[q] + j] = bf16(s_t * sum_c P[c, m, ucol[q] + j])
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void lora_reduce_kernel(Plan pl, LoraReduceArgs a) {
-  const int per_row = a.n_slots * a.rpad / 4;  // 4-column groups per row
-  const int g = blockIdx.x * 256 + threadIdx.x;
-  if (g >= pl.T * per_row) return;
-  const int m = g / per_row, e = g % per_row;
-  const int q = e / (a.rpad / 4), j = (e % (a.rpad / 4)) * 4;
-  const float sc = a.scale[pl.row_task[m]];
-  const float* P = a.P + (int64_t)m * a.ldp + a.ucol[q] + j;
-  const int64_t cs = (int64_t)pl.T * a.ldp;
-  float4 s4[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) s4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-  int c = 0;
-  for (; c + 4 <= a.kchunks; c += 4) {
-    float4 v[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = *reinterpret_cast<const float4*>(P + (c + i) * cs);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      s4[i].x += v[i].x; s4[i].y += v[i].y; s4[i].z += v[i].z; s4[i].w += v[i].w;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < 3; ++i) {  // the last kchunks mod 4 chunks
-    if (c + i >= a.kchunks) break;
-    const float4 v = *reinterpret_cast<const float4*>(P + (c + i) * cs);
-    s4[i].x += v.x; s4[i].y += v.y; s4[i].z += v.z; s4[i].w += v.w;
-  }
-  const float r4[4] = {(s4[0].x + s4[1].x) + (s4[2].x + s4[3].x), (s4[0].y + s4[1].y) + (s4[2].y + s4[3].y),
-                       (s4[0].z + s4[1].z) + (s4[2].z + s4[3].z), (s4[0].w + s4[1].w) + (s4[2].w + s4[3].w)};
-  bf16x4 o;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) o[i] = (bf16)(r4[i] * sc);
-  *reinterpret_cast<bf16x4*>(a.U + (int64_t)m * a.ldu + a.ucol[q] + j) = o;
-}
-
-// ---------------------------------------------------------------------------
-// LoRA expand into one more partial slice: L[m, n] = U[m, slot(n)] . B_t[n', :r]
-// for every column n of Z (SwiGLU: gate columns [0, N), up [N, 2N)); zero
-// where the task has no adapter for the slot.  Block = one task row tile
-// (<= 64 rows) x 256 columns; wave w owns 64 columns as four 16-column
-// blocks.  B_t rows feed the MFMA A slot, U rows the B slot, so each lane
-// ends with 4 consecutive columns of one row.  B_t is read once per (tile,
-// column): the per-task adapter gather.
-// ---------------------------------------------------------------------------
-constexpr int EXP_COLS = 256;
-
-__global__ __launch_bounds__(256) void lora_expand_z_kernel(Plan pl, ExpandZArgs a) {
-  __shared__ int s_task;
-  const int tile = blockIdx.x;
-  const int t = block_tile_task(pl, tile, &s_task);
-  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
-  const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int cw = blockIdx.y * EXP_COLS + wave * 64;   // the wave's first Z column
-  if (cw >= a.NZ) return;
-  const int slot = min(cw / a.slot_width, 2);
-  const int brow0 = cw - slot * a.slot_width;
-  const int r = min(a.rank[t], a.max_rank);
-  const bool on = r > 0 && a.B[slot] != nullptr;
-  // the task's B rows of the wave's 64 columns, all of the rank (<= 64)
-  bf16x8 bf[2][4];
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int cb = 0; cb < 4; ++cb) bf[kk][cb] = bf16x8{};
-  const bf16* Bt = on ? (const bf16*)a.B[slot][t] : nullptr;
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int kof = kk * 32 + 8 * (lane >> 4);
-    if (!on || kof >= r) continue;
-#pragma unroll
-    for (int cb = 0; cb < 4; ++cb)
-      bf[kk][cb] = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)(brow0 + cb * 16 + (lane & 15)) * r + kof);
-  }
-  for (int rb = r0; rb < r1; rb += 16) {
-    const int m = rb + (lane & 15);
-    f32x4 acc[4];
-#pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (on) {
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        if (kk * 32 >= r) break;
-        const int kof = kk * 32 + 8 * (lane >> 4);
-        bf16x8 uf = bf16x8{};
-        if (kof < r && m < r1) uf = *reinterpret_cast<const bf16x8*>(a.U + (int64_t)m * a.ldu + a.ucol[slot] + kof);
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[cb] = mfma16(bf[kk][cb], uf, acc[cb]);
-      }
-    }
-    if (m < r1) {
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        *reinterpret_cast<float4*>(a.L + (int64_t)m * a.NZ + cw + cb * 16 + 4 * (lane >> 4)) =
-            make_float4(acc[cb][0], acc[cb][1], acc[cb][2], acc[cb][3]);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Finalize: sum of the partial slices (fixed order) + bias + epilogue, one
-// thread per row and 4 output columns; every load is independent of the
+// Finalize: sum of the partial slices (fixed order) + the row's LoRA
+// difference (fin_lora_delta, from the split shrink's partials) + bias +
+// epilogue.  Block (column range, row): the row's U is rebuilt once in LDS,
+// then each thread takes 4 output columns; every load is independent of the
 // others, so the kernel streams the partials.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
-  const int per_row = a.N / 4;
-  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (g >= (int64_t)a.M * per_row) return;
-  const int m = (int)(g / per_row), n = (int)(g % per_row) * 4;
+  __shared__ float Us[3 * VFM_MAX_RANK];
+  const int m = blockIdx.y;
+  int t = 0, r = 0;
+  if (a.lora.enabled) {                       // block-uniform
+    t = a.lora.row_task[m];
+    r = fin_lora_u(a.lora, m, Us);
+  }
+  const int n = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (n >= a.N) return;
   const bool swiglu = a.epi == EPI_SWIGLU;
   const int nz = swiglu ? 2 * a.N : a.N;   // columns of Z
   const int64_t zs = (int64_t)a.M * nz;
   const float* z = a.Z + (int64_t)m * nz + n;
   float4 v = sum_slices(z, zs, a.nslices);
+  if (a.lora.enabled) {
+    if (swiglu) {
+      add4(v, fin_lora_delta(a.lora, t, r, 0, n, Us));
+    } else {
+      const int slot = min(n / a.lora.slot_width, 2);
+      add4(v, fin_lora_delta(a.lora, t, r, slot, n - slot * a.lora.slot_width, Us));
+    }
+  }
   if (a.bias && !swiglu) {
     const bf16x4 bv = *reinterpret_cast<const bf16x4*>((const bf16*)a.bias + n);
     v.x += (float)bv[0]; v.y += (float)bv[1]; v.z += (float)bv[2]; v.w += (float)bv[3];
@@ -386,7 +297,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   const float g4[4] = {v.x, v.y, v.z, v.w};
   float u4[4] = {0.f, 0.f, 0.f, 0.f};
   if (swiglu) {
-    const float4 u = sum_slices(z + a.N, zs, a.nslices);
+    float4 u = sum_slices(z + a.N, zs, a.nslices);
+    if (a.lora.enabled) add4(u, fin_lora_delta(a.lora, t, r, 1, n, Us));
     u4[0] = u.x; u4[1] = u.y; u4[2] = u.z; u4[3] = u.w;
   }
   bf16x4 o;
@@ -457,23 +369,9 @@ hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a0, hipStr
   return hipGetLastError();
 }
 
-hipError_t launch_lora_reduce(const Plan& pl, const LoraReduceArgs& a, hipStream_t s) {
-  const int64_t n = (int64_t)pl.T * a.n_slots * a.rpad / 4;
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(lora_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pl, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_lora_expand_z(const Plan& pl, const ExpandZArgs& a, hipStream_t s) {
-  if (pl.n_rtiles == 0) return hipSuccess;
-  dim3 grid(pl.n_rtiles, (a.NZ + EXP_COLS - 1) / EXP_COLS);
-  hipLaunchKernelGGL(lora_expand_z_kernel, grid, dim3(256), 0, s, pl, a);
-  return hipGetLastError();
-}
-
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s) {
-  const int64_t n = (int64_t)a.M * (a.N / 4);
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  if (a.M == 0 || a.N == 0) return hipSuccess;
+  const int per_row = a.N / 4;
+  hipLaunchKernelGGL(finalize_kernel, dim3((per_row + 255) / 256, a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }

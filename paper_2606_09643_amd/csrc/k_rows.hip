@@ -172,10 +172,16 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
                                                             const T* __restrict__ b, int kind, float eps,
                                                             T* __restrict__ h) {
   __shared__ float red[2][4];
+  __shared__ float Us[3 * VFM_MAX_RANK];
   const int row = blockIdx.x, tid = threadIdx.x;
   const int nch = a.N >> 2;
   const int64_t zs = (int64_t)a.M * a.N;
   float* xr = (float*)a.out + (int64_t)row * a.ldo;
+  int t = 0, r = 0;
+  if (a.lora.enabled) {                       // block-uniform
+    t = a.lora.row_task[row];
+    r = fin_lora_u(a.lora, row, Us);
+  }
   float4 v[MAXC];
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
@@ -183,6 +189,10 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
     v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (c < nch) {
       float4 s4 = sum_slices(a.Z + (int64_t)row * a.N + 4 * c, zs, a.nslices);
+      if (a.lora.enabled) {
+        const int slot = min(4 * c / a.lora.slot_width, 2);
+        add4(s4, fin_lora_delta(a.lora, t, r, slot, 4 * c - slot * a.lora.slot_width, Us));
+      }
       if (a.bias) {
         const bf16x4 bv = *reinterpret_cast<const bf16x4*>((const bf16*)a.bias + 4 * c);
         s4.x += (float)bv[0]; s4.y += (float)bv[1]; s4.z += (float)bv[2]; s4.w += (float)bv[3];

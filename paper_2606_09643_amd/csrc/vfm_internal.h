@@ -240,35 +240,79 @@ struct ShrinkSplitArgs {
 hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a, hipStream_t s);
 int shrink_chunks(int K);
 
-// U[m, ucol[q] + j] = bf16(scale_t * sum_c P[c, m, ucol[q] + j]), q < n_slots, j < rpad.
-struct LoraReduceArgs {
-  const float* P; int ldp; int kchunks;
-  bf16* U; int ldu;
+// Per-task LoRA of a small-batch projection group, applied by the finalize
+// pass: for row m of task t, U = bf16(s_t * sum_c P[c, m, ucol[i] + j]) (the
+// split shrink's partials, four running sums by chunk index mod 4, added
+// pairwise) and
+// column n of slot i gains sum_{j < r_t} U[i][j] B_{t,i}[n', j], n' = the
+// column within its slot (SwiGLU: gate columns slot 0, up columns slot 1).
+struct FinLora {
+  int enabled;
+  const float* P; int ldp; int64_t cstride; int kchunks;   // P[c, m, col] at c * cstride + m * ldp + col
   int ucol[3]; int n_slots; int rpad;
-  const float* scale;
-};
-hipError_t launch_lora_reduce(const Plan& pl, const LoraReduceArgs& a, hipStream_t s);
-
-// Per-task LoRA expand into a partial slice L [M, NZ] (fp32, every entry
-// written): L[m, n] = U[m, ucol[slot] ..] . B_{t,slot}[n - slot * slot_width, :r_t]
-// with slot = n / slot_width (a multiple of 64; SwiGLU: slot_width = N, so
-// gate columns are slot 0 and up columns slot 1).
-struct ExpandZArgs {
-  const bf16* U; int ldu; int ucol[3];
   const void* const* B[3]; int slot_width;
-  const int32_t* rank; int max_rank;
-  float* L; int NZ;
+  const float* scale; const int32_t* rank; int max_rank;
+  const int32_t* row_task;
 };
-hipError_t launch_lora_expand_z(const Plan& pl, const ExpandZArgs& a, hipStream_t s);
 
 // Sum of nslices partial slices Z[s] ([M, N], SwiGLU [M, 2N]: gate then up
-// columns) in a fixed order, plus bias, and the epilogue of GemmEpi.
+// columns) in a fixed order, plus bias, plus the fused LoRA difference, and
+// the epilogue of GemmEpi.
 struct FinalizeArgs {
   const float* Z; int nslices; int M; int N; int epi;   // epi: GemmEpi
   const void* bias;
   void* out; int ldo;
+  FinLora lora;
 };
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
+
+// The fused LoRA of the finalize pass for row m.  Every thread of the block
+// calls fin_lora_u: it fills Us[i * rpad + j] for the slots with adapters
+// and j < r (r = the row's task rank, returned) and ends with a barrier.
+__device__ inline int fin_lora_u(const FinLora& L, int m, float* Us) {
+  const int t = L.row_task[m];
+  const int r = min(L.rank[t], L.max_rank) & ~7;
+  const float sc = L.scale[t];
+  for (int q = threadIdx.x; q < L.n_slots * L.rpad; q += blockDim.x) {
+    const int i = q / L.rpad, j = q % L.rpad;
+    if (j >= r || L.B[i] == nullptr) continue;
+    const float* p = L.P + (int64_t)m * L.ldp + L.ucol[i] + j;
+    float s4[4] = {0.f, 0.f, 0.f, 0.f};
+    // 8 independent loads in flight per batch (chunks past the end add 0),
+    // summed in chunk order into the running sum of chunk index mod 4
+    for (int c0 = 0; c0 < L.kchunks; c0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = c0 + e < L.kchunks ? p[(c0 + e) * L.cstride] : 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s4[e & 3] += v[e];
+    }
+    Us[q] = (float)(bf16)(((s4[0] + s4[1]) + (s4[2] + s4[3])) * sc);
+  }
+  __syncthreads();
+  return r;
+}
+
+// LoRA difference of 4 consecutive columns of slot i of row m (task t, rank
+// r): rows brow .. brow + 3 of B_{t,i}, a fixed-order fp32 sum over the rank.
+__device__ inline float4 fin_lora_delta(const FinLora& L, int t, int r, int i, int brow, const float* Us) {
+  float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (r <= 0 || L.B[i] == nullptr) return d;
+  const bf16* Bt = (const bf16*)L.B[i][t] + (int64_t)brow * r;
+  const float* u = Us + i * L.rpad;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int j0 = 0; j0 < r; j0 += 8) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)c * r + j0);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[c] = fmaf(u[j0 + e], (float)bv[e], acc[c]);
+    }
+  }
+  d.x = acc[0]; d.y = acc[1]; d.z = acc[2]; d.w = acc[3];
+  return d;
+}
+
 // Residual finalize fused with the next pre-norm (small batches): per row,
 // x += sum of the slices + bias (exactly as launch_finalize with EPI_RESID),
 // then h = Norm(x) as launch_norm.
