@@ -759,6 +759,40 @@ def test_mixed_step_over_cache(ctx_long, layout):
         # "-chunked": request 3 is a 40-row prompt chunk after its ctx cached tokens
         seq_len = np.array([70, 1, 33, 40 if "chunked" in layout else 1, 1], np.int32)
         ctx = np.array([0, 63, 0, ctx_long, 1100], np.int32)
+    worst = _run_mixed_step(w, task_id, seq_len, ctx, layout)
+    assert worst < tol(w)
+
+
+# A 1024-wide decoder with 16 heads of 64 dims (the head_dim-64 kernels);
+# the 7B one has 32 heads of 128.
+DECODER_DH64 = dict(d=1024, n_heads=16, head_dim=64, d_ff=2816)
+
+
+@pytest.mark.parametrize("dh,layout", [(128, "paged"), (128, "contiguous"), (64, "paged"), (64, "contiguous")])
+def test_long_prompt_chunks_over_cache(dh, layout):
+    """Chunked prefill in the cache-reading flash kernel away from its easy
+    case: a 170-row prompt chunk after 333 cached tokens (three 64-query
+    blocks, so q0 > 0, and a context that is not a multiple of 64) and a
+    65-row chunk after 100, next to a 300-row prompt (so the first pass is
+    the flash kernel, not the short one) and a decode row at ctx 1100; head
+    dims 128 and 64, pages of 64 in random order or the contiguous cache.
+    Every row against the oracle with those cached keys, and every new K /
+    V row in its slots."""
+    w = wl.WORKLOADS[4]
+    if dh == 64:
+        w = w.replace(**DECODER_DH64)
+    task_id = np.array([3, 0, 63, 3, 5], np.int32)
+    seq_len = np.array([300, 170, 1, 65, 2], np.int32)
+    ctx = np.array([0, 333, 1100, 100, 0], np.int32)
+    worst = _run_mixed_step(w, task_id, seq_len, ctx, layout)
+    assert worst < tol(w)
+
+
+def _run_mixed_step(w, task_id, seq_len, ctx, layout):
+    """One mixed (or, for "causal-paged", prompts-only causal) step of one
+    decoder layer over a paged or contiguous cache holding seeded K / V;
+    checks every new K / V row and returns the worst row error of the
+    layer's output against the oracle."""
     batch = wl.Batch(task_id, seq_len, ctx)
     model = R.Model(w, n_layers=1, b_std=0.1)
     inp = R.Inputs(w, batch)
@@ -815,7 +849,7 @@ def test_mixed_step_over_cache(ctx_long, layout):
         v_new = np64(_page_rows(vp, table, i, c + L, page))[c:]
         assert O.row_rel_error(k_new, k) < tol(w) and O.row_rel_error(v_new, v) < tol(w)
     log(f"  max rel err {worst:.3e}")
-    assert worst < tol(w)
+    return worst
 
 
 @pytest.mark.parametrize("idx,seed", [(1, 0), (1, 1), (1, 2), (2, 3), (2, 4), (3, 5), (2, 6)])
