@@ -52,8 +52,8 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
   // zero page); each wave's activation rows go through a register ring of
   // the same depth, so NST - 1 chunks are in flight while one is consumed.
   // LDS rows are 128 B with chunk swizzle kc ^ ((row >> 1) & 7).
-  constexpr int NST = 4;
   constexpr int AR = NP * NSUB * 16;            // A rows per chunk
+  constexpr int NST = 4;
   constexpr int ARND = AR * 8 / 256;            // 16-byte pieces per thread and chunk
   constexpr int GRP = ARND + 2;                 // loads per lane and chunk
   // one LDS object (the task slot sits past the ring): with a second one the

@@ -269,7 +269,7 @@ hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
 // The fused LoRA of the finalize pass for row m.  Every thread of the block
 // calls fin_lora_u: it fills Us[i * rpad + j] for the slots with adapters
 // and j < r (r = the row's task rank, returned) and ends with a barrier.
-__device__ inline int fin_lora_u(const FinLora& L, int m, float* Us) {
+__device__ __forceinline__ int fin_lora_u(const FinLora& L, int m, float* Us) {
   const int t = L.row_task[m];
   const int r = min(L.rank[t], L.max_rank) & ~7;
   const float sc = L.scale[t];
@@ -295,16 +295,19 @@ __device__ inline int fin_lora_u(const FinLora& L, int m, float* Us) {
 
 // LoRA difference of 4 consecutive columns of slot i of row m (task t, rank
 // r): rows brow .. brow + 3 of B_{t,i}, a fixed-order fp32 sum over the rank.
-__device__ inline float4 fin_lora_delta(const FinLora& L, int t, int r, int i, int brow, const float* Us) {
+__device__ __forceinline__ float4 fin_lora_delta(const FinLora& L, int t, int r, int i, int brow, const float* Us) {
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
   if (r <= 0 || L.B[i] == nullptr) return d;
+  // B_t comes from a device pointer table: read it as global memory, not
+  // through generic (flat) addressing
+  typedef const bf16x8 __attribute__((address_space(1))) gbf16x8;
   const bf16* Bt = (const bf16*)L.B[i][t] + (int64_t)brow * r;
   const float* u = Us + i * L.rpad;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int j0 = 0; j0 < r; j0 += 8) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(Bt + (int64_t)c * r + j0);
+      const bf16x8 bv = *(gbf16x8*)(Bt + (int64_t)c * r + j0);
 #pragma unroll
       for (int e = 0; e < 8; ++e) acc[c] = fmaf(u[j0 + e], (float)bv[e], acc[c]);
     }
