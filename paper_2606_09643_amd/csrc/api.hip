@@ -382,6 +382,7 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
         ShrinkArgs a = {};
         a.X = X; a.ldx = K; a.K = K; a.U = U; a.ldu = ldu; a.rpad = rpad;
         a.rank = lora->rank; a.scale = lora->scale;
+        a.nsub = std::min(std::max(1, (lora->max_rank + 15) / 16), rpad / 16);
         for (int p : projs) {
           if (!has(p)) continue;
           a.A[a.n_proj] = lora->A[p];
@@ -523,6 +524,7 @@ extern "C" int vfm_lora_apply(int32_t dtype, int32_t proj, int32_t d_in, int32_t
   ShrinkArgs a = {};
   a.X = x; a.ldx = d_in; a.K = d_in; a.U = workspace; a.ldu = rpad; a.rpad = rpad;
   a.rank = lora->rank; a.scale = lora->scale;
+  a.nsub = std::min(std::max(1, (lora->max_rank + 15) / 16), rpad / 16);
   a.A[0] = lora->A[proj]; a.ucol[0] = 0; a.n_proj = 1;
   VFM_HIP(launch_lora_shrink(dtype, pl, a, s));
   ExpandArgs e = {};

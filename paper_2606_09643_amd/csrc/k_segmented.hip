@@ -51,20 +51,22 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
   // 64-column chunks fed by global_load_lds (rows past the rank come from a
   // zero page); each wave's activation rows go through a register ring of
   // the same depth, so NST - 1 chunks are in flight while one is consumed.
-  // LDS rows are 128 B with chunk swizzle kc ^ ((row >> 1) & 7).
-  constexpr int AR = NP * NSUB * 16;            // A rows per chunk
+  // LDS rows are 128 B with chunk swizzle kc ^ ((row >> 1) & 7).  Only the
+  // NSUB 16-row sub-tiles that the largest rank reaches are computed.
+  constexpr int AR = NP * NSUB * 16;            // A rows the MFMAs read per chunk
+  constexpr int ARD = (AR + 31) / 32 * 32;      // rows fetched (one block pass moves 32)
   constexpr int NST = 4;
-  constexpr int ARND = AR * 8 / 256;            // 16-byte pieces per thread and chunk
+  constexpr int ARND = ARD / 32;                // 16-byte pieces per thread and chunk
   constexpr int GRP = ARND + 2;                 // loads per lane and chunk
   // one LDS object (the task slot sits past the ring): with a second one the
   // compiler would wait for the ring's DMA before every fragment read
-  __shared__ __attribute__((aligned(16))) bf16 As[NST][AR * 64 + 8];
+  __shared__ __attribute__((aligned(16))) bf16 As[NST][ARD * 64 + 8];
   const int tile = blockIdx.x;
-  const int t = block_tile_task(pl, tile, reinterpret_cast<int*>(&As[NST - 1][AR * 64]));
+  const int t = block_tile_task(pl, tile, reinterpret_cast<int*>(&As[NST - 1][ARD * 64]));
   const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
   const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rank = min(a.rank[t], a.rpad) & ~7;
+  const int rank = min(a.rank[t], NSUB * 16) & ~7;
   const float sc = a.scale[t];
   const bf16* X = (const bf16*)a.X;
   bf16* U = (bf16*)a.U;
@@ -82,7 +84,7 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
     for (int i = 0; i < ARND; ++i) {
       const int row = prow0 + i * 32;                     // row = (pp*NSUB + s2)*16 + j
       const int pp = row / (NSUB * 16), j = row % (NSUB * 16);
-      asrc[i] = j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
+      asrc[i] = row < AR && j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
     }
     // rows past the tile's end read its last row (results discarded)
     const bf16* xrow = X + (int64_t)min(m, r1 - 1) * a.ldx + 8 * (lane >> 4);
@@ -140,6 +142,10 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
         for (int i = 0; i < 4; ++i) o[i] = (bf16)(acc[pp][s2][i] * sc);
         *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[pp] + s2 * 16 + 4 * (lane >> 4)) = o;
       }
+    // the slot's columns past the computed sub-tiles (past every task's rank)
+    for (int pp = 0; pp < NP; ++pp)
+      for (int s2 = NSUB; s2 < a.rpad / 16; ++s2)
+        *reinterpret_cast<bf16x4*>(U + (int64_t)m * a.ldu + a.ucol[pp] + s2 * 16 + 4 * (lane >> 4)) = bf16x4{};
   }
 }
 
@@ -449,12 +455,14 @@ hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hi
   if (pl.n_rtiles == 0 || a.n_proj == 0) return hipSuccess;
   if (dtype == VFM_BF16) {
     dim3 grid(pl.n_rtiles);
+    // sub-tiles the table's ranks need: 1 (rank <= 16), 2 (<= 32) or 4
+    const int ns = a.nsub <= 1 ? 1 : (a.nsub == 2 ? 2 : 4);
 #define SHR(NP_, NS_) hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
-    if (a.rpad == 32) {
-      if (a.n_proj == 1) SHR(1, 2); else if (a.n_proj == 2) SHR(2, 2); else SHR(3, 2);
-    } else {
-      if (a.n_proj == 1) SHR(1, 4); else if (a.n_proj == 2) SHR(2, 4); else SHR(3, 4);
-    }
+#define SHR_NP(NS_) do { if (a.n_proj == 1) SHR(1, NS_); else if (a.n_proj == 2) SHR(2, NS_); else SHR(3, NS_); } while (0)
+    if (ns == 1) SHR_NP(1);
+    else if (ns == 2) SHR_NP(2);
+    else SHR_NP(4);
+#undef SHR_NP
 #undef SHR
   } else if (a.K % 4 == 0) {
     dim3 grid(4 * pl.n_rtiles, a.n_proj);

@@ -168,10 +168,12 @@ hipError_t launch_norm(int dtype, const float* x, int T, int d, const void* g, c
 
 // Segmented LoRA shrink: U[m, ucol[p] + j] = scale_t * sum_k X[m,k] A_{t,p}[j,k]
 // for j < rank_t, zero for rank_t <= j < rpad; p over n_proj projections.
+// nsub: 16-column sub-tiles worth computing, ceil(max_rank / 16) <= rpad / 16
+// (columns past them are written as zeros).
 struct ShrinkArgs {
   const void* X; int ldx; int K;
   const void* const* A[3]; int ucol[3]; int n_proj;
-  void* U; int ldu; int rpad;
+  void* U; int ldu; int rpad; int nsub;
   const int32_t* rank; const float* scale;
 };
 hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s);
