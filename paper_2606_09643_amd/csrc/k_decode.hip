@@ -305,7 +305,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     float y = g4[c];
-    if (swiglu) y = y / (1.f + __expf(-y)) * u4[c];
+    if (swiglu) y = silu_fast(y) * u4[c];
     else if (a.epi == EPI_GELU) y = gelu_fast(y);
     o[c] = (bf16)y;
   }

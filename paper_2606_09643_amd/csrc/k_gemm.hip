@@ -40,7 +40,7 @@ __device__ __forceinline__ int swz(int row, int kc) { return kc ^ swz_bits(row);
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.f + erff(v * 0.70710678118654752440f));
 }
-__device__ __forceinline__ float silu_f(float v) { return v / (1.f + expf(-v)); }
+__device__ __forceinline__ float silu_exact(float v) { return v / (1.f + expf(-v)); }  // fp32 outputs
 
 __device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -123,7 +123,7 @@ __device__ __forceinline__ void epilogue_frags(const GemmArgs& a, int wrow0, int
         if (j >= a.N) continue;
         bf16x4 o;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) o[r] = (bf16)(silu_f(acc[mi][ni][r]) * acc[mi][ni + 1][r]);
+        for (int r = 0; r < 4; ++r) o[r] = (bf16)(silu_fast(acc[mi][ni][r]) * acc[mi][ni + 1][r]);
         *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + j) = o;
       }
     }
@@ -220,7 +220,7 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
           const int j = (sub >> 1) * 16 + 4 * g;     // tile column of the lane's 4 values
           bf16x4 o;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = (bf16)(silu_f(acc[mi][ni][e]) * acc[mi][ni + 1][e]);
+          for (int e = 0; e < 4; ++e) o[e] = (bf16)(silu_fast(acc[mi][ni][e]) * acc[mi][ni + 1][e]);
           *reinterpret_cast<bf16x4*>(T + r * NC + lds_chunk<QR>(r, j >> 3) * 8 + (j & 4)) = o;
         }
       }
@@ -833,7 +833,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       v[j] = acc[i][j] + (bias ? bias[n + j] : 0.f);
-      if (SWIGLU) v[j] = silu_f(acc[i][j]) * acc2[i][j];
+      if (SWIGLU) v[j] = silu_exact(acc[i][j]) * acc2[i][j];
       else if (EPI == EPI_GELU) v[j] = gelu_erf(v[j]);
     }
     float* dst = (float*)a.out + (int64_t)m * a.ldo + n;

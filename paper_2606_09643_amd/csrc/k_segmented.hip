@@ -36,33 +36,27 @@ typedef const void __attribute__((address_space(1)))* gptr_t;
 typedef void __attribute__((address_space(3)))* lptr_t;
 __device__ __attribute__((aligned(16))) bf16 g_seg_zero[8];  // zero-initialised at load
 
-// A 16-byte global load the compiler does not track; the kernel's own vmcnt
-// waits cover it (loads complete in issue order).  Without this the
-// compiler waits for every outstanding load at the loop's back-edge.
-__device__ __forceinline__ void gload16_untracked(bf16x8& dst, const bf16* p) {
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(p) : "memory");
-}
-
 template <int NP, int NSUB>
 __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
   // One block per 64-row tile of one task; wave w owns 16 rows and every
-  // projection of the group, so each row is read once for all of them.  The
-  // task's A rows (shared by the 4 waves) go through an LDS ring of NST
-  // 64-column chunks fed by global_load_lds (rows past the rank come from a
-  // zero page); each wave's activation rows go through a register ring of
-  // the same depth, so NST - 1 chunks are in flight while one is consumed.
-  // LDS rows are 128 B with chunk swizzle kc ^ ((row >> 1) & 7).  Only the
-  // NSUB 16-row sub-tiles that the largest rank reaches are computed.
+  // projection of the group, so each row is read once for all of them.  Each
+  // 64-column chunk of the task's A rows (shared by the 4 waves) and of the
+  // tile's 64 activation rows goes through an LDS ring of NST stages fed by
+  // global_load_lds: every wave-wide load moves 8 whole 128-byte rows, and
+  // NST - 1 chunks are in flight while one is consumed.  A rows past the rank
+  // come from a zero page; only the NSUB 16-row sub-tiles that the largest
+  // rank reaches are computed.  LDS rows are 128 B with chunk swizzle
+  // kc ^ ((row >> 1) & 7); a stage holds ARD A rows, then the 64 X rows.
   constexpr int AR = NP * NSUB * 16;            // A rows the MFMAs read per chunk
-  constexpr int ARD = (AR + 31) / 32 * 32;      // rows fetched (one block pass moves 32)
+  constexpr int ARD = (AR + 31) / 32 * 32;      // A rows fetched (one block pass moves 32)
+  constexpr int SR = ARD + VFM_ROW_TILE;        // LDS rows per stage
   constexpr int NST = 4;
-  constexpr int ARND = ARD / 32;                // 16-byte pieces per thread and chunk
-  constexpr int GRP = ARND + 2;                 // loads per lane and chunk
+  constexpr int ND = SR / 32;                   // 16-byte pieces per thread and chunk
   // one LDS object (the task slot sits past the ring): with a second one the
   // compiler would wait for the ring's DMA before every fragment read
-  __shared__ __attribute__((aligned(16))) bf16 As[NST][ARD * 64 + 8];
+  __shared__ __attribute__((aligned(16))) bf16 As[NST][SR * 64 + 8];
   const int tile = blockIdx.x;
-  const int t = block_tile_task(pl, tile, reinterpret_cast<int*>(&As[NST - 1][ARD * 64]));
+  const int t = block_tile_task(pl, tile, reinterpret_cast<int*>(&As[NST - 1][SR * 64]));
   const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
   const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -77,30 +71,29 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
 #pragma unroll
     for (int s2 = 0; s2 < NSUB; ++s2) acc[pp][s2] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (rank > 0) {   // block-uniform
-    const bf16* asrc[ARND];
+    const bf16* src0[ND];
     const int prow0 = wave * 8 + (lane >> 3);
     const int kcl = (lane & 7) ^ ((prow0 >> 1) & 7);   // same for prow0 + 32 i
 #pragma unroll
-    for (int i = 0; i < ARND; ++i) {
-      const int row = prow0 + i * 32;                     // row = (pp*NSUB + s2)*16 + j
-      const int pp = row / (NSUB * 16), j = row % (NSUB * 16);
-      asrc[i] = row < AR && j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
+    for (int i = 0; i < ND; ++i) {
+      const int row = prow0 + i * 32;
+      if (row < ARD) {                                  // row = (pp*NSUB + s2)*16 + j
+        const int pp = row / (NSUB * 16), j = row % (NSUB * 16);
+        src0[i] = row < AR && j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
+      } else {                                          // rows past the tile's end re-read its last row
+        src0[i] = X + (int64_t)min(r0 + row - ARD, r1 - 1) * a.ldx + kcl * 8;
+      }
     }
-    // rows past the tile's end read its last row (results discarded)
-    const bf16* xrow = X + (int64_t)min(m, r1 - 1) * a.ldx + 8 * (lane >> 4);
     const int nc = a.K / 64;
-    bf16x8 xr[NST][2];
     // every chunk index past the end re-reads the last chunk, so each step
-    // issues the same GRP loads and one wait count holds throughout
+    // issues the same ND loads and one wait count holds throughout
     auto issue = [&](int c, int st) {
       const int cc = min(c, nc - 1);
 #pragma unroll
-      for (int i = 0; i < ARND; ++i) {
-        const bf16* src = asrc[i] ? asrc[i] + cc * 64 : g_seg_zero;
+      for (int i = 0; i < ND; ++i) {
+        const bf16* src = src0[i] ? src0[i] + cc * 64 : g_seg_zero;
         __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(&As[st][(i * 4 + wave) * 512]), 16, 0, 0);
       }
-      gload16_untracked(xr[st][0], xrow + cc * 64);
-      gload16_untracked(xr[st][1], xrow + cc * 64 + 32);
     };
 #pragma unroll
     for (int i = 0; i < NST - 1; ++i) issue(i, i);
@@ -110,22 +103,22 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
         const int c = c0 + j;
         if (c >= nc) break;
         // chunk c landed once at most (NST - 2) later groups are outstanding
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * GRP) : "memory");
-        asm volatile("" : "+v"(xr[j][0]), "+v"(xr[j][1]));   // uses stay below the wait
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * ND) : "memory");
         __builtin_amdgcn_s_barrier();     // every wave's part is in LDS; stage (c-1) is free
         issue(c + NST - 1, (j + NST - 1) % NST);
         const bf16* Ab = As[j];
-        const bf16x8 x0 = xr[j][0], x1 = xr[j][1];
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           const int kc = kk * 4 + (lane >> 4);
+          const int xr = ARD + wave * 16 + (lane & 15);
+          const bf16x8 xf = *reinterpret_cast<const bf16x8*>(Ab + xr * 64 + ((kc ^ ((xr >> 1) & 7)) * 8));
 #pragma unroll
           for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
             for (int s2 = 0; s2 < NSUB; ++s2) {
               const int r = (pp * NSUB + s2) * 16 + (lane & 15);
               const bf16x8 af = *reinterpret_cast<const bf16x8*>(Ab + r * 64 + ((kc ^ ((r >> 1) & 7)) * 8));
-              acc[pp][s2] = mfma16(af, kk ? x1 : x0, acc[pp][s2]);
+              acc[pp][s2] = mfma16(af, xf, acc[pp][s2]);
             }
         }
       }

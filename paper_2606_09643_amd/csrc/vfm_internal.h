@@ -154,6 +154,16 @@ __device__ inline float gelu_fast(float v) {
   return v * fmaf(p, t, 0.5f);
 }
 
+// SiLU for bf16 outputs, v sigmoid(v) = v / (1 + 2^(-v log2 e)), from the
+// hardware base-2 exponential and reciprocal (each within about 1 ulp, far
+// below the 2^-9 relative rounding of the bf16 result): 5 VALU operations
+// against ~23 for the library exponential and an IEEE divide.  For very
+// negative v the power overflows to +inf, the reciprocal gives 0 and the
+// result a signed zero, as the exact form does.
+__device__ __forceinline__ float silu_fast(float v) {
+  return v * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(v * -1.44269504088896341f));
+}
+
 // Benchmark timing hooks (profile.hip): bracket one launch of class `cls`.
 int prof_begin(int cls, hipStream_t s);
 void prof_end(int idx, hipStream_t s);
