@@ -210,7 +210,10 @@ __device__ __forceinline__ int pair_key(int ks, int x) {  // key of row x of sub
 // O^T = V^T P^T is read from the row-major V tile with gfx950's transposing
 // LDS read (ds_read_b64_tr_b16, vtr_frag), so V is never transposed in
 // registers.  Causal: a wave skips key blocks entirely past its queries and
-// masks only the block on its diagonal.
+// masks only the block on its diagonal.  The causal variant is built for 3
+// waves per SIMD (168 VGPRs, no spills; 3 blocks of 32 KB LDS per CU) instead
+// of the 2 its unconstrained 204 registers allow: the extra resident block
+// hides the per-step staging and barriers of the others.
 // ---------------------------------------------------------------------------
 // V tile row-major in LDS ([64 keys][DH] bf16) with 32-byte segments
 // swizzled per row: segment s of key row r sits at s ^ vswz(r).  vswz makes
@@ -255,7 +258,7 @@ __device__ __forceinline__ bf16x8 vtr_frag(const bf16* Vs, int vbase, int u, int
 }
 
 template <int DH, bool CAUSAL, bool FROM_CACHE = false>
-__global__ __launch_bounds__(256) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 3 : 2))) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                                 int d, bf16* __restrict__ out,
                                                                 float scale_log2,
                                                                 const bf16* __restrict__ kc = nullptr,
