@@ -260,7 +260,7 @@ __device__ __forceinline__ bf16x8 vtr_frag(const bf16* Vs, int vbase, int u, int
 template <int DH, bool CAUSAL, bool FROM_CACHE = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 3 : 2))) void attn_prefill_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                                 int d, bf16* __restrict__ out,
-                                                                float scale_log2,
+                                                                float scale_log2, int skip_len,
                                                                 const bf16* __restrict__ kc = nullptr,
                                                                 const bf16* __restrict__ vc = nullptr,
                                                                 int64_t kv_slots = 0, KvPages kpg = {}) {
@@ -278,6 +278,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 3 
   // pass has already put the chunk's rows; query i sits at position ctx + i
   const int ctx = FROM_CACHE ? pl.ctx[p] : 0;
   if (FROM_CACHE && (ctx == 0 || L == 1)) return;   // block-uniform: other kernels' requests
+  if (!FROM_CACHE && L <= skip_len) return;        // the whole-request kernel's
   const int NK = ctx + L;                          // keys of the request
   const int q0 = (b - pl.qblk_off[p]) * 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -422,7 +423,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 3 
 
 
 // ---------------------------------------------------------------------------
-// Prefill attention for requests of at most 256 tokens (bf16, MFMA).
+// Prefill attention for requests of at most 256 tokens (bf16, MFMA, head
+// dim 64; the launcher picks it by each request's own length).
 // One block per (request, head): K and V of the whole request are staged in
 // LDS once, row-major (V^T fragments come from the transposing LDS read, as
 // in the flash kernel), then each wave takes 16-query groups; with all keys
@@ -441,6 +443,7 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
   const int p = blockIdx.x, h = blockIdx.y;
   const int R = pl.cu_seqlens[p];
   const int L = pl.cu_seqlens[p + 1] - R;
+  if (L > LMAX) return;                         // block-uniform: a flash-kernel request
   constexpr int Lp = LMAX;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
   const int64_t ld = 3 * (int64_t)d;
@@ -996,9 +999,13 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
     pi = prof_begin(VFM_PROF_ATTN, s);
     dim3 grid(pl.n_qblocks, H);
     const bool causal = c.attn != VFM_ATTN_BIDIR;
-    if (dtype == VFM_BF16 && pl.max_seqlen <= 256) {
+    const int short_rows = DH == 64 ? VFM_SHORT_ATTN_ROWS : 0;   // whole-request kernel up to this
+    if (dtype == VFM_BF16 && short_rows > 0 && pl.max_short > 0) {
+      // requests of at most VFM_SHORT_ATTN_ROWS rows (the others return);
+      // keys past a request's length add exact zeros, so the sub-tile count
+      // does not change its result
       dim3 g2(pl.n_req, H);
-      const int nks = ((pl.max_seqlen + 31) / 32) * 2;   // 16-key sub-tiles, even
+      const int nks = ((pl.max_short + 31) / 32) * 2;   // 16-key sub-tiles, even
 #define SHORT(D_, C_, N_)                                                                           \
   hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_, N_>), g2, dim3(256), 0, s, pl, (const bf16*)qkv, \
                      d, (bf16*)out, scale_log2)
@@ -1009,18 +1016,20 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
     case 10: SHORT(D_, C_, 10); break; case 12: SHORT(D_, C_, 12); break; \
     case 14: SHORT(D_, C_, 14); break; default: SHORT(D_, C_, 16); break; \
   }
-      if (DH == 64) { if (causal) { SHORT_N(64, true); } else { SHORT_N(64, false); } }
-      else { if (causal) { SHORT_N(128, true); } else { SHORT_N(128, false); } }
+      if (causal) { SHORT_N(64, true); } else { SHORT_N(64, false); }
 #undef SHORT_N
 #undef SHORT
-    } else if (dtype == VFM_BF16) {
+    }
+    if (dtype == VFM_BF16 && (short_rows == 0 || pl.n_long > 0)) {
+      // requests longer than short_rows (the others return)
 #define PRE(D_, C_)                                                                            \
   hipLaunchKernelGGL((attn_prefill_bf16_kernel<D_, C_>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
-                     d, (bf16*)out, scale_log2)
+                     d, (bf16*)out, scale_log2, short_rows)
       if (DH == 64) { if (causal) PRE(64, true); else PRE(64, false); }
       else { if (causal) PRE(128, true); else PRE(128, false); }
 #undef PRE
-    } else {
+    }
+    if (dtype != VFM_BF16) {
       if (DH == 64)
         hipLaunchKernelGGL((attn_prefill_simt_kernel<float, 64>), grid, dim3(256), 0, s, pl,
                            (const float*)qkv, d, (float*)out, scale_log2, (int)causal);
@@ -1034,7 +1043,7 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
     if (mixed && chunked && dtype == VFM_BF16) {
 #define CHUNK(D_)                                                                                     \
   hipLaunchKernelGGL((attn_prefill_bf16_kernel<D_, true, true>), grid, dim3(256), 0, s, pl,           \
-                     (const bf16*)qkv, d, (bf16*)out, scale_log2, (const bf16*)k_cache,              \
+                     (const bf16*)qkv, d, (bf16*)out, scale_log2, 0, (const bf16*)k_cache,           \
                      (const bf16*)v_cache, kv_slots, kp)
       if (DH == 64) CHUNK(64); else CHUNK(128);
 #undef CHUNK

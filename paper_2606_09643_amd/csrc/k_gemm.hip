@@ -344,7 +344,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   constexpr int NTILE = SWIGLU ? BNT / 2 : BNT;  // output columns per block
-  const int MT = (a.M + BMT - 1) / BMT, NTn = (a.N + NTILE - 1) / NTILE, ntiles = MT * NTn;
+  const int MT = (a.m_hi - a.m_lo + BMT - 1) / BMT, NTn = (a.N + NTILE - 1) / NTILE, ntiles = MT * NTn;
   const int per = gridDim.x / 8;
   const int Lid = (blockIdx.x % 8) * per + blockIdx.x / 8;
   if (Lid >= ntiles) return;
@@ -357,7 +357,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     tm = fm + r % gm;
     tn = r / gm;
   }
-  const int m0 = tm * BMT, n0 = tn * NTILE;
+  const int m0 = a.m_lo + tm * BMT, n0 = tn * NTILE;
   const bf16* X = (const bf16*)a.X;
   const GemmLora& L = a.lora;
 
@@ -847,22 +847,56 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
   }
 }
 
-// Tile shape of the large GEMM for an M x N product: the candidate with the
-// least estimated time, rounds of 256 concurrent tiles times the bytes a tile
-// moves per K step (BMT + BNT rows of 128 B; the loop is bound by that
-// stream), among shapes whose column tiles do not straddle a LoRA slot.
+// Tile shapes of the large GEMM for an M x N product.  A launch of R tiles
+// costs its rounds of 256 concurrent tiles (one per CU) times the bytes a
+// tile moves per K step (BMT + BNT rows of 128 B; the loop is bound by that
+// stream).  The candidates are the shapes whose column tiles do not straddle
+// a LoRA slot.  Besides one launch of the cheapest shape, the rows may be
+// split: whole 256-row tiles of one shape in full rounds, then the remaining
+// rows with narrower tiles, so the last, partly filled round costs less.
+// Every shape runs the same K steps in the same order, so a row's outputs do
+// not depend on which launch or tile shape computes it.
 struct LargeShape { int bm, bn; };
-inline LargeShape large_shape(int M, int N, bool sw, int lora_slot_width) {
-  const LargeShape cand[3] = {{256, 256}, {256, 192}, {256, 128}};
-  LargeShape best = {0, 0};
+constexpr LargeShape kLargeShapes[3] = {{256, 256}, {256, 192}, {256, 128}};
+inline bool shape_ok(const LargeShape& c, bool sw, int lora_slot_width) {
+  return !(lora_slot_width > 0 && !sw && lora_slot_width % c.bn);
+}
+inline double launch_cost(int rows, int N, bool sw, const LargeShape& c) {
+  if (rows <= 0) return 0.0;
+  const int nt = sw ? c.bn / 2 : c.bn;
+  const long tiles = (long)((rows + c.bm - 1) / c.bm) * ((N + nt - 1) / nt);
+  const long rounds = (tiles + 255) / 256;
+  return (double)rounds * (c.bm + c.bn) * (sw ? 2.0 * nt / c.bn : 1.0);
+}
+struct LargePlan { LargeShape main, tail; int m1; };   // rows [0, m1) main, [m1, M) tail
+inline LargePlan large_plan(int M, int N, bool sw, int lora_slot_width) {
+  LargePlan best = {{0, 0}, {0, 0}, M};
   double best_cost = 0.0;
-  for (const LargeShape& c : cand) {
-    if (lora_slot_width > 0 && !sw && lora_slot_width % c.bn) continue;
-    const int nt = sw ? c.bn / 2 : c.bn;
-    const long tiles = (long)((M + c.bm - 1) / c.bm) * ((N + nt - 1) / nt);
-    const long rounds = (tiles + 255) / 256;
-    const double cost = (double)rounds * (c.bm + c.bn) * (sw ? 2.0 * nt / c.bn : 1.0);
-    if (best.bm == 0 || cost < best_cost * 0.97) { best = c; best_cost = cost; }
+  for (const LargeShape& c : kLargeShapes) {
+    if (!shape_ok(c, sw, lora_slot_width)) continue;
+    const double cost = launch_cost(M, N, sw, c);
+    if (best.main.bm == 0 || cost < best_cost * 0.97) { best = {c, {0, 0}, M}; best_cost = cost; }
+  }
+  if (best.main.bm == 0) return best;
+  const double single = best_cost;
+  const LargeShape mc = best.main;
+  const int nt = sw ? mc.bn / 2 : mc.bn;
+  const int ntn = (N + nt - 1) / nt, mt = (M + mc.bm - 1) / mc.bm;
+  // A last round under a quarter full already runs well below a full
+  // round's time (its few tiles do not share L2 and HBM bandwidth): no split
+  // (measured: the 7B QKV's 32-tile last round is cheaper than a 256 x 128
+  // tail launch).  Otherwise a split must beat the single launch by 1.5%.
+  const int last = (int)(((long)mt * ntn) % 256);
+  if (last == 0 || last < 64) return best;
+  const int full = (int)(((long)mt * ntn) / 256 * 256 / ntn);   // row tiles filling whole rounds
+  for (int r1 = full; r1 >= 1 && r1 >= full - 2; --r1) {
+    const int m1 = r1 * mc.bm;
+    if (m1 >= M) continue;
+    for (const LargeShape& t : kLargeShapes) {
+      if (!shape_ok(t, sw, lora_slot_width)) continue;
+      const double cost = launch_cost(m1, N, sw, mc) + launch_cost(M - m1, N, sw, t);
+      if (cost < single * 0.985 && cost < best_cost) { best = {mc, t, m1}; best_cost = cost; }
+    }
   }
   return best;
 }
@@ -870,24 +904,38 @@ inline LargeShape large_shape(int M, int N, bool sw, int lora_slot_width) {
 template <int EPI, bool SW, int BMT, int BNT>
 void launch_large(const GemmArgs& a, hipStream_t s) {
   const int nt = SW ? BNT / 2 : BNT;
-  const int ntiles = ((a.M + BMT - 1) / BMT) * ((a.N + nt - 1) / nt);
+  const int ntiles = ((a.m_hi - a.m_lo + BMT - 1) / BMT) * ((a.N + nt - 1) / nt);
   const int grid = (ntiles + 7) / 8 * 8;
   hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW, BMT, BNT>), dim3(grid), dim3(512), 0, s, a);
 }
+template <int EPI, bool SW>
+void launch_large_shape(const GemmArgs& a, const LargeShape& sh, hipStream_t s) {
+  if (sh.bn == 256) launch_large<EPI, SW, 256, 256>(a, s);
+  else if (sh.bn == 192) launch_large<EPI, SW, 256, 192>(a, s);
+  else launch_large<EPI, SW, 256, 128>(a, s);
+}
 
 template <int EPI, bool SW>
-hipError_t launch_one(int dtype, const GemmArgs& a, hipStream_t s) {
-  const LargeShape sh = large_shape(a.M, a.N, SW, a.lora.enabled ? a.lora.slot_width : 0);
-  const bool fits32 = (int64_t)a.M * a.ldx < ((int64_t)1 << 31) && (int64_t)a.N * a.K < ((int64_t)1 << 31);
-  if (dtype == VFM_BF16 && a.M >= 1024 && sh.bm > 0 && fits32) {
-    if (sh.bn == 256) launch_large<EPI, SW, 256, 256>(a, s);
-    else if (sh.bn == 192) launch_large<EPI, SW, 256, 192>(a, s);
-    else launch_large<EPI, SW, 256, 128>(a, s);
+hipError_t launch_one(int dtype, const GemmArgs& a0, hipStream_t s) {
+  const LargePlan pl = large_plan(a0.M, a0.N, SW, a0.lora.enabled ? a0.lora.slot_width : 0);
+  const bool fits32 = (int64_t)a0.M * a0.ldx < ((int64_t)1 << 31) && (int64_t)a0.N * a0.K < ((int64_t)1 << 31);
+  if (dtype == VFM_BF16 && a0.M >= 1024 && pl.main.bm > 0 && fits32) {
+    GemmArgs a = a0;
+    a.m_lo = 0;
+    a.m_hi = pl.m1;
+    launch_large_shape<EPI, SW>(a, pl.main, s);
+    if (pl.m1 < a0.M) {
+      a.m_lo = pl.m1;
+      a.m_hi = a0.M;
+      launch_large_shape<EPI, SW>(a, pl.tail, s);
+    }
   } else if (dtype == VFM_BF16) {
+    const GemmArgs& a = a0;
     const int nt = SW ? BN / 2 : BN;
     const int grid = ((a.M + BM - 1) / BM) * ((a.N + nt - 1) / nt);
     hipLaunchKernelGGL((gemm_bf16_kernel<EPI, SW>), dim3(grid), dim3(256), 0, s, a);
   } else {
+    const GemmArgs& a = a0;
     const int grid = ((a.M + 63) / 64) * ((a.N + 63) / 64);
     hipLaunchKernelGGL((gemm_f32_kernel<EPI, SW>), dim3(grid), dim3(256), 0, s, a);
   }

@@ -407,7 +407,11 @@ inline int maxi_for(int d) { return d <= 1024 ? 4 : (d <= 4096 ? 16 : 32); }
 hipError_t launch_norm(int dtype, const float* x, int T, int d, const void* g, const void* b,
                        int kind, float eps, void* out, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (T < 2048 && d >= 1024) {   // few rows: a block per row (d <= 8192: <= 8 chunks per thread)
+  // Small bf16 batches (the small-batch path's side of VFM_SMALL_BATCH_ROWS):
+  // a block per row (d <= 8192: <= 8 chunks per thread).  The choice follows
+  // that threshold and nothing else, since the two kernels sum a row in
+  // different orders: a row's result depends only on which side its batch is.
+  if (dtype == VFM_BF16 && T < VFM_SMALL_BATCH_ROWS && d >= 1024) {
 #define NORM_BLOCK(TT)                                                                           \
   hipLaunchKernelGGL((norm_rows_block_kernel<TT, 8>), dim3(T), dim3(256), 0, s, x, d, (const TT*)g, \
                      (const TT*)b, kind, eps, (TT*)out)

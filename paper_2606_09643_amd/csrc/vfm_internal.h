@@ -47,7 +47,17 @@ struct Plan {
   const int32_t *order, *task, *cu_seqlens, *seg_req, *seg_row, *cu_orig, *out_off, *ctx,
       *kv_start, *qblk_off, *rtile_off, *row_task, *row_req, *pos;
   int32_t n_req, n_tasks, T, max_seqlen, n_qblocks, n_rtiles, total_outputs;
+  // launch facts from the host copy: the longest request of at most
+  // VFM_SHORT_ATTN_ROWS rows (0 if none) and the number of longer ones
+  int32_t max_short, n_long;
 };
+
+// Prompt attention with head dim 64 takes the whole-request kernel for
+// requests of at most this many rows and the flash kernel for longer ones
+// (head dim 128: the flash kernel for every prompt; its whole-request variant
+// needs 128 KB of LDS and measured slower), by each request's own length, so
+// a request's result does not depend on the rest of the batch.
+constexpr int VFM_SHORT_ATTN_ROWS = 256;
 
 inline Plan make_plan(const int32_t* host, const int32_t* dev) {
   Plan p;
@@ -73,6 +83,14 @@ inline Plan make_plan(const int32_t* host, const int32_t* dev) {
   p.row_task = dev + o.row_task;
   p.row_req = dev + o.row_req;
   p.pos = dev + o.pos;
+  p.max_short = 0;
+  p.n_long = 0;
+  const int32_t* cu = host + o.cu_seqlens;
+  for (int i = 0; i < p.n_req; ++i) {
+    const int len = cu[i + 1] - cu[i];
+    if (len > VFM_SHORT_ATTN_ROWS) ++p.n_long;
+    else if (len > p.max_short) p.max_short = len;
+  }
   return p;
 }
 
@@ -223,6 +241,7 @@ struct GemmArgs {
   int epi;
   void* out; int ldo;              // EPI_STORE/GELU/SWIGLU (dtype) or EPI_RESID (fp32)
   GemmLora lora;
+  int m_lo, m_hi;                  // rows one large-tile launch covers (set by launch_gemm)
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
 

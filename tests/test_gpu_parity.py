@@ -177,21 +177,33 @@ def test_lora_apply(dtype, idx):
 
 # Batch-invariance cases: workload 2 with every task alone still above the
 # small-batch threshold (large-tile kernels), workload 4 below it (split-K).
+# The "tail" cases make the large-tile GEMMs compute a task's rows with other
+# tile shapes than when the task runs alone: the mixed batch's last,
+# partly filled round of 256 x 256 tiles goes to a second launch of 256 x 128
+# tiles (7B O / down: rows 4096.. of 5300; ViT-B MLP-up: rows 5376.. of
+# 7092), while alone the first task's O / down (1204 rows, workload 4) and
+# QKV (2758 rows, workload 2) run as 256 x 128 and the other tasks' rows as
+# 256 x 256 tiles; both also cross the row count at which the pre-norms of
+# the old code switched kernels.  "4-mixlen" puts 200-row prompts (the
+# whole-request attention kernel) beside 300-row ones (the flash kernel).
 INVARIANCE = {
-    2: dict(task_id=[5, 0, 2, 0, 5, 2, 2, 5, 0, 5, 0, 2, 0, 2, 5, 5, 2, 0], seq_len=[197] * 18),
-    4: SMALL[4],
+    "2": (2, dict(task_id=[5, 0, 2, 0, 5, 2, 2, 5, 0, 5, 0, 2, 0, 2, 5, 5, 2, 0], seq_len=[197] * 18)),
+    "4": (4, SMALL[4]),
+    "2-tail": (2, dict(task_id=[0] * 14 + [5] * 14 + [9] * 8, seq_len=[197] * 36)),
+    "4-tail": (4, dict(task_id=[1, 1, 9, 9, 9, 9], seq_len=[602, 602, 1024, 1024, 1024, 1024])),
+    "4-mixlen": (4, dict(task_id=[1] * 6 + [9] * 4, seq_len=[200] * 6 + [300] * 4)),
 }
 
 
-@pytest.mark.parametrize("idx", [2, 4])
-def test_batch_invariance_and_zero_rank_bit_exact(idx):
+@pytest.mark.parametrize("name", list(INVARIANCE))
+def test_batch_invariance_and_zero_rank_bit_exact(name):
     """A task's rows are bit-identical whether co-batched with other tasks or
     run alone (both batches on one side of the small-batch threshold), and a
     rank-0 task equals the bare backbone bit for bit."""
+    idx, case = INVARIANCE[name]
     w = wl.WORKLOADS[idx]
     ranks = np.full(w.n_tasks, w.rank, np.int32)
     ranks[0] = 0
-    case = INVARIANCE[idx]
     w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, ranks=ranks, b_std=0.1,
                                                     case=case)
     small = pb.T < B.VFM_SMALL_BATCH_ROWS
