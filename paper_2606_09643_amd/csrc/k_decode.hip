@@ -262,13 +262,21 @@ __global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitA
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   __shared__ float Us[3 * VFM_MAX_RANK];
-  const int m = blockIdx.y;
+  // Block b takes (column block, row) number (b % 8) * per + b / 8, rows
+  // fastest: consecutive blocks of one XCD (one L2) take consecutive rows of
+  // one column block, so a task's B rows, read again for its next rows, come
+  // from that XCD's L2 instead of beyond it.
+  const int ncb = (a.N / 4 + 255) / 256;
+  const int per = gridDim.x / 8;
+  const int lid = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (lid >= ncb * a.M) return;               // block-uniform
+  const int m = lid % a.M, cb = lid / a.M;
   int t = 0, r = 0;
   if (a.lora.enabled) {                       // block-uniform
     t = a.lora.row_task[m];
     r = fin_lora_u(a.lora, m, Us);
   }
-  const int n = (blockIdx.x * 256 + threadIdx.x) * 4;
+  const int n = (cb * 256 + threadIdx.x) * 4;
   if (n >= a.N) return;
   const bool swiglu = a.epi == EPI_SWIGLU;
   const int nz = swiglu ? 2 * a.N : a.N;   // columns of Z
@@ -371,7 +379,7 @@ hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a0, hipStr
 
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
-  const int per_row = a.N / 4;
-  hipLaunchKernelGGL(finalize_kernel, dim3((per_row + 255) / 256, a.M), dim3(256), 0, s, a);
+  const int ncb = (a.N / 4 + 255) / 256;
+  hipLaunchKernelGGL(finalize_kernel, dim3(((int64_t)ncb * a.M + 7) / 8 * 8), dim3(256), 0, s, a);
   return hipGetLastError();
 }

@@ -173,7 +173,11 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
                                                             T* __restrict__ h) {
   __shared__ float red[2][4];
   __shared__ float Us[3 * VFM_MAX_RANK];
-  const int row = blockIdx.x, tid = threadIdx.x;
+  // block b takes row (b % 8) * per + b / 8: consecutive rows (often one
+  // task's) run on one XCD, so the task's B rows come from that XCD's L2
+  const int per = gridDim.x / 8;
+  const int row = (blockIdx.x % 8) * per + blockIdx.x / 8, tid = threadIdx.x;
+  if (row >= a.M) return;                     // block-uniform
   const int nch = a.N >> 2;
   const int64_t zs = (int64_t)a.M * a.N;
   float* xr = (float*)a.out + (int64_t)row * a.ldo;
@@ -438,7 +442,7 @@ hipError_t launch_finalize_norm(int dtype, const FinalizeArgs& a, const void* g,
   if (a.M == 0) return hipSuccess;
   if (a.epi != EPI_RESID || dtype != VFM_BF16 || a.N % 4 || a.N > 8192 || a.ldo != a.N)
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL((finalize_norm_kernel<bf16, 8>), dim3(a.M), dim3(256), 0, s, a, (const bf16*)g,
+  hipLaunchKernelGGL((finalize_norm_kernel<bf16, 8>), dim3((a.M + 7) / 8 * 8), dim3(256), 0, s, a, (const bf16*)g,
                      (const bf16*)b, kind, eps, (bf16*)h);
   return hipGetLastError();
 }
