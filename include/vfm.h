@@ -324,7 +324,7 @@ int vfm_layer_forward(const vfm_cfg* cfg, const vfm_layer_weights* w, const vfm_
  * the library, one per GPU, held by each GPU the library runs on until the
  * process ends.  A batch whose workspace (vfm_workspace_size) exceeds it is
  * refused on the host with VFM_ERR_WORKSPACE (the decode step of 256 rows of
- * a 4096-wide, 11008-MLP decoder needs about 105 MiB; a 12 608-row ViT-B
+ * a 4096-wide, 11008-MLP decoder needs about 93 MiB; a 12 608-row ViT-B
  * batch about 117 MiB).  The call allocates nothing (no hipMalloc, hipFree or
  * allocating library routine): the array's device address is looked up once
  * per device, on the first call with that device current.  stream must
