@@ -370,6 +370,9 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
   // output buffer); the small-batch path then fuses the two, and the caller
   // skips its own norm launch when `fused_norm` comes back true
   bool fused_norm = false;
+  // set for the QKV projection of a small batch: the finalize applies RoPE
+  // (and the cache write) itself
+  FinRope fin_rope = {};
   auto project = [&](int cls, const void* X, int K, const void* W, const void* W2,
                      const void* bias, int N, int epi, void* out, int ldo,
                      std::initializer_list<int> projs, int slot_width, const void* norm_g = nullptr,
@@ -422,12 +425,14 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
     FinalizeArgs fa = {};
     fa.Z = Z; fa.nslices = k.nsplit; fa.M = T; fa.N = N; fa.epi = epi; fa.bias = bias;
     fa.out = out; fa.ldo = ldo;
+    fa.rope = fin_rope;
     if (any) {
       // the split shrink writes fp32 partials; the finalize pass sums them
       // into each row's U and adds U B_t^T to the row's columns
       ShrinkSplitArgs a = {};
       a.X = X; a.ldx = K; a.K = K; a.P = P; a.ldp = ldu; a.rpad = rpad;
       a.kchunks = shrink_chunks(K); a.rank = lora->rank;
+      a.nsub = std::min(std::max(1, (lora->max_rank + 15) / 16), rpad / 16);
       for (int p : projs) {
         if (!has(p)) continue;
         a.A[a.n_proj] = lora->A[p];
@@ -462,14 +467,26 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
 
   // a2: pre-norm 1
   VFM_TIMED(VFM_PROF_NORM, launch_norm(c.dtype, x, T, d, w->norm1_w, w->norm1_b, c.norm, c.norm_eps, h, s));
+  // a5 (small bf16 batches): the QKV finalize also applies the rotary
+  // embedding of q and k and, with a KV cache, writes each row's rotated k
+  // and its v to its slot
+  const bool cache_write = k_cache != nullptr && c.attn != VFM_ATTN_BIDIR;
+  const bool rope_writes_kv = c.rope_theta > 0.f && cache_write;
+  const bool rope_in_finalize = skinny && c.dtype == VFM_BF16 && c.rope_theta > 0.f &&
+                                (c.head_dim == 64 || c.head_dim == 128) && d % 256 == 0;
+  if (rope_in_finalize) {
+    fin_rope.on = 1; fin_rope.d = d; fin_rope.head_dim = c.head_dim; fin_rope.log2_theta = log2f(c.rope_theta);
+    fin_rope.pl = pl; fin_rope.kp = kp; fin_rope.kv_slots = kv_slots;
+    fin_rope.kc = rope_writes_kv ? (bf16*)k_cache : nullptr;
+    fin_rope.vc = rope_writes_kv ? (bf16*)v_cache : nullptr;
+  }
   // a3 + a4: shared QKV projection with the per-task LoRA of q, k, v
   VFM_TRY(project(VFM_PROF_GEMM_QKV, h, d, w->w_qkv, nullptr, w->b_qkv, 3 * d, EPI_STORE, qkv,
                   3 * d, {VFM_Q, VFM_K, VFM_V}, d));
+  fin_rope = FinRope{};
   // a5: rotary embedding of q and k
   // (with a KV cache the same pass writes each row's rotated k and its v)
-  const bool cache_write = k_cache != nullptr && c.attn != VFM_ATTN_BIDIR;
-  const bool rope_writes_kv = c.rope_theta > 0.f && cache_write;
-  if (c.rope_theta > 0.f)
+  if (c.rope_theta > 0.f && !rope_in_finalize)
     VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta,
                                           rope_writes_kv ? k_cache : nullptr, rope_writes_kv ? v_cache : nullptr,
                                           kv_slots, kp, s));

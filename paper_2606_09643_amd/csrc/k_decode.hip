@@ -207,7 +207,7 @@ __global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitA
   const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
   const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rank = min(a.rank[t], a.rpad);
+  const int rank = min(a.rank[t], NSUB * 16);
   const int m = r0 + wave * 16 + (lane & 15);
   const int k0 = c * a.kchunk, k1 = min(k0 + a.kchunk, a.K);
   const bf16* X = (const bf16*)a.X;
@@ -262,6 +262,7 @@ __global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitA
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   __shared__ float Us[3 * VFM_MAX_RANK];
+  __shared__ float rcs[64], rsn[64];          // the row's rotary angles (head_dim / 2 <= 64)
   // Block b takes (column block, row) number (b % 8) * per + b / 8, rows
   // fastest: consecutive blocks of one XCD (one L2) take consecutive rows of
   // one column block, so a task's B rows, read again for its next rows, come
@@ -275,6 +276,17 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   if (a.lora.enabled) {                       // block-uniform
     t = a.lora.row_task[m];
     r = fin_lora_u(a.lora, m, Us);
+  }
+  if (a.rope.on) {                            // block-uniform: the row's angles, as launch_rope
+    const int half = a.rope.head_dim >> 1;
+    if (threadIdx.x < half) {
+      const float inv = exp2f(-(2.0f * (float)threadIdx.x / (float)a.rope.head_dim) * a.rope.log2_theta);
+      float sn, cs;
+      sincosf((float)a.rope.pl.pos[m] * inv, &sn, &cs);
+      rcs[threadIdx.x] = cs;
+      rsn[threadIdx.x] = sn;
+    }
+    __syncthreads();
   }
   const int n = (cb * 256 + threadIdx.x) * 4;
   if (n >= a.N) return;
@@ -302,6 +314,27 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
     *xo = xv;
     return;
   }
+  if (a.rope.on && n < 2 * a.rope.d) {        // q and k columns (whole waves: d % 256 == 0)
+    // rotate-half: column i of a head pairs with column i + head_dim / 2,
+    // held head_dim / 8 lanes away (4 columns per lane)
+    const int dh = a.rope.head_dim, half = dh >> 1;
+    const int cin = n % dh;
+    float4 pv;
+    pv.x = __shfl_xor(v.x, dh / 8, 64);
+    pv.y = __shfl_xor(v.y, dh / 8, 64);
+    pv.z = __shfl_xor(v.z, dh / 8, 64);
+    pv.w = __shfl_xor(v.w, dh / 8, 64);
+    const bool second = cin >= half;
+    const int i0 = second ? cin - half : cin;
+    float x4[4] = {v.x, v.y, v.z, v.w};
+    const float p4[4] = {pv.x, pv.y, pv.z, pv.w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float cs = rcs[i0 + c], sn = rsn[i0 + c];
+      x4[c] = second ? p4[c] * sn + x4[c] * cs : x4[c] * cs - p4[c] * sn;
+    }
+    v = make_float4(x4[0], x4[1], x4[2], x4[3]);
+  }
   const float g4[4] = {v.x, v.y, v.z, v.w};
   float u4[4] = {0.f, 0.f, 0.f, 0.f};
   if (swiglu) {
@@ -318,6 +351,15 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
     o[c] = (bf16)y;
   }
   *reinterpret_cast<bf16x4*>((bf16*)a.out + (int64_t)m * a.ldo + n) = o;
+  if (a.rope.on && a.rope.kc != nullptr && n >= a.rope.d) {   // the row's k (rotated) and v to its slot
+    const int dd = a.rope.d, dh = a.rope.head_dim;
+    const bool isv = n >= 2 * dd;
+    const int cc = isv ? n - 2 * dd : n - dd;
+    const int hh = cc / dh;
+    const int64_t slot = kv_slot(a.rope.pl, a.rope.kp, a.rope.pl.row_req[m], a.rope.pl.pos[m]);
+    bf16* dst = (isv ? a.rope.vc : a.rope.kc) + ((int64_t)hh * a.rope.kv_slots + slot) * dh + (cc - hh * dh);
+    *reinterpret_cast<bf16x4*>(dst) = o;
+  }
 }
 
 // Column-tile width and K split of the small-batch GEMM for an N x K
@@ -368,11 +410,12 @@ hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a0, hipStr
   a.kchunk = 256;
   dim3 grid(pl.n_rtiles, a.kchunks);
 #define VFM_SS(NP_, NS_) hipLaunchKernelGGL((shrink_split_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
-  if (a.rpad == 32) {
-    if (a.n_proj == 1) VFM_SS(1, 2); else if (a.n_proj == 2) VFM_SS(2, 2); else VFM_SS(3, 2);
-  } else {
-    if (a.n_proj == 1) VFM_SS(1, 4); else if (a.n_proj == 2) VFM_SS(2, 4); else VFM_SS(3, 4);
-  }
+  // only the sub-tiles the table's largest rank reaches: 1 (rank <= 16), 2 (<= 32) or 4
+#define VFM_SS_NP(NS_) do { if (a.n_proj == 1) VFM_SS(1, NS_); else if (a.n_proj == 2) VFM_SS(2, NS_); else VFM_SS(3, NS_); } while (0)
+  if (a.nsub <= 1) VFM_SS_NP(1);
+  else if (a.nsub == 2) VFM_SS_NP(2);
+  else VFM_SS_NP(4);
+#undef VFM_SS_NP
 #undef VFM_SS
   return hipGetLastError();
 }

@@ -262,14 +262,29 @@ int skinny_splits(int N, int K);
 // Split-K segmented LoRA shrink into fp32 partials:
 // P[c, m, ucol[p] + j] = sum over K chunk c of X[m, k] A_{t,p}[j, k] for
 // j < rpad (zero past rank_t); kchunks chunks of kchunk columns.
+// nsub: 16-column sub-tiles worth computing, ceil(max_rank / 16) <= rpad / 16
+// (the finalize reads no partial column past a task's rank).
 struct ShrinkSplitArgs {
   const void* X; int ldx; int K;
   const void* const* A[3]; int ucol[3]; int n_proj;
-  float* P; int ldp; int rpad; int kchunk; int kchunks;
+  float* P; int ldp; int rpad; int nsub; int kchunk; int kchunks;
   const int32_t* rank;
 };
 hipError_t launch_shrink_split(const Plan& pl, const ShrinkSplitArgs& a, hipStream_t s);
 int shrink_chunks(int K);
+
+// Where the K / V of token k of plan position p live in a head-major cache:
+// slot kv_start[p] + k, or with a page table (original request order,
+// max_pages columns) slot table[order[p]][k >> log2_page] pages in.
+struct KvPages {
+  const int32_t* table;       // device; NULL: contiguous (kv_start)
+  int max_pages, log2_page;
+};
+__device__ inline int64_t kv_slot(const Plan& pl, const KvPages& kp, int p, int k) {
+  if (!kp.table) return (int64_t)pl.kv_start[p] + k;
+  const int pg = kp.table[(int64_t)pl.order[p] * kp.max_pages + (k >> kp.log2_page)];
+  return ((int64_t)pg << kp.log2_page) + (k & ((1 << kp.log2_page) - 1));
+}
 
 // Per-task LoRA of a small-batch projection group, applied by the finalize
 // pass: for row m of task t, U = bf16(s_t * sum_c P[c, m, ucol[i] + j]) (the
@@ -286,6 +301,17 @@ struct FinLora {
   const int32_t* row_task;
 };
 
+// Rotary embedding of the q and k columns, applied by the finalize of a
+// small batch's QKV projection (EPI_STORE, bf16): rotate-half per head of
+// head_dim columns at each row's position (pl.pos), before the bf16 rounding;
+// with kc / vc non-null the row's rotated k and its v also go to its cache
+// slot (kv_slot), as launch_rope does.  Needs head_dim 64 or 128 and d a
+// multiple of 256 (a wave's 256 columns then lie in one part of the row).
+struct FinRope {
+  int on; int d; int head_dim; float log2_theta;
+  Plan pl; bf16* kc; bf16* vc; int64_t kv_slots; KvPages kp;
+};
+
 // Sum of nslices partial slices Z[s] ([M, N], SwiGLU [M, 2N]: gate then up
 // columns) in a fixed order, plus bias, plus the fused LoRA difference, and
 // the epilogue of GemmEpi.
@@ -294,6 +320,7 @@ struct FinalizeArgs {
   const void* bias;
   void* out; int ldo;
   FinLora lora;
+  FinRope rope;
 };
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
 
@@ -352,19 +379,6 @@ __device__ __forceinline__ float4 fin_lora_delta(const FinLora& L, int t, int r,
 // then h = Norm(x) as launch_norm.
 hipError_t launch_finalize_norm(int dtype, const FinalizeArgs& a, const void* g, const void* b, int kind,
                                 float eps, void* h, hipStream_t s);
-
-// Where the K / V of token k of plan position p live in a head-major cache:
-// slot kv_start[p] + k, or with a page table (original request order,
-// max_pages columns) slot table[order[p]][k >> log2_page] pages in.
-struct KvPages {
-  const int32_t* table;       // device; NULL: contiguous (kv_start)
-  int max_pages, log2_page;
-};
-__device__ inline int64_t kv_slot(const Plan& pl, const KvPages& kp, int p, int k) {
-  if (!kp.table) return (int64_t)pl.kv_start[p] + k;
-  const int pg = kp.table[(int64_t)pl.order[p] * kp.max_pages + (k >> kp.log2_page)];
-  return ((int64_t)pg << kp.log2_page) + (k & ((1 << kp.log2_page) - 1));
-}
 
 // In-place rotary embedding of the q and k parts of qkv [T, 3d]; with
 // k_cache / v_cache (head-major [n_heads, kv_slots, head_dim]) non-null, each
