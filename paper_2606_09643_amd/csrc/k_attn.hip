@@ -424,15 +424,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CAUSAL ? 3 
 
 // ---------------------------------------------------------------------------
 // Prefill attention for requests of at most 256 tokens (bf16, MFMA, head
-// dim 64; the launcher picks it by each request's own length).
+// dim 64; the launcher picks it by each request's own length).  NW waves
+// take the 16-query groups in turn: with 8 (the launcher's choice) a
+// 197-token request's 13 groups cost a wave at most 2 instead of 4, and two
+// such blocks (56 KB of LDS, 124 VGPRs) still share a CU.
 // One block per (request, head): K and V of the whole request are staged in
 // LDS once, row-major (V^T fragments come from the transposing LDS read, as
 // in the flash kernel), then each wave takes 16-query groups; with all keys
 // resident the softmax is one pass (max, exp, sum) with no rescaling.  Keys
 // are padded to a multiple of 32 with zeros and masked.
 // ---------------------------------------------------------------------------
-template <int DH, bool CAUSAL, int NKS>
-__global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
+template <int DH, bool CAUSAL, int NKS, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void attn_short_bf16_kernel(Plan pl, const bf16* __restrict__ qkv,
                                                               int d, bf16* __restrict__ out,
                                                               float scale_log2) {
   // NKS 16-key sub-tiles cover every request of the batch (NKS * 16 >= L)
@@ -452,11 +455,12 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
   // Stage K and V.  Every global load of a thread is issued before its
   // first LDS store, so the block pays the load latency once.
   {
-    constexpr int KPT = (LMAX * CH + 255) / 256;  // K (and V) chunks per thread
+    constexpr int NT = 64 * NW;
+    constexpr int KPT = (LMAX * CH + NT - 1) / NT;  // K (and V) chunks per thread
     bf16x8 kr[KPT], vr[KPT];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      const int c = tid + NT * i, key = c / CH, ch = c % CH;
       kr[i] = bf16x8{};
       vr[i] = bf16x8{};
       if (key < L && c < LMAX * CH) {
@@ -466,7 +470,7 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
     }
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const int c = tid + 256 * i, key = c / CH, ch = c % CH;
+      const int c = tid + NT * i, key = c / CH, ch = c % CH;
       if (c < LMAX * CH) {
         *reinterpret_cast<bf16x8*>(&Ks[key * DH + sswz<DH>(key, ch) * 8]) = kr[i];
         *reinterpret_cast<bf16x8*>(&Vs[key * DH + vswz_chunk<DH>(key, ch) * 8]) = vr[i];
@@ -483,12 +487,12 @@ __global__ __launch_bounds__(256) void attn_short_bf16_kernel(Plan pl, const bf1
   };
   bf16x8 qnext[DH / 32];
   if (wave * 16 < L) load_q(wave, qnext);
-  for (int qg = wave; qg * 16 < L; qg += 4) {
+  for (int qg = wave; qg * 16 < L; qg += NW) {
     const int qi = qg * 16 + (lane & 15);
     bf16x8 qf[DH / 32];
 #pragma unroll
     for (int s2 = 0; s2 < DH / 32; ++s2) qf[s2] = qnext[s2];
-    if ((qg + 4) * 16 < L) load_q(qg + 4, qnext);   // in flight during this group
+    if ((qg + NW) * 16 < L) load_q(qg + NW, qnext);   // in flight during this group
     f32x4 st[NKS];
     float mx = NEG_BIG;
     // The key swizzle of row 16*ks + (lane & 15) does not depend on ks, so
@@ -1007,7 +1011,7 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
       dim3 g2(pl.n_req, H);
       const int nks = ((pl.max_short + 31) / 32) * 2;   // 16-key sub-tiles, even
 #define SHORT(D_, C_, N_)                                                                           \
-  hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_, N_>), g2, dim3(256), 0, s, pl, (const bf16*)qkv, \
+  hipLaunchKernelGGL((attn_short_bf16_kernel<D_, C_, N_, 8>), g2, dim3(512), 0, s, pl, (const bf16*)qkv, \
                      d, (bf16*)out, scale_log2)
 #define SHORT_N(D_, C_)                                            \
   switch (nks) {                                                   \
