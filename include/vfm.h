@@ -66,11 +66,13 @@ enum { VFM_EMBED_ROWS = 0, VFM_EMBED_TOKENS = 1, VFM_EMBED_PATCHES = 2 };
 #define VFM_ROW_TILE 64
 #define VFM_MAX_RANK 64
 
-/* bf16 batches with fewer rows than this take the small-batch projection
- * kernels (weight-streaming split-K GEMM, LoRA expand after the reduction);
- * larger ones take the large-tile kernels with the LoRA expand fused.  Both
- * fix their summation order from the weight shapes alone, so a row's output
- * is bit-identical across batches on the same side of this threshold. */
+/* bf16 batches with fewer rows than this take the small-batch kernels
+ * (weight-streaming split-K GEMM whose finalize pass adds each row's LoRA
+ * difference, block-per-row norms); larger ones take the large-tile kernels
+ * with the LoRA expand fused and wave-per-row norms.  Both fix their
+ * summation order from the weight shapes alone, and attention picks its
+ * kernel by each request's own length, so a row's output is bit-identical
+ * across batches on the same side of this threshold. */
 #define VFM_SMALL_BATCH_ROWS 1024
 
 /* Backbone shape.  Supported: d_model = n_heads * head_dim, head_dim in
