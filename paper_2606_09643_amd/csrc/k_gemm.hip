@@ -333,7 +333,7 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
 constexpr int LGM = 4;
 
 
-template <int EPI, bool SWIGLU, int BMT, int BNT>
+template <int EPI, bool SWIGLU, int BMT, int BNT, bool PACK>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   constexpr int NW = 8, NTH = 512, WN = 2, TM = BMT / 4, TN = BNT / 2, FM = TM / 16, FN = TN / 16;
   constexpr int ACH = BMT * 8 / NTH, BCH = BNT * 8 / NTH;  // 16-byte chunks per lane and stage
@@ -394,21 +394,30 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // one task each.  The task ids of the tile's rows arrive with the first
   // operand DMA (RPL per lane); ballots of the rows that start a run then
   // list the runs, so a task without rows in the tile (an id absent from the
-  // batch included) costs no step.  Each run gets `parts` extra K steps whose
-  // A tile is U (the run's rows, the slot's columns; other rows zero) and B
-  // tile B_t of the run's task (zero past its rank).  A run's rank and B
-  // pointers are loaded while the previous run's first step is issued; their
-  // first use is a step later, after that step's vmcnt(0), so no step waits
-  // on a dependent load.  (Kept out of LDS on purpose: a second LDS object
-  // makes the compiler wait for the in-flight DMA before every fragment
-  // read.)
+  // batch included) costs no step.  A LoRA step is a 64-column K step whose
+  // A tile is U (the slot's columns; rows of other runs zero) and whose B
+  // tile is B_t (zero past the rank).  Without PACK a step serves one run:
+  // ranks <= 32 fill its first 32 columns (a half step; SwiGLU: gate in the
+  // low 32, up in the high 32), a SwiGLU run of a larger rank takes two
+  // steps (gate, then up).  With PACK (every rank <= 16) the step's columns
+  // are cut into P slots, one run each (16 columns; SwiGLU: 16 gate then 16
+  // up), so a tile with many small runs (a few rows each of many tasks)
+  // needs a quarter (a half) of the steps.  Every product a row meets
+  // outside its own slot has a zero operand, so its sum does not depend on
+  // which runs share its step.  A lane's 16-byte chunk of a step row is
+  // fixed for the tile, and so is its slot.  A group's task ids come from
+  // the tile's row tasks (registers), its ranks and B pointers from the
+  // small per-task tables, which the scalar cache holds.
   const int nk = a.K / BK;
   constexpr int RPL = BMT / 64;                    // tile rows per lane
   static_assert(BMT % 64 == 0, "rows per lane");
   const int parts = (SWIGLU && L.max_rank > 32) ? 2 : 1;
-  const int rpad = L.max_rank > 32 ? 64 : 32;
-  // ranks <= 32 outside SwiGLU fill only the first 32 columns of a LoRA step
-  const bool half = !SWIGLU && rpad == 32;
+  // chunks (8 columns) per projection of a slot, chunks per slot, slots per step
+  const int hc = PACK ? 2 : L.max_rank > 32 ? 8 : 4;
+  const int cwc = (SWIGLU && parts == 1) ? 2 * hc : hc;
+  constexpr int P = PACK ? (SWIGLU ? 2 : 4) : 1;
+  const int slot = PACK ? kc0 / (SWIGLU ? 4 : 2) : 0;     // this lane's slot
+  const int q = PACK ? kc0 % (SWIGLU ? 4 : 2) : kc0;      // and its chunk within the slot
   bool live = false;
   if (L.enabled) {
     if (SWIGLU) live = L.B[0] != nullptr || L.B[1] != nullptr;
@@ -420,13 +429,6 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   for (int j = 0; j < RPL; ++j) rt[j] = live ? L.row_task[min(m0 + RPL * lane + j, a.M - 1)] : 0;
   uint64_t rstart[RPL];                            // bit l of rstart[j]: row RPL*l + j starts a run
   int nlora = 0, nsteps = nk;
-  // issue-side run state (wave-uniform): current run rows [cs, ce) of the
-  // tile, its rank and B pointers; the next run's rank / pointers in flight
-  int cs = 0, ce = 0, cr = 0;
-  const bf16 *cb0 = nullptr, *cb1 = nullptr;
-  int v_nr = 0;
-  const void* v_nb0 = nullptr;
-  const void* v_nb1 = nullptr;
   auto first_start_ge = [&](int r) -> int {        // first run start at tile row >= r, else BMT
     int best = BMT;
 #pragma unroll
@@ -439,24 +441,48 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     }
     return best;
   };
-  // Run metadata flows through a two-deep pipeline: when run k becomes
-  // current, the task id of run k+2's first row and the rank / B pointers of
-  // run k+1 (whose task id arrived one run earlier) are loaded.
-  int v_nt = 0;                                    // task of the run after next
-  auto load_task = [&](int r) { v_nt = L.row_task[m0 + r]; };
-  auto prefetch_run = [&](int t) {                 // rank and B pointers of task t
-    v_nr = L.rank[t];
-    if (SWIGLU) {
-      if (L.B[0]) v_nb0 = L.B[0][t];
-      if (L.B[1]) v_nb1 = L.B[1][t];
-    } else if (L.B[lslot]) {
-      v_nb0 = L.B[lslot][t];
-    }
+  auto task_at = [&](int r) -> int {               // task of tile row r (wave-uniform r)
+    int t = __builtin_amdgcn_readlane(rt[0], r / RPL);
+#pragma unroll
+    for (int j = 1; j < RPL; ++j)
+      if (r % RPL == j) t = __builtin_amdgcn_readlane(rt[j], r / RPL);
+    return t;
   };
-  auto take_run = [&]() {                          // the prefetched values become current
-    cr = min(v_nr, L.max_rank) & ~7;
-    cb0 = (const bf16*)v_nb0;
-    cb1 = (const bf16*)v_nb1;
+  // The current step's group (wave-uniform): where it starts and ends
+  // (g_start == g_end: no group yet).  A group's ranks and B pointers are
+  // read when its first step is issued, from the small per-task tables (the
+  // scalar cache holds them), its task ids straight from the tile's row tasks.
+  int g_start = 0, g_end = 0;
+  int cs = 0, ce = 0, cr = 0;                      // this lane's run: tile rows [cs, ce), rank
+  const bf16* cb = nullptr;                        // and B pointer
+  bool half_next = false;                          // the issued step fills only its first 32 columns
+  auto load_step = [&](int part) {
+    const int start = part == 0 ? g_end : g_start;
+    int b[P + 1];
+    b[0] = start;
+#pragma unroll
+    for (int u = 1; u <= P; ++u) b[u] = b[u - 1] < BMT ? first_start_ge(b[u - 1] + 1) : BMT;
+    int used = 0, mt = -1;
+    cs = ce = BMT;
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      const bool has = b[u] < BMT;
+      const int t = has ? task_at(b[u]) : -1;
+      used += has ? cwc : 0;
+      if (u == slot) { cs = b[u]; ce = b[u + 1]; mt = t; }
+    }
+    g_start = start;
+    g_end = b[P];
+    half_next = used <= 4;
+    // the lane's projection: its slot's gate or up half (SwiGLU), else the block's
+    const int proj = SWIGLU ? (parts == 2 ? part : (q >= hc ? 1 : 0)) : lslot;
+    const void* const* tab = proj == 0 ? L.B[0] : proj == 1 ? L.B[1] : L.B[2];
+    cr = 0;
+    cb = nullptr;
+    if (mt >= 0) {
+      cr = min(L.rank[mt], L.max_rank) & ~7;
+      if (tab != nullptr) cb = (const bf16*)tab[mt];
+    }
   };
 
   f32x4 acc[FM][FN];
@@ -499,41 +525,26 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       return;
     }
     const int step = e - nk, part = step % parts;
-    if (part == 0) {                               // the next run becomes current
-      if (step > 0) cs = ce;
-      ce = first_start_ge(cs + 1);
-      take_run();
-      if (ce < BMT) {                              // run k+1 starts at ce
-        prefetch_run(v_nt);
-        const int ce2 = first_start_ge(ce + 1);
-        if (ce2 < BMT) load_task(ce2);             // run k+2
-      }
-    }
-    const int r = cr;
-    const int s0 = m0 + cs, s1 = min(m0 + ce, a.M);
+    load_step(part);
     const bf16* U = (const bf16*)L.U;
-    // A: the run's rows of U; 64 columns starting at the step's slot.  Only
-    // columns of slots the shrink wrote are read (the rest are zeroed in LDS),
-    // so stale workspace bytes never meet a zero of B.
-    int ucolA;
-    bool colA;
-    if (SWIGLU && rpad == 32) {
-      ucolA = L.ucol[0];
-      colA = (kc0 < 4) ? (L.B[0] != nullptr) : (L.B[1] != nullptr);
-    } else if (SWIGLU) {
-      ucolA = L.ucol[part];
-      colA = L.B[part] != nullptr;
-    } else {
-      ucolA = L.ucol[lslot];
-      colA = kc0 * 8 < rpad;
+    // this lane's chunk: projection (SwiGLU: gate or up) and chunk within it
+    int proj = 0, qq = q;
+    if (SWIGLU) {
+      if (parts == 2) proj = part;
+      else { proj = q >= hc ? 1 : 0; qq = q - proj * hc; }
     }
-    // with `half`, columns 32..63 are neither loaded nor read
-    const bool skip = half && kc0 >= 4;
+    // A: the run's rows of U at the slot's columns.  Only columns the shrink
+    // wrote are read (the rest are zeroed in LDS), so stale workspace bytes
+    // never meet a zero of B.
+    const int ucolA = L.ucol[SWIGLU ? proj : lslot] + qq * 8;
+    const bool colA = qq * 8 < (L.max_rank > 32 ? 64 : 32) && (!SWIGLU || (proj ? L.B[1] : L.B[0]) != nullptr);
+    // with a half step, columns 32..63 are neither loaded nor read
+    const bool skip = half_next && kc0 >= 4;
 #pragma unroll
     for (int i = 0; i < ACH; ++i) {
-      const int m = m0 + row0 + i * RSTEP;
-      const bool on = colA && m >= s0 && m < s1;
-      if (!skip) dma_or_zero(on, U + (int64_t)m * L.ldu + ucolA + kc0 * 8, As + (i * NW + wave) * 512);
+      const int row = row0 + i * RSTEP, m = m0 + row;
+      const bool on = colA && row >= cs && row < ce && m < a.M;
+      if (!skip) dma_or_zero(on, U + (int64_t)m * L.ldu + ucolA, As + (i * NW + wave) * 512);
     }
     // B: B_t rows of this block's output columns, zero past the rank
 #pragma unroll
@@ -543,16 +554,11 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       if (SWIGLU) {
         const int sub = row >> 4, which = sub & 1;
         const int j = n0 + (sub >> 1) * 16 + (row & 15);
-        int kc = kc0;
-        bool on;
-        if (L.max_rank > 32) on = (which == part) && L.B[part] != nullptr;
-        else { on = which ? (kc0 >= 4) : (kc0 < 4); kc = which ? kc0 - 4 : kc0; }
-        const bf16* Bt = which ? cb1 : cb0;
-        if (on && kc * 8 < r && j < a.N && Bt != nullptr) src = Bt + (int64_t)j * r + kc * 8;
+        if (which == proj && qq * 8 < cr && j < a.N && cb != nullptr) src = cb + (int64_t)j * cr + qq * 8;
       } else {
         const int nrow = n0 + row - lslot * L.slot_width;
-        if (kc0 * 8 < r && n0 + row < a.N && nrow < L.slot_width && cb0 != nullptr)
-          src = cb0 + (int64_t)nrow * r + kc0 * 8;
+        if (qq * 8 < cr && n0 + row < a.N && nrow < L.slot_width && cb != nullptr)
+          src = cb + (int64_t)nrow * cr + qq * 8;
       }
       if (!skip) dma_or_zero(src != nullptr, src, Bs + (i * NW + wave) * 512);
     }
@@ -600,11 +606,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     int nruns = 0;
 #pragma unroll
     for (int j = 0; j < RPL; ++j) nruns += __builtin_popcountll(rstart[j]);
-    nlora = nruns * parts;
+    nlora = (nruns + P - 1) / P * parts;
     nsteps = nk + nlora;
-    prefetch_run(__builtin_amdgcn_readfirstlane(rt[0]));   // the first run (row 0: lane 0, j = 0)
-    const int c1 = first_start_ge(1);
-    if (c1 < BMT) load_task(c1);                   // task of the second run
   }
   if (nk < 2) __builtin_amdgcn_s_waitcnt(0xF70);   // no backbone step covers them
   for (int e = 0; e + 1 < nk; ++e) {
@@ -613,9 +616,11 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
     __builtin_amdgcn_s_waitcnt(0xF70);
     __builtin_amdgcn_s_barrier();
   }
+  bool half_cur = false;                           // step e fills only its first 32 columns
   for (int e = nk - 1; e < nsteps; ++e) {
     if (e + 1 < nsteps) issue(e + 1);
-    compute(e, half && e >= nk);
+    compute(e, e >= nk && half_cur);
+    half_cur = half_next;
     __builtin_amdgcn_s_waitcnt(0x0070);   // vmcnt(0) lgkmcnt(0): DMA and zero writes done
     __builtin_amdgcn_s_barrier();
   }
@@ -906,7 +911,11 @@ void launch_large(const GemmArgs& a, hipStream_t s) {
   const int nt = SW ? BNT / 2 : BNT;
   const int ntiles = ((a.m_hi - a.m_lo + BMT - 1) / BMT) * ((a.N + nt - 1) / nt);
   const int grid = (ntiles + 7) / 8 * 8;
-  hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW, BMT, BNT>), dim3(grid), dim3(512), 0, s, a);
+  // ranks <= 16 share LoRA steps (up to four runs per step)
+  if (a.lora.enabled && a.lora.max_rank <= 16)
+    hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW, BMT, BNT, true>), dim3(grid), dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_bf16_large_kernel<EPI, SW, BMT, BNT, false>), dim3(grid), dim3(512), 0, s, a);
 }
 template <int EPI, bool SW>
 void launch_large_shape(const GemmArgs& a, const LargeShape& sh, hipStream_t s) {

@@ -53,7 +53,7 @@ def test_no_scratch_spills(all_asm):
 
 def test_large_gemm_keeps_lds_dma_in_flight(all_asm):
     ks = {k: v for k, v in _kernels(all_asm["k_gemm.hip"]).items() if "gemm_bf16_large_kernel" in k}
-    assert len(ks) == 12   # 4 epilogues x 3 tile shapes
+    assert len(ks) == 24   # 4 epilogues x 3 tile shapes x packed / one-run LoRA steps
     for name, body in ks.items():
         lines = [l.strip() for l in body.splitlines() if l.strip() and not l.strip().startswith(";")]
         assert any(l.startswith("global_load_lds_dwordx4") for l in lines), name

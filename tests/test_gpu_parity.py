@@ -192,6 +192,10 @@ INVARIANCE = {
     "2-tail": (2, dict(task_id=[0] * 14 + [5] * 14 + [9] * 8, seq_len=[197] * 36)),
     "4-tail": (4, dict(task_id=[1, 1, 9, 9, 9, 9], seq_len=[602, 602, 1024, 1024, 1024, 1024])),
     "4-mixlen": (4, dict(task_id=[1] * 6 + [9] * 4, seq_len=[200] * 6 + [300] * 4)),
+    # larger ranks take the unpacked LoRA steps of the large GEMM: half
+    # steps (rank <= 32) and, above 32, two steps per SwiGLU run
+    "2-tail-r32": (2, dict(task_id=[0] * 14 + [5] * 14 + [9] * 8, seq_len=[197] * 36), 32),
+    "4-tail-r64": (4, dict(task_id=[1, 1, 9, 9, 9, 9], seq_len=[602, 602, 1024, 1024, 1024, 1024]), 64),
 }
 
 
@@ -200,9 +204,9 @@ def test_batch_invariance_and_zero_rank_bit_exact(name):
     """A task's rows are bit-identical whether co-batched with other tasks or
     run alone (both batches on one side of the small-batch threshold), and a
     rank-0 task equals the bare backbone bit for bit."""
-    idx, case = INVARIANCE[name]
+    idx, case, *rank = INVARIANCE[name]
     w = wl.WORKLOADS[idx]
-    ranks = np.full(w.n_tasks, w.rank, np.int32)
+    ranks = np.full(w.n_tasks, rank[0] if rank else w.rank, np.int32)
     ranks[0] = 0
     w_, batch, model, inp, kv, pb, fwd, pl = _setup(idx, n_layers=1, ranks=ranks, b_std=0.1,
                                                     case=case)
@@ -378,6 +382,81 @@ def test_large_gemm_many_task_runs():
     worst = max(O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]) for p in range(batch.n_req))
     log(f"  max row rel err {worst:.3e}")
     assert worst < tol(w)
+
+
+@pytest.mark.parametrize("ranks", [(0, 8, 24, 32), (16, 40, 64, 8)])
+def test_large_gemm_ranks_above_16(ranks):
+    """The large GEMM's LoRA steps for ranks above 16 (one run per step:
+    half steps up to rank 32, and above 32 a SwiGLU run's gate and up
+    steps), over short requests of many tasks as in the test above.  B's
+    spread is scaled by sqrt(16 / largest rank), so the adapters' difference
+    has the size of a rank-16 adapter with B ~ N(0, 0.1), the strength the
+    bf16 tolerance is set for (a rank-r difference grows as sqrt(r))."""
+    b_std = 0.1 * np.sqrt(16 / max(ranks))
+    rng = np.random.default_rng(11)
+    n = 96
+    task_id = rng.integers(0, 64, size=n)
+    seq_len = 1 + (np.arange(n) * 7) % 25
+    rk = np.array([ranks[t % len(ranks)] for t in range(64)], np.int32)
+    case = dict(task_id=task_id.tolist(), seq_len=seq_len.tolist())
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(4, n_layers=1, b_std=b_std, ranks=rk, case=case)
+    assert pb.T >= 1024, pb.T
+    log(f"layer workload 4, ranks {ranks}, B ~ N(0, {b_std:.3f}), {n} short requests, T={pb.T}")
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    got = fwd.x.double().cpu().numpy()
+    res = oracle_layer_rows(w, oracle_weights(model.layers[0]), model.adapters[0], pl, x_in,
+                            range(batch.n_req))
+    cu = pl["cu_seqlens"]
+    worst = max(O.row_rel_error(got[cu[p]:cu[p + 1]], res[p][0]) for p in range(batch.n_req))
+    log(f"  max row rel err {worst:.3e}")
+    assert worst < tol(w)
+
+
+def test_packed_lora_steps_bit_exact():
+    """Runs of a tile share a LoRA step (up to four of rank <= 16): a task
+    whose rows sit among many one-row requests of other tasks (so its run
+    shares steps with theirs, in another slot than when alone) gives the
+    same bits as the task run alone, and matches the oracle; the one-row
+    requests match the oracle too."""
+    w = wl.WORKLOADS[4]
+    big = 9
+    singles_lo = list(range(1, 8))                  # its run is the eighth of the first tile
+    singles_hi = list(range(10, 51))                # 41 one-row runs after its last rows
+    task_id = singles_lo + [big] * 3 + singles_hi
+    seq_len = [1] * len(singles_lo) + [400] * 3 + [1] * len(singles_hi)
+    ranks = np.array([8 * (t % 3) for t in range(w.n_tasks)], np.int32)
+    ranks[big] = 16
+    case = dict(task_id=task_id, seq_len=seq_len)
+    w, batch, model, inp, kv, pb, fwd, pl = _setup(4, n_layers=1, b_std=0.1, ranks=ranks, case=case)
+    assert pb.T >= B.VFM_SMALL_BATCH_ROWS
+    log(f"layer workload 4, task {big} (1200 rows) among {len(singles_lo) + len(singles_hi)} one-row tasks")
+    x_in = as_f32(expected_embed(w, batch, inp, pl))
+    set_rows(fwd.x, x_in)
+    fwd.layer(0)
+    torch.cuda.synchronize()
+    mixed = fwd.x.cpu().numpy()
+    res = oracle_layer_rows(w, oracle_weights(model.layers[0]), model.adapters[0], pl, x_in,
+                            range(batch.n_req))
+    cu = pl["cu_seqlens"]
+    worst = max(O.row_rel_error(mixed[cu[p]:cu[p + 1]].astype(np.float64), res[p][0])
+                for p in range(batch.n_req))
+    log(f"  max row rel err {worst:.3e}")
+    assert worst < tol(w)
+    # the task alone: its requests in the same order, so its plan rows are
+    # the mixed plan's segment of that task
+    keep = [i for i, t in enumerate(task_id) if t == big]
+    sub = _batch(w, [big] * len(keep), [seq_len[i] for i in keep])
+    pbs = R.make_batch(w, sub, model.heads)
+    assert pbs.T >= B.VFM_SMALL_BATCH_ROWS
+    f2 = R.Forward(model, pbs, R.Inputs(w, sub))
+    seg = slice(int(pl["seg_row"][big]), int(pl["seg_row"][big + 1]))
+    set_rows(f2.x, x_in[seg])
+    f2.layer(0)
+    torch.cuda.synchronize()
+    assert np.array_equal(mixed[seg], f2.x.cpu().numpy())
 
 
 @pytest.mark.parametrize("idx", [1, 3, 4, 5])
