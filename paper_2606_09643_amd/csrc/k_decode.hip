@@ -261,7 +261,7 @@ __global__ __launch_bounds__(256) void shrink_split_kernel(Plan pl, ShrinkSplitA
 // others, so the kernel streams the partials.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
-  __shared__ float Us[3 * VFM_MAX_RANK];
+  __shared__ float Us[3 * VFM_MAX_RANK], red[256];
   __shared__ float rcs[64], rsn[64];          // the row's rotary angles (head_dim / 2 <= 64)
   // Block b takes (column block, row) number (b % 8) * per + b / 8, rows
   // fastest: consecutive blocks of one XCD (one L2) take consecutive rows of
@@ -275,7 +275,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   int t = 0, r = 0;
   if (a.lora.enabled) {                       // block-uniform
     t = a.lora.row_task[m];
-    r = fin_lora_u(a.lora, m, Us);
+    r = fin_lora_u(a.lora, m, Us, red);
   }
   if (a.rope.on) {                            // block-uniform: the row's angles, as launch_rope
     const int half = a.rope.head_dim >> 1;

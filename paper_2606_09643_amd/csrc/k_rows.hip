@@ -172,7 +172,7 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
                                                             const T* __restrict__ b, int kind, float eps,
                                                             T* __restrict__ h) {
   __shared__ float red[2][4];
-  __shared__ float Us[3 * VFM_MAX_RANK];
+  __shared__ float Us[3 * VFM_MAX_RANK], ured[256];
   // block b takes row (b % 8) * per + b / 8: consecutive rows (often one
   // task's) run on one XCD, so the task's B rows come from that XCD's L2
   const int per = gridDim.x / 8;
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
   int t = 0, r = 0;
   if (a.lora.enabled) {                       // block-uniform
     t = a.lora.row_task[row];
-    r = fin_lora_u(a.lora, row, Us);
+    r = fin_lora_u(a.lora, row, Us, ured);
   }
   float4 v[MAXC];
 #pragma unroll

@@ -325,27 +325,47 @@ struct FinalizeArgs {
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
 
 // The fused LoRA of the finalize pass for row m.  Every thread of the block
-// calls fin_lora_u: it fills Us[i * rpad + j] for the slots with adapters
-// and j < r (r = the row's task rank, returned) and ends with a barrier.
-__device__ __forceinline__ int fin_lora_u(const FinLora& L, int m, float* Us) {
+// calls fin_lora_u: it fills Us[i * rpad + j] = bf16(scale_t * sum over the
+// K chunks c of P[c, m, ucol[i] + j]) for the slots with adapters and j < r
+// (r = the row's task rank, returned) and ends with a barrier.  All threads
+// share the sums: thread q takes element (i, j) = q % (n_slots * r) and
+// chunk group q / (n_slots * r) of G = blockDim / (n_slots * r) groups
+// (chunks g, g + G, ... added in increasing order, 8 loads in flight), and
+// the G group sums are added in group order through red[blockDim].  The
+// order follows from the row's rank and the weight's K split alone, never
+// from the batch.
+__device__ __forceinline__ int fin_lora_u(const FinLora& L, int m, float* Us, float* red) {
   const int t = L.row_task[m];
   const int r = min(L.rank[t], L.max_rank) & ~7;
   const float sc = L.scale[t];
-  for (int q = threadIdx.x; q < L.n_slots * L.rpad; q += blockDim.x) {
-    const int i = q / L.rpad, j = q % L.rpad;
-    if (j >= r || L.B[i] == nullptr) continue;
-    const float* p = L.P + (int64_t)m * L.ldp + L.ucol[i] + j;
-    float s4[4] = {0.f, 0.f, 0.f, 0.f};
-    // 8 independent loads in flight per batch (chunks past the end add 0),
-    // summed in chunk order into the running sum of chunk index mod 4
-    for (int c0 = 0; c0 < L.kchunks; c0 += 8) {
-      float v[8];
+  const int ne = L.n_slots * r;                 // <= 3 * VFM_MAX_RANK = 192 < 256 threads
+  if (ne == 0) return r;                        // block-uniform: no slot reads Us
+  const int G = blockDim.x / ne;
+  const int q = threadIdx.x, g = q / ne, e = q - g * ne;
+  float s = 0.f;
+  if (g < G) {
+    const int i = e / r, j = e - i * r;
+    if (L.B[i] != nullptr) {
+      const float* p = L.P + (int64_t)m * L.ldp + L.ucol[i] + j;
+      for (int c0 = g; c0 < L.kchunks; c0 += 8 * G) {
+        float v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = c0 + e < L.kchunks ? p[(c0 + e) * L.cstride] : 0.f;
+        for (int k = 0; k < 8; ++k) {
+          const int c = c0 + k * G;
+          v[k] = c < L.kchunks ? p[(int64_t)c * L.cstride] : 0.f;
+        }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s4[e & 3] += v[e];
+        for (int k = 0; k < 8; ++k) s += v[k];
+      }
     }
-    Us[q] = (float)(bf16)(((s4[0] + s4[1]) + (s4[2] + s4[3])) * sc);
+  }
+  red[q] = s;
+  __syncthreads();
+  if (q < ne) {
+    float u = 0.f;
+    for (int k = 0; k < G; ++k) u += red[k * ne + q];
+    const int i = q / r, j = q - i * r;
+    Us[i * L.rpad + j] = (float)(bf16)(u * sc);
   }
   __syncthreads();
   return r;
