@@ -373,6 +373,8 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
   // set for the QKV projection of a small batch: the finalize applies RoPE
   // (and the cache write) itself
   FinRope fin_rope = {};
+  // set for the QKV projection of a large bf16 batch: the GEMM applies RoPE
+  GemmRope gemm_rope = {};
   auto project = [&](int cls, const void* X, int K, const void* W, const void* W2,
                      const void* bias, int N, int epi, void* out, int ldo,
                      std::initializer_list<int> projs, int slot_width, const void* norm_g = nullptr,
@@ -397,6 +399,7 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
       GemmArgs g = {};
       g.X = X; g.ldx = K; g.W = W; g.W2 = W2; g.bias = bias;
       g.M = T; g.N = N; g.K = K; g.epi = epi; g.out = out; g.ldo = ldo;
+      g.rope = gemm_rope;
       if (any) {
         GemmLora& L = g.lora;
         int i = 0;
@@ -470,10 +473,19 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
   // a5 (small bf16 batches): the QKV finalize also applies the rotary
   // embedding of q and k and, with a KV cache, writes each row's rotated k
   // and its v to its slot
+  // (large bf16 batches): the QKV GEMM's store pass rotates q and k, and the
+  // cache write is the attention launcher's plain copy
   const bool cache_write = k_cache != nullptr && c.attn != VFM_ATTN_BIDIR;
-  const bool rope_writes_kv = c.rope_theta > 0.f && cache_write;
-  const bool rope_in_finalize = skinny && c.dtype == VFM_BF16 && c.rope_theta > 0.f &&
-                                (c.head_dim == 64 || c.head_dim == 128) && d % 256 == 0;
+  const bool rope_fusable = c.dtype == VFM_BF16 && c.rope_theta > 0.f &&
+                            (c.head_dim == 64 || c.head_dim == 128) && d % 256 == 0;
+  const bool rope_in_finalize = skinny && rope_fusable;
+  const bool rope_in_gemm = !skinny && rope_fusable && T >= 1024 &&
+                            (int64_t)T * d < ((int64_t)1 << 31) && (int64_t)3 * d * d < ((int64_t)1 << 31);
+  const bool rope_writes_kv = c.rope_theta > 0.f && cache_write && !rope_in_gemm;
+  if (rope_in_gemm) {
+    gemm_rope.on = 1; gemm_rope.d = d; gemm_rope.head_dim = c.head_dim;
+    gemm_rope.log2_theta = log2f(c.rope_theta); gemm_rope.pos = pl.pos;
+  }
   if (rope_in_finalize) {
     fin_rope.on = 1; fin_rope.d = d; fin_rope.head_dim = c.head_dim; fin_rope.log2_theta = log2f(c.rope_theta);
     fin_rope.pl = pl; fin_rope.kp = kp; fin_rope.kv_slots = kv_slots;
@@ -484,9 +496,10 @@ int layer_impl(const vfm_cfg& c, const vfm_layer_weights* w, const vfm_lora_tabl
   VFM_TRY(project(VFM_PROF_GEMM_QKV, h, d, w->w_qkv, nullptr, w->b_qkv, 3 * d, EPI_STORE, qkv,
                   3 * d, {VFM_Q, VFM_K, VFM_V}, d));
   fin_rope = FinRope{};
+  gemm_rope = GemmRope{};
   // a5: rotary embedding of q and k
   // (with a KV cache the same pass writes each row's rotated k and its v)
-  if (c.rope_theta > 0.f && !rope_in_finalize)
+  if (c.rope_theta > 0.f && !rope_in_finalize && !rope_in_gemm)
     VFM_TIMED(VFM_PROF_OTHER, launch_rope(c.dtype, pl, qkv, d, c.n_heads, c.head_dim, c.rope_theta,
                                           rope_writes_kv ? k_cache : nullptr, rope_writes_kv ? v_cache : nullptr,
                                           kv_slots, kp, s));

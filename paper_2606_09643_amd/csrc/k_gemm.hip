@@ -23,6 +23,8 @@
 //
 // fp32 path: a plain LDS-tiled FMA GEMM with the same epilogues (the tiny
 // fp32 encoder workload only needs exactness, not speed).
+#include <type_traits>
+
 #include "vfm_internal.h"
 
 namespace {
@@ -256,6 +258,41 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
     }
     __syncthreads();
     bf16* out = (bf16*)a.out;
+    if (EPI == EPI_STORE && !SWIGLU && a.rope.on && n0 < 2 * a.rope.d) {   // block-uniform
+      // Rotary embedding of the q / k columns on the staged rows (the tile
+      // holds whole heads): a thread takes 8 columns i .. i + 7 of a head's
+      // first half and their partners i + head_dim / 2, rotates both in
+      // fp32 and stores both.  The angle pos * theta^(-2i / head_dim), in
+      // revolutions reduced to [0, 1), feeds the hardware sine and cosine.
+      const int hc = a.rope.head_dim / 8;            // 16-byte chunks per head
+      const int hh = hc / 2;
+      const float l2t = a.rope.log2_theta, inv_hd = 2.0f / (float)a.rope.head_dim;
+#pragma unroll 2
+      for (int e = tid; e < BMT * (QR / 2); e += NTH) {
+        const int r = e / (QR / 2), qq = e % (QR / 2);
+        const int q1 = (qq / hh) * hc + qq % hh, q2 = q1 + hh;
+        const int m = m0 + r;
+        const bf16x8 v1 = *reinterpret_cast<const bf16x8*>(T + r * NC + lds_chunk<QR>(r, q1) * 8);
+        const bf16x8 v2 = *reinterpret_cast<const bf16x8*>(T + r * NC + lds_chunk<QR>(r, q2) * 8);
+        if (m >= a.M) continue;
+        const float pf = (float)a.rope.pos[m];
+        const int i0 = (qq % hh) * 8;                // frequency index of the first column
+        bf16x8 o1, o2;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float x = pf * (exp2f(-(float)(i0 + j) * inv_hd * l2t) * 0.15915494309189535f);
+          const float fr = x - floorf(x);
+          const float cs = __builtin_amdgcn_cosf(fr), sn = __builtin_amdgcn_sinf(fr);
+          const float x1 = (float)v1[j], x2 = (float)v2[j];
+          o1[j] = (bf16)(x1 * cs - x2 * sn);
+          o2[j] = (bf16)(x2 * cs + x1 * sn);
+        }
+        bf16* orow = out + (int64_t)m * a.ldo + n0;
+        *reinterpret_cast<bf16x8*>(orow + q1 * 8) = o1;
+        *reinterpret_cast<bf16x8*>(orow + q2 * 8) = o2;
+      }
+      return;
+    }
 #pragma unroll 4
     for (int e = tid; e < BMT * QR; e += NTH) {
       const int r = e / QR, q = e % QR;
@@ -863,8 +900,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 // not depend on which launch or tile shape computes it.
 struct LargeShape { int bm, bn; };
 constexpr LargeShape kLargeShapes[3] = {{256, 256}, {256, 192}, {256, 128}};
-inline bool shape_ok(const LargeShape& c, bool sw, int lora_slot_width) {
-  return !(lora_slot_width > 0 && !sw && lora_slot_width % c.bn);
+inline bool shape_ok(const LargeShape& c, bool sw, int lora_slot_width, int rope_hd) {
+  return !(lora_slot_width > 0 && !sw && lora_slot_width % c.bn) && !(rope_hd > 0 && c.bn % rope_hd);
 }
 inline double launch_cost(int rows, int N, bool sw, const LargeShape& c) {
   if (rows <= 0) return 0.0;
@@ -874,11 +911,11 @@ inline double launch_cost(int rows, int N, bool sw, const LargeShape& c) {
   return (double)rounds * (c.bm + c.bn) * (sw ? 2.0 * nt / c.bn : 1.0);
 }
 struct LargePlan { LargeShape main, tail; int m1; };   // rows [0, m1) main, [m1, M) tail
-inline LargePlan large_plan(int M, int N, bool sw, int lora_slot_width) {
+inline LargePlan large_plan(int M, int N, bool sw, int lora_slot_width, int rope_hd) {
   LargePlan best = {{0, 0}, {0, 0}, M};
   double best_cost = 0.0;
   for (const LargeShape& c : kLargeShapes) {
-    if (!shape_ok(c, sw, lora_slot_width)) continue;
+    if (!shape_ok(c, sw, lora_slot_width, rope_hd)) continue;
     const double cost = launch_cost(M, N, sw, c);
     if (best.main.bm == 0 || cost < best_cost * 0.97) { best = {c, {0, 0}, M}; best_cost = cost; }
   }
@@ -898,7 +935,7 @@ inline LargePlan large_plan(int M, int N, bool sw, int lora_slot_width) {
     const int m1 = r1 * mc.bm;
     if (m1 >= M) continue;
     for (const LargeShape& t : kLargeShapes) {
-      if (!shape_ok(t, sw, lora_slot_width)) continue;
+      if (!shape_ok(t, sw, lora_slot_width, rope_hd)) continue;
       const double cost = launch_cost(m1, N, sw, mc) + launch_cost(M - m1, N, sw, t);
       if (cost < single * 0.985 && cost < best_cost) { best = {mc, t, m1}; best_cost = cost; }
     }
@@ -926,7 +963,9 @@ void launch_large_shape(const GemmArgs& a, const LargeShape& sh, hipStream_t s) 
 
 template <int EPI, bool SW>
 hipError_t launch_one(int dtype, const GemmArgs& a0, hipStream_t s) {
-  const LargePlan pl = large_plan(a0.M, a0.N, SW, a0.lora.enabled ? a0.lora.slot_width : 0);
+  // the fused rotary embedding needs whole heads in a tile
+  const LargePlan pl = large_plan(a0.M, a0.N, SW, a0.lora.enabled ? a0.lora.slot_width : 0,
+                                  a0.rope.on ? a0.rope.head_dim : 0);
   const bool fits32 = (int64_t)a0.M * a0.ldx < ((int64_t)1 << 31) && (int64_t)a0.N * a0.K < ((int64_t)1 << 31);
   if (dtype == VFM_BF16 && a0.M >= 1024 && pl.main.bm > 0 && fits32) {
     GemmArgs a = a0;
@@ -938,6 +977,8 @@ hipError_t launch_one(int dtype, const GemmArgs& a0, hipStream_t s) {
       a.m_hi = a0.M;
       launch_large_shape<EPI, SW>(a, pl.tail, s);
     }
+  } else if (a0.rope.on) {
+    return hipErrorInvalidValue;   // only the large-tile kernel applies the rotary embedding
   } else if (dtype == VFM_BF16) {
     const GemmArgs& a = a0;
     const int nt = SW ? BN / 2 : BN;

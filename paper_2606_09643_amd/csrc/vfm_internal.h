@@ -233,6 +233,16 @@ struct GemmLora {
   const int32_t* rank; const int32_t* row_task; const int32_t* seg_row;
   int max_rank;
 };
+// Rotary embedding applied by the QKV GEMM of a large bf16 batch (EPI_STORE):
+// rotate-half of the q and k columns (the first 2d) per head of head_dim
+// columns at each row's position pos[m], in the epilogue's store pass on the
+// staged bf16 sums (rounded again after the rotation, as a separate pass
+// over q and k would).  Needs head_dim 64 or 128 and d a multiple of 256;
+// the launcher then picks tiles whose width is a multiple of head_dim.
+struct GemmRope {
+  int on; int d; int head_dim; float log2_theta;
+  const int32_t* pos;
+};
 struct GemmArgs {
   const void* X; int ldx;
   const void* W; const void* W2;   // W2: SwiGLU up weights
@@ -241,6 +251,7 @@ struct GemmArgs {
   int epi;
   void* out; int ldo;              // EPI_STORE/GELU/SWIGLU (dtype) or EPI_RESID (fp32)
   GemmLora lora;
+  GemmRope rope;
   int m_lo, m_hi;                  // rows one large-tile launch covers (set by launch_gemm)
 };
 hipError_t launch_gemm(int dtype, const GemmArgs& a, hipStream_t s);
