@@ -57,7 +57,9 @@ __device__ __forceinline__ void wait_vm() {
 
 template <int NWN, int WST>
 __global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
-  constexpr int BN = 64 * NWN, NW = 4 * NWN, XW = NW / 2, WW = NW - XW;
+  // loader waves: half for each operand, except 192 columns (12 waves), whose
+  // 256 activation rows need a power-of-two share (8 activation, 4 weight)
+  constexpr int BN = 64 * NWN, NW = 4 * NWN, XW = NWN == 3 ? 8 : NW / 2, WW = NW - XW;
   constexpr int SA = SBM * SBK, SB = BN * SBK;
   constexpr int XR = SBM / (8 * XW), WR = BN / (8 * WW);    // 1 KB rounds per stage and loader wave
   static_assert(XR * 8 * XW == SBM && WR * 8 * WW == BN, "loader rounds");
@@ -363,19 +365,32 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
 }
 
 // Column-tile width and K split of the small-batch GEMM for an N x K
-// weight: wide weights (N >= 8192) take 256-column tiles, narrow ones
-// 128-column tiles, and K is split until one row tile fills the chip once
-// (one block per CU), at most 6 ways for wide weights so the fp32 partials
-// stay below the weight bytes.  The split depends on the weight shape only,
-// never on the batch, so a row's result does not depend on the other rows.
+// weight: for each tile width (128, 192, 256 columns) K is split until one
+// row tile fills the chip once (one block per CU), at most 6 ways for wide
+// weights (N >= 8192) so the fp32 partials stay below the weight bytes; the
+// width whose blocks each stream the fewest weight bytes wins (the 7B
+// gate/up weight: 230 blocks of 192 columns instead of 172 of 256).  The
+// split depends on the weight shape only, never on the batch, so a row's
+// result does not depend on the other rows.
 void skinny_shape(int N, int K, int* bn, int* nsplit) {
   const int nkt = K / SBK;
   const bool wide = N >= 8192;
-  const int b = wide ? 256 : 128;
-  const int tiles = (N + b - 1) / b;
   const int cap = wide ? 6 : 16;
-  *bn = b;
-  *nsplit = std::max(1, std::min(std::min(256 / tiles, cap), nkt));
+  // the tile width whose one round of blocks streams the fewest weight
+  // steps per block (rounds x width x K steps of a split); ties go to fewer
+  // splits (fewer partial bytes)
+  long best = -1;
+  for (const int b : {128, 192, 256}) {
+    const int tiles = (N + b - 1) / b;
+    const int ns = std::max(1, std::min(std::min(256 / tiles, cap), nkt));
+    const long rounds = ((long)tiles * ns + 255) / 256;
+    const long cost = rounds * b * ((nkt + ns - 1) / ns);
+    if (best < 0 || cost < best || (cost == best && ns < *nsplit)) {
+      best = cost;
+      *bn = b;
+      *nsplit = ns;
+    }
+  }
 }
 
 }  // namespace
@@ -395,6 +410,8 @@ hipError_t launch_gemm_skinny(const SkinnyArgs& a0, hipStream_t s) {
   dim3 grid((ntn * a.nsplit + 7) & ~7, (a.M + SBM - 1) / SBM);
   if (bn == 128)
     hipLaunchKernelGGL((gemm_skinny_kernel<2, 4>), grid, dim3(512), 0, s, a);
+  else if (bn == 192)
+    hipLaunchKernelGGL((gemm_skinny_kernel<3, 4>), grid, dim3(768), 0, s, a);
   else
     hipLaunchKernelGGL((gemm_skinny_kernel<4, 3>), grid, dim3(1024), 0, s, a);
   return hipGetLastError();
