@@ -6,6 +6,8 @@ the row-normwise relative error (max over rows of max|g - o| / max|o|):
 2e-2 for bf16 workloads, 1e-5 for the fp32 one.  Integer plan outputs are
 checked bit-exact on the host (tests/test_abi_cpu.py).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -527,8 +529,23 @@ def test_prefill_writes_kv_cache(rope):
     cache: with RoPE the rotation pass writes them, without it the cache-write
     kernel does.  Slots between the requests keep their previous contents.
     Decoder layer, ragged prompts (1, 130, 64, 77 tokens)."""
-    w = wl.WORKLOADS[4]
-    case = SMALL[4]
+    _prefill_with_cache(wl.WORKLOADS[4], SMALL[4], rope)
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_large_batch_rope_in_gemm_with_cache(hd):
+    """A batch above the small-batch threshold on a decoder of width 1024
+    with head_dim 64 or 128: the QKV GEMM's store pass applies RoPE (tiles
+    holding whole heads) and the cache-write kernel copies the rotated keys
+    and the values to the cache.  Outputs and cached K / V against the
+    oracle, gap slots untouched; ragged prompts of 300, 1, 513 and 260."""
+    w = dataclasses.replace(wl.WORKLOADS[4], d=1024, n_heads=1024 // hd, head_dim=hd, d_ff=2816, n_tasks=8)
+    case = dict(task_id=[3, 0, 7, 3], seq_len=[300, 1, 513, 260])
+    assert sum(case["seq_len"]) >= B.VFM_SMALL_BATCH_ROWS
+    _prefill_with_cache(w, case, True)
+
+
+def _prefill_with_cache(w, case, rope):
     batch = _batch(w, **case)
     model = R.Model(w, n_layers=1, b_std=0.1)
     inp = R.Inputs(w, batch)
@@ -546,7 +563,7 @@ def test_prefill_writes_kv_cache(rope):
     sentinel = 7.0
     kc = torch.full((w.n_heads, slots, w.head_dim), sentinel, dtype=torch.bfloat16, device="cuda")
     vc = torch.full_like(kc, sentinel)
-    log(f"prefill layer with KV cache, rope={rope}, T={pb.T}, slots={slots}")
+    log(f"prefill layer with KV cache, d={w.d}, head_dim={w.head_dim}, rope={rope}, T={pb.T}, slots={slots}")
     pl = oracle_plan(w, batch)
     x_in = as_f32(expected_embed(w, batch, inp, pl))
     set_rows(fwd.x, x_in)
