@@ -360,12 +360,12 @@ __device__ __forceinline__ void epilogue_lds(const GemmArgs& a, char* lds, int m
 // so that the last round of tiles fills the 256 CUs as far as possible.
 //
 // The per-task LoRA expand runs as extra 64-wide K steps of the same
-// pipeline: for every task t with rows in the tile, the A tile holds the
-// shrink outputs U[m, slot cols] of t's rows (rows of other tasks come from a
-// zero page) and the B tile holds B_t[n, :r_t] (zero past the rank).  For a
-// SwiGLU block the A tile is [U_gate | U_up] and gate rows of B carry B_gate
-// in the low 32 columns, up rows carry B_up in the high 32.  The MFMA loop
-// cannot tell these steps from the backbone's.
+// pipeline: for the tasks t with rows in the tile, the A tile holds the
+// shrink outputs U[m, slot cols] of t's rows (rows of other tasks zero) and
+// the B tile holds B_t[n, :r_t] (zero past the rank); with ranks <= 16 up to
+// four tasks share a step, each in its own 16 columns (SwiGLU: two, 16 gate
+// and 16 up columns each).  The MFMA loop cannot tell these steps from the
+// backbone's.
 // ---------------------------------------------------------------------------
 constexpr int LGM = 4;
 
@@ -443,8 +443,8 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
   // outside its own slot has a zero operand, so its sum does not depend on
   // which runs share its step.  A lane's 16-byte chunk of a step row is
   // fixed for the tile, and so is its slot.  A group's task ids come from
-  // the tile's row tasks (registers), its ranks and B pointers from the
-  // small per-task tables, which the scalar cache holds.
+  // the tile's row tasks (registers); each lane reads its slot's rank and B
+  // pointer from the small per-task tables (cache hits after the first).
   const int nk = a.K / BK;
   constexpr int RPL = BMT / 64;                    // tile rows per lane
   static_assert(BMT % 64 == 0, "rows per lane");
@@ -485,10 +485,9 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_large_kernel(GemmArgs a) {
       if (r % RPL == j) t = __builtin_amdgcn_readlane(rt[j], r / RPL);
     return t;
   };
-  // The current step's group (wave-uniform): where it starts and ends
-  // (g_start == g_end: no group yet).  A group's ranks and B pointers are
-  // read when its first step is issued, from the small per-task tables (the
-  // scalar cache holds them), its task ids straight from the tile's row tasks.
+  // The current step's group (wave-uniform): the tile rows where it starts
+  // and where the next one starts; read when the group's first step is
+  // issued (a SwiGLU group of a rank above 32 takes two steps).
   int g_start = 0, g_end = 0;
   int cs = 0, ce = 0, cr = 0;                      // this lane's run: tile rows [cs, ce), rank
   const bf16* cb = nullptr;                        // and B pointer
