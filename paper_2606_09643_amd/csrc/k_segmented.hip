@@ -36,29 +36,81 @@ typedef const void __attribute__((address_space(1)))* gptr_t;
 typedef void __attribute__((address_space(3)))* lptr_t;
 __device__ __attribute__((aligned(16))) bf16 g_seg_zero[8];  // zero-initialised at load
 
-template <int NP, int NSUB>
-__global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
-  // One block per 64-row tile of one task; wave w owns 16 rows and every
-  // projection of the group, so each row is read once for all of them.  Each
-  // 64-column chunk of the task's A rows (shared by the 4 waves) and of the
-  // tile's 64 activation rows goes through an LDS ring of NST stages fed by
-  // global_load_lds: every wave-wide load moves 8 whole 128-byte rows, and
-  // NST - 1 chunks are in flight while one is consumed.  A rows past the rank
-  // come from a zero page; only the NSUB 16-row sub-tiles that the largest
-  // rank reaches are computed.  LDS rows are 128 B with chunk swizzle
-  // kc ^ ((row >> 1) & 7); a stage holds ARD A rows, then the 64 X rows.
+// The task owning tile `tile` of the tiling that cuts each task's rows into
+// ceil(rows_t / ROWS) tiles, in task order, and the tile's first row; one
+// wave counts the tiles (each lane a contiguous run of tasks, then a prefix
+// over the lanes) and the lane holding the tile finds it.  Returns false
+// (block-uniform) past the last tile.  sl: 2 ints of LDS.
+template <int ROWS>
+__device__ inline bool rows_tile_task(const Plan& pl, int tile, int* sl, int* t_out, int* r0_out) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x, n = pl.n_tasks;
+    if (lane == 0) sl[0] = -1;
+    const int per = (n + 63) / 64;
+    const int t0 = min(lane * per, n), t1 = min(t0 + per, n);
+    int cnt = 0;
+    for (int t = t0; t < t1; ++t) cnt += (pl.seg_row[t + 1] - pl.seg_row[t] + ROWS - 1) / ROWS;
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += v;
+    }
+    int off = incl - cnt;
+    if (tile >= off && tile < incl) {
+      for (int t = t0; t < t1; ++t) {
+        const int nt = (pl.seg_row[t + 1] - pl.seg_row[t] + ROWS - 1) / ROWS;
+        if (tile < off + nt) {
+          sl[0] = t;
+          sl[1] = pl.seg_row[t] + (tile - off) * ROWS;
+          break;
+        }
+        off += nt;
+      }
+    }
+  }
+  __syncthreads();
+  *t_out = sl[0];
+  *r0_out = sl[1];
+  return *t_out >= 0;
+}
+
+template <int NP, int NSUB, int NWV>
+__global__ __launch_bounds__(64 * NWV) void shrink_bf16_kernel(Plan pl, ShrinkArgs a) {
+  // One block per tile of 16 * NWV rows of one task (the plan's 64-row tiles
+  // with 4 waves; 96-row tiles with 6 when the batch has more 64-row tiles
+  // than CUs, so one round of blocks covers it); wave w owns 16 rows and
+  // every projection of the group, so each row is read once for all of
+  // them.  Each 64-column chunk of the task's A rows (shared by the waves)
+  // and of the tile's activation rows goes through an LDS ring of NST stages
+  // fed by global_load_lds: every wave-wide load moves 8 whole 128-byte rows,
+  // and NST - 1 chunks are in flight while one is consumed.  A rows past the
+  // rank come from a zero page; only the NSUB 16-row sub-tiles that the
+  // largest rank reaches are computed.  LDS rows are 128 B with chunk
+  // swizzle kc ^ ((row >> 1) & 7); a stage holds AR A rows, then the tile's
+  // rows, then padding to whole block passes.  A row's sums are the same
+  // MFMAs in the same order for either tile size.
+  static_assert(NWV == 4 || NWV == 6, "the swizzle repeats every block pass for an even wave count");
+  constexpr int ROWS = 16 * NWV;                // activation rows per block
   constexpr int AR = NP * NSUB * 16;            // A rows the MFMAs read per chunk
-  constexpr int ARD = (AR + 31) / 32 * 32;      // A rows fetched (one block pass moves 32)
-  constexpr int SR = ARD + VFM_ROW_TILE;        // LDS rows per stage
+  constexpr int PR = 8 * NWV;                   // LDS rows one block pass of 16-byte loads fills
+  constexpr int SR = (AR + ROWS + PR - 1) / PR * PR;   // LDS rows per stage
   constexpr int NST = 4;
-  constexpr int ND = SR / 32;                   // 16-byte pieces per thread and chunk
+  constexpr int ND = SR / PR;                   // 16-byte pieces per thread and chunk
+  static_assert(NWV != 4 || ROWS == VFM_ROW_TILE, "the plan's row tiles");
   // one LDS object (the task slot sits past the ring): with a second one the
   // compiler would wait for the ring's DMA before every fragment read
   __shared__ __attribute__((aligned(16))) bf16 As[NST][SR * 64 + 8];
+  int* const sl = reinterpret_cast<int*>(&As[NST - 1][SR * 64]);
   const int tile = blockIdx.x;
-  const int t = block_tile_task(pl, tile, reinterpret_cast<int*>(&As[NST - 1][SR * 64]));
-  const int r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
-  const int r1 = min(r0 + VFM_ROW_TILE, pl.seg_row[t + 1]);
+  int t, r0;
+  if (NWV == 4) {
+    t = block_tile_task(pl, tile, sl);
+    r0 = pl.seg_row[t] + (tile - pl.rtile_off[t]) * VFM_ROW_TILE;
+  } else if (!rows_tile_task<ROWS>(pl, tile, sl, &t, &r0)) {
+    return;                                     // block-uniform: past the last tile
+  }
+  const int r1 = min(r0 + ROWS, pl.seg_row[t + 1]);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rank = min(a.rank[t], NSUB * 16) & ~7;
   const float sc = a.scale[t];
@@ -73,15 +125,17 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
   if (rank > 0) {   // block-uniform
     const bf16* src0[ND];
     const int prow0 = wave * 8 + (lane >> 3);
-    const int kcl = (lane & 7) ^ ((prow0 >> 1) & 7);   // same for prow0 + 32 i
+    const int kcl = (lane & 7) ^ ((prow0 >> 1) & 7);   // same for prow0 + PR i
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
-      const int row = prow0 + i * 32;
-      if (row < ARD) {                                  // row = (pp*NSUB + s2)*16 + j
+      const int row = prow0 + i * PR;
+      if (row < AR) {                                   // row = (pp*NSUB + s2)*16 + j
         const int pp = row / (NSUB * 16), j = row % (NSUB * 16);
-        src0[i] = row < AR && j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
-      } else {                                          // rows past the tile's end re-read its last row
-        src0[i] = X + (int64_t)min(r0 + row - ARD, r1 - 1) * a.ldx + kcl * 8;
+        src0[i] = j < rank ? (const bf16*)a.A[pp][t] + (int64_t)j * a.K + kcl * 8 : nullptr;
+      } else if (row < AR + ROWS) {                     // rows past the tile's end re-read its last row
+        src0[i] = X + (int64_t)min(r0 + row - AR, r1 - 1) * a.ldx + kcl * 8;
+      } else {
+        src0[i] = nullptr;                              // padding rows (never read)
       }
     }
     const int nc = a.K / 64;
@@ -92,7 +146,7 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
 #pragma unroll
       for (int i = 0; i < ND; ++i) {
         const bf16* src = src0[i] ? src0[i] + cc * 64 : g_seg_zero;
-        __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(&As[st][(i * 4 + wave) * 512]), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(&As[st][(i * NWV + wave) * 512]), 16, 0, 0);
       }
     };
 #pragma unroll
@@ -110,7 +164,7 @@ __global__ __launch_bounds__(256) void shrink_bf16_kernel(Plan pl, ShrinkArgs a)
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
           const int kc = kk * 4 + (lane >> 4);
-          const int xr = ARD + wave * 16 + (lane & 15);
+          const int xr = AR + wave * 16 + (lane & 15);
           const bf16x8 xf = *reinterpret_cast<const bf16x8*>(Ab + xr * 64 + ((kc ^ ((xr >> 1) & 7)) * 8));
 #pragma unroll
           for (int pp = 0; pp < NP; ++pp)
@@ -447,10 +501,17 @@ __global__ __launch_bounds__(256) void greedy_kernel(Plan pl, const float* __res
 hipError_t launch_lora_shrink(int dtype, const Plan& pl, const ShrinkArgs& a, hipStream_t s) {
   if (pl.n_rtiles == 0 || a.n_proj == 0) return hipSuccess;
   if (dtype == VFM_BF16) {
-    dim3 grid(pl.n_rtiles);
+    // the plan's 64-row tiles while one round of blocks holds them, else
+    // 96-row tiles (a bound on their count; blocks past the last one leave)
+    const bool big = pl.n_rtiles > 256;
+    const dim3 grid(big ? (pl.T + 95) / 96 + std::min(pl.n_tasks, pl.n_req) : pl.n_rtiles);
     // sub-tiles the table's ranks need: 1 (rank <= 16), 2 (<= 32) or 4
     const int ns = a.nsub <= 1 ? 1 : (a.nsub == 2 ? 2 : 4);
-#define SHR(NP_, NS_) hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_>), grid, dim3(256), 0, s, pl, a)
+#define SHR(NP_, NS_)                                                                              \
+  do {                                                                                             \
+    if (big) hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_, 6>), grid, dim3(384), 0, s, pl, a); \
+    else hipLaunchKernelGGL((shrink_bf16_kernel<NP_, NS_, 4>), grid, dim3(256), 0, s, pl, a);     \
+  } while (0)
 #define SHR_NP(NS_) do { if (a.n_proj == 1) SHR(1, NS_); else if (a.n_proj == 2) SHR(2, NS_); else SHR(3, NS_); } while (0)
     if (ns == 1) SHR_NP(1);
     else if (ns == 2) SHR_NP(2);

@@ -194,6 +194,10 @@ INVARIANCE = {
     "2-tail": (2, dict(task_id=[0] * 14 + [5] * 14 + [9] * 8, seq_len=[197] * 36)),
     "4-tail": (4, dict(task_id=[1, 1, 9, 9, 9, 9], seq_len=[602, 602, 1024, 1024, 1024, 1024])),
     "4-mixlen": (4, dict(task_id=[1] * 6 + [9] * 4, seq_len=[200] * 6 + [300] * 4)),
+    # 17 000 rows: more 64-row tiles than CUs, so the large-batch LoRA shrink
+    # takes 96-row tiles, while each task alone (12 000 / 5 000 rows) keeps
+    # the plan's 64-row tiles
+    "4-big": (4, dict(task_id=[1] * 12 + [9] * 5, seq_len=[1000] * 17)),
     # larger ranks take the unpacked LoRA steps of the large GEMM: half
     # steps (rank <= 32) and, above 32, two steps per SwiGLU run
     "2-tail-r32": (2, dict(task_id=[0] * 14 + [5] * 14 + [9] * 8, seq_len=[197] * 36), 32),
