@@ -1,8 +1,11 @@
 """Batch-aware fair queueing (BFQ): the oracle against what the paper and
 the mathematics fix, and the library's scheduler (C ABI, host only) against
 the oracle, decision by decision.  CPU only."""
+import json
 import math
+import os
 import time
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -17,29 +20,70 @@ INF = float("inf")
 # oracle pins
 # --------------------------------------------------------------------------
 
-def test_oracle_tags_follow_eq_1_2_and_the_eq_3_retagging():
-    """A worked example by hand.  Weights (1, 2), T(1) = 1, T(2) = 1.5,
-    T(3) = 2, b_max 3.  Arrivals (all at v = 0): task 0 r10, task 1 r11,
-    task 1 r12, task 0 r13.
-      Eq. 1-2: r10 S 0 F 1;  r11 S 0 F 0.5;  r12 S 0.5 F 1;  r13 S 1 F 2.
-      Batch in start-tag order (ties: lower task): r10, r11, r12 (b = 3).
-      Eq. 3 with l(3) = 2/3: task 0: r10 S 0 F 2/3, then queued r13 S 2/3
-      F 4/3; task 1: r11 S 0 F 1/3, r12 S 1/3 F 2/3.  v = max(2/3, 2/3).
-      A request of task 1 arriving now: S = max(2/3, v) = 2/3, F = 2/3 + 1/2."""
-    q = BO.BFQ([1.0, 2.0], [0.0, 1.0, 1.5, 2.0], 3)
-    q.enqueue(0, 10, 0.0, INF)
-    q.enqueue(1, 11, 0.0, INF)
-    q.enqueue(1, 12, 0.0, INF)
-    q.enqueue(0, 13, 0.0, INF)
-    tags = [(r.req, r.S, r.F) for qq in q.queues for r in qq]
-    assert tags == [(10, 0.0, 1.0), (13, 1.0, 2.0), (11, 0.0, 0.5), (12, 0.5, 1.0)]
-    assert q.next_batch(0.0) == [(10, 0), (11, 1), (12, 1)]
-    r13 = q.queues[0][0]
-    assert math.isclose(r13.S, 2 / 3) and math.isclose(r13.F, 4 / 3)
-    assert math.isclose(q.v(), 2 / 3)
-    q.enqueue(1, 14, 1.0, INF)
-    r14 = q.queues[1][0]
-    assert math.isclose(r14.S, 2 / 3) and math.isclose(r14.F, 2 / 3 + 0.5)
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "bfq_worked_examples.json")
+
+
+def _worked_examples():
+    with open(GOLDEN) as f:
+        return json.load(f)["examples"]
+
+
+class _OracleView:
+    """The oracle's scheduler behind the library binding's query calls."""
+
+    def __init__(self, weights, batch_time, b_max):
+        self.q = BO.BFQ(weights, batch_time, b_max)
+
+    def enqueue(self, task, req, arrival):
+        self.q.enqueue(task, req, arrival, INF)
+
+    def next_batch(self, now):
+        return self.q.next_batch(now)
+
+    def charge(self, task, service):
+        self.q.charge(task, service)
+
+    def queued(self, task):
+        return self.q.queued(task)
+
+    def tags(self, task, k):
+        r = self.q.queues[task][k]
+        return r.S, r.F
+
+    def v(self):
+        return self.q.v()
+
+
+@pytest.mark.parametrize("impl", ["oracle", "library"])
+@pytest.mark.parametrize("ex", _worked_examples(), ids=lambda e: e["name"])
+def test_worked_examples_by_hand(ex, impl):
+    """The hand-worked tag sequences of tests/golden/bfq_worked_examples.json
+    (Eq. 1-2 tags, the Eq. 3 re-tagging after a batch, token-level charging;
+    Section 4.2), replayed step by step on the oracle and on the library.
+    The global tag v is checked on the oracle (the library shows it through
+    the tags of later arrivals)."""
+    fr = lambda x: float(Fraction(x))
+    w = [fr(x) for x in ex["weights"]]
+    t = [fr(x) for x in ex["batch_time"]]
+    q = _OracleView(w, t, ex["b_max"]) if impl == "oracle" else B.BFQ(w, t, ex["b_max"])
+    for i, st in enumerate(ex["steps"]):
+        op, where = st[0], f"{ex['name']} step {i}: {st}"
+        if op == "enqueue":
+            q.enqueue(st[1], st[2], fr(st[3]))
+        elif op == "batch":
+            assert q.next_batch(fr(st[1])) == [tuple(x) for x in st[2]], where
+        elif op == "charge":
+            q.charge(st[1], fr(st[2]))
+        elif op == "tags":
+            assert q.queued(st[1]) == len(st[2]), where
+            for k, (s_, f_) in enumerate(st[2]):
+                s, f = q.tags(st[1], k)
+                assert math.isclose(s, fr(s_), abs_tol=1e-12) and math.isclose(f, fr(f_), abs_tol=1e-12), where
+        elif op == "v":
+            if impl == "oracle":
+                assert math.isclose(q.v(), fr(st[1]), abs_tol=1e-12), where
+        else:
+            raise AssertionError(f"unknown step {op}")
 
 
 @pytest.mark.parametrize("weights", [[1.0, 1.0], [1.0, 2.0, 4.0], [0.5, 1.0, 2.0, 4.0], [4.0, 1.0]])
@@ -271,34 +315,6 @@ def test_library_decision_time():
     dt = spent / reps
     print(f"BFQ: {dt * 1e6:.1f} us per batch decision ({n_tasks} tasks, b_max {b_max}, 512 queued)")
     assert dt < 1e-3
-
-
-def test_oracle_token_charge_worked_example():
-    """Token-level work charged in service-time units (Section 4.2,
-    token-based FMs), by hand.  Weights (1, 2), T(1) = 1, b_max 1.  r0 of
-    task 0 and r1 of task 1 arrive at v = 0: r0 S 0 F 1, r1 S 0 F 0.5.  The
-    first batch takes r0 (tie -> lower task) and re-tags it with l(1) = 1:
-    F 1; v = 1.  Task 0 then produces decode tokens worth 3 time units:
-    charge(0, 3) moves its finish tag to 1 + 3/1 = 4, v = 4.  A new request
-    of task 0 (arriving now) gets S = max(4, 4) = 4, F = 5.  A charge of 1
-    unit to task 1 (nothing dispatched yet) moves its queued r1 to
-    S = max(0 + 1/2, v at its arrival = 0) = 0.5, F = 1, so r1 goes first,
-    then task 0's new request."""
-    q = BO.BFQ([1.0, 2.0], [0.0, 1.0], 1)
-    q.enqueue(0, 0, 0.0, INF)
-    q.enqueue(1, 1, 0.0, INF)
-    assert q.next_batch(0.0) == [(0, 0)]
-    assert math.isclose(q.v(), 1.0)
-    q.charge(0, 3.0)
-    assert math.isclose(q.f_disp[0], 4.0) and math.isclose(q.v(), 4.0)
-    q.enqueue(0, 2, 1.0, INF)
-    r2 = q.queues[0][0]
-    assert (r2.S, r2.F) == (4.0, 5.0)
-    q.charge(1, 1.0)
-    r1 = q.queues[1][0]
-    assert (r1.S, r1.F) == (0.5, 1.0)
-    assert q.next_batch(1.0) == [(1, 1)]
-    assert q.next_batch(2.0) == [(2, 0)]
 
 
 def test_oracle_charging_every_token_keeps_weighted_shares():
