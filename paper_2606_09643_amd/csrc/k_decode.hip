@@ -113,11 +113,12 @@ __global__ __launch_bounds__(256 * NWN) void gemm_skinny_kernel(SkinnyArgs a) {
       __builtin_amdgcn_global_load_lds((gptr_t)(src[i] + j * SBK),
                                        (lptr_t)(Xs + (j & 1) * SA + (i * XW + lw) * 512), 16, 0, 0);
   };
+  // the weights are read once per forward: nontemporal (cache policy 2, nt)
   auto issue_w = [&](int j, int slot) {
 #pragma unroll
     for (int i = 0; i < WR; ++i)
       __builtin_amdgcn_global_load_lds((gptr_t)(src[i] + j * SBK),
-                                       (lptr_t)(Ws + slot * SB + (i * WW + lw) * 512), 16, 0, 0);
+                                       (lptr_t)(Ws + slot * SB + (i * WW + lw) * 512), 16, 0, 2);
   };
 
   f32x4 acc[4][4];

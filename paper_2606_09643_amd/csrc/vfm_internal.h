@@ -121,9 +121,16 @@ __device__ __forceinline__ void add4(float4& a, const float4& b) {
   a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
 }
 
+// 16-byte load with the nontemporal hint (data read once)
+__device__ __forceinline__ float4 load4_nt(const float* p) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  const f4v v = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
 // Sum of ns fp32 partial slices (stride zs floats) at z, 4 columns, in a
 // fixed order: slice j goes to lane j mod 4 of four running sums, which are
-// then added pairwise.
+// then added pairwise.  Each partial is read once: nontemporal loads.
 __device__ __forceinline__ float4 sum_slices(const float* z, int64_t zs, int ns) {
   float4 s4[4];
 #pragma unroll
@@ -132,13 +139,13 @@ __device__ __forceinline__ float4 sum_slices(const float* z, int64_t zs, int ns)
   for (; sp + 4 <= ns; sp += 4) {
     float4 v[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = *reinterpret_cast<const float4*>(z + (sp + j) * zs);
+    for (int j = 0; j < 4; ++j) v[j] = load4_nt(z + (sp + j) * zs);
 #pragma unroll
     for (int j = 0; j < 4; ++j) add4(s4[j], v[j]);
   }
 #pragma unroll
   for (int j = 0; j < 3; ++j)  // the last ns mod 4 slices
-    if (sp + j < ns) add4(s4[j], *reinterpret_cast<const float4*>(z + (sp + j) * zs));
+    if (sp + j < ns) add4(s4[j], load4_nt(z + (sp + j) * zs));
   add4(s4[0], s4[1]);
   add4(s4[2], s4[3]);
   add4(s4[0], s4[2]);
