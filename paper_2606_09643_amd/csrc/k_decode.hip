@@ -276,8 +276,10 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   if (lid >= ncb * a.M) return;               // block-uniform
   const int m = lid % a.M, cb = lid / a.M;
   int t = 0, r = 0;
+  FinB bp = {};
   if (a.lora.enabled) {                       // block-uniform
     t = a.lora.row_task[m];
+    bp = fin_lora_bptrs(a.lora, t);
     r = fin_lora_u(a.lora, m, Us, red);
   }
   if (a.rope.on) {                            // block-uniform: the row's angles, as launch_rope
@@ -300,10 +302,10 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   float4 v = sum_slices(z, zs, a.nslices);
   if (a.lora.enabled) {
     if (swiglu) {
-      add4(v, fin_lora_delta(a.lora, t, r, 0, n, Us));
+      add4(v, fin_lora_delta(a.lora, bp, r, 0, n, Us));
     } else {
       const int slot = min(n / a.lora.slot_width, 2);
-      add4(v, fin_lora_delta(a.lora, t, r, slot, n - slot * a.lora.slot_width, Us));
+      add4(v, fin_lora_delta(a.lora, bp, r, slot, n - slot * a.lora.slot_width, Us));
     }
   }
   if (a.bias && !swiglu) {
@@ -342,7 +344,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
   float u4[4] = {0.f, 0.f, 0.f, 0.f};
   if (swiglu) {
     float4 u = sum_slices(z + a.N, zs, a.nslices);
-    if (a.lora.enabled) add4(u, fin_lora_delta(a.lora, t, r, 1, n, Us));
+    if (a.lora.enabled) add4(u, fin_lora_delta(a.lora, bp, r, 1, n, Us));
     u4[0] = u.x; u4[1] = u.y; u4[2] = u.z; u4[3] = u.w;
   }
   bf16x4 o;

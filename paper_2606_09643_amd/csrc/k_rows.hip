@@ -182,8 +182,10 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
   const int64_t zs = (int64_t)a.M * a.N;
   float* xr = (float*)a.out + (int64_t)row * a.ldo;
   int t = 0, r = 0;
+  FinB bp = {};
   if (a.lora.enabled) {                       // block-uniform
     t = a.lora.row_task[row];
+    bp = fin_lora_bptrs(a.lora, t);
     r = fin_lora_u(a.lora, row, Us, ured);
   }
   float4 v[MAXC];
@@ -195,7 +197,7 @@ __global__ __launch_bounds__(256) void finalize_norm_kernel(FinalizeArgs a, cons
       float4 s4 = sum_slices(a.Z + (int64_t)row * a.N + 4 * c, zs, a.nslices);
       if (a.lora.enabled) {
         const int slot = min(4 * c / a.lora.slot_width, 2);
-        add4(s4, fin_lora_delta(a.lora, t, r, slot, 4 * c - slot * a.lora.slot_width, Us));
+        add4(s4, fin_lora_delta(a.lora, bp, r, slot, 4 * c - slot * a.lora.slot_width, Us));
       }
       if (a.bias) {
         const bf16x4 bv = *reinterpret_cast<const bf16x4*>((const bf16*)a.bias + 4 * c);

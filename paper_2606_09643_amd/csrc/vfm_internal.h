@@ -389,15 +389,29 @@ __device__ __forceinline__ int fin_lora_u(const FinLora& L, int m, float* Us, fl
   return r;
 }
 
+// The row's task's B pointers of every slot, read at the start of the
+// finalize (t is the block's own), so that after the U rebuild the B rows
+// are requested at once instead of after one more dependent load.
+struct FinB { const bf16* p0; const bf16* p1; const bf16* p2; };
+__device__ __forceinline__ FinB fin_lora_bptrs(const FinLora& L, int t) {
+  FinB b;
+  b.p0 = L.B[0] != nullptr ? (const bf16*)L.B[0][t] : nullptr;
+  b.p1 = L.B[1] != nullptr ? (const bf16*)L.B[1][t] : nullptr;
+  b.p2 = L.B[2] != nullptr ? (const bf16*)L.B[2][t] : nullptr;
+  return b;
+}
+
 // LoRA difference of 4 consecutive columns of slot i of row m (task t, rank
 // r): rows brow .. brow + 3 of B_{t,i}, a fixed-order fp32 sum over the rank.
-__device__ __forceinline__ float4 fin_lora_delta(const FinLora& L, int t, int r, int i, int brow, const float* Us) {
+__device__ __forceinline__ float4 fin_lora_delta(const FinLora& L, const FinB& bp, int r, int i, int brow,
+                                                 const float* Us) {
   float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (r <= 0 || L.B[i] == nullptr) return d;
+  const bf16* B0 = i == 0 ? bp.p0 : i == 1 ? bp.p1 : bp.p2;
+  if (r <= 0 || B0 == nullptr) return d;
   // B_t comes from a device pointer table: read it as global memory, not
   // through generic (flat) addressing
   typedef const bf16x8 __attribute__((address_space(1))) gbf16x8;
-  const bf16* Bt = (const bf16*)L.B[i][t] + (int64_t)brow * r;
+  const bf16* Bt = B0 + (int64_t)brow * r;
   const float* u = Us + i * L.rpad;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int j0 = 0; j0 < r; j0 += 8) {
