@@ -35,7 +35,7 @@ SMALL = {
     2: dict(task_id=[5, 0, 5, 2, 9, 0], seq_len=[197] * 6),
     3: dict(task_id=[1, 1, 7, 0, 31, 7], seq_len=[64] * 6),
     4: dict(task_id=[3, 0, 3, 63], seq_len=[1, 130, 64, 77]),
-    5: dict(task_id=[2, 2, 0, 127, 5], seq_len=[1] * 5, ctx=[0, 63, 300, 64, 2048]),
+    5: dict(task_id=[2, 2, 0, 127, 5], seq_len=[1] * 5, ctx=[0, 63, 300, 64, 4200]),
 }
 
 
@@ -819,7 +819,7 @@ def test_paged_decode_matches_contiguous(page):
     """A decode layer over a paged cache (pages in random order, spare pages
     in the pool) gives bit-identical rows to the same layer over the
     contiguous head-major cache, and writes the new token's K / V into its
-    page.  Contexts 0, 63, 300, 64 and 2048 (three key chunks)."""
+    page.  Contexts 0, 63, 300, 64 and 4200 (three 2048-key chunks)."""
     w, batch, model, inp, kv, pb, fwd, pl = _setup(5)
     log(f"paged decode, page {page}, ctx {list(batch.ctx)}")
     fwd.embed()
