@@ -1067,8 +1067,8 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   float* part = (float*)ws;
   const int mx = mixed ? 1 : 0;
   dim3 grid(H, pl.n_req, nchunk), gm(pl.n_req, H);
-  // 6 keys per key stream and step (7B decode layer: 808 us against 823 us
-  // with 4 and 817-825 us with 8, same machine)
+  // 6 keys per key stream and step (7B decode layer, 2048-key chunks: 722 us
+  // against 738 us with 4 and 731 us with 8, same machine)
 #define DEC_K(PG, D_)                                                                                     \
   if (dtype == VFM_BF16)                                                                                   \
     hipLaunchKernelGGL((attn_decode_bf16_kernel<D_, 6, PG>), grid, dim3(256), 0, s, pl, (const bf16*)qkv, \
@@ -1082,10 +1082,12 @@ hipError_t launch_attention(int dtype, const Plan& pl, const vfm_cfg& c, const v
   pi = prof_begin(VFM_PROF_ATTN, s);                                                                   \
   if (kp.table) { DEC_K(true, D_); } else { DEC_K(false, D_); }                                       \
   prof_end(pi, s);                                                                                     \
-  pi = prof_begin(VFM_PROF_OTHER, s);                                                                  \
-  hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
-                     nchunk, d, mx, (TT*)out);                                                         \
-  prof_end(pi, s)
+  if (nchunk > 1) { /* some request has more than one chunk to merge */                                \
+    pi = prof_begin(VFM_PROF_OTHER, s);                                                                \
+    hipLaunchKernelGGL((attn_decode_merge_kernel<TT, D_>), gm, dim3(D_), 0, s, pl, (const float*)part, \
+                       nchunk, d, mx, (TT*)out);                                                       \
+    prof_end(pi, s);                                                                                   \
+  }
   if (dtype == VFM_BF16) {
     if (DH == 64) { DEC(bf16, 64); } else { DEC(bf16, 128); }
   } else {
