@@ -46,7 +46,7 @@ def _decoder_prefill_picks(pl):
 
 
 def _decode_picks(pl, batch):
-    """The longest context (several 1024-key chunks) and the shortest, plus
+    """The longest context (2049 keys: two 2048-key chunks) and the shortest, plus
     the first and last request of the largest task segment."""
     ctx = batch.ctx[pl["order"]]
     out = [int(np.argmax(ctx)), int(np.argmin(ctx))]
