@@ -272,3 +272,15 @@ def test_prompt_steps_refuse_cached_context():
     c = cfg(B.VFM_ATTN_CAUSAL)
     assert lib.vfm_layer_forward(C.byref(c), C.byref(weights), None, C.byref(zero), fake,
                                  None, None, 0, None, 0, None) == B.VFM_ERR_WORKSPACE
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU only: --gpus above 1 exits with status 2
+    and says so, before touching a device."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    p = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "4"], cwd=root,
+                       capture_output=True, text=True, timeout=300)
+    assert p.returncode == 2, (p.returncode, p.stdout[-500:], p.stderr[-500:])
+    assert "one GPU only" in p.stdout + p.stderr
