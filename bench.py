@@ -354,7 +354,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-task forward "
-              "shards by request with no cross-GPU exchange, and this build measures one GPU's "
+              "shards by request with no cross-GPU exchange, and bench.py measures one GPU's "
               "share.", file=sys.stderr)
         sys.exit(2)
 

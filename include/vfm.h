@@ -47,7 +47,7 @@ typedef enum {
   VFM_ERR_ARG = -1,         /* null pointer or bad enum value */
   VFM_ERR_SHAPE = -2,       /* sizes inconsistent or outside the supported set */
   VFM_ERR_TASK = -3,        /* task id out of range */
-  VFM_ERR_UNSUPPORTED = -4, /* valid request this build does not implement */
+  VFM_ERR_UNSUPPORTED = -4, /* valid request the library does not implement */
   VFM_ERR_WORKSPACE = -5,   /* workspace missing or too small */
   VFM_ERR_HIP = -6          /* HIP runtime error at launch */
 } vfm_status;

@@ -139,7 +139,7 @@ extern "C" const char* vfm_status_string(int status) {
     case VFM_ERR_ARG: return "invalid argument (null pointer or bad enum)";
     case VFM_ERR_SHAPE: return "inconsistent or unsupported sizes";
     case VFM_ERR_TASK: return "task id out of range";
-    case VFM_ERR_UNSUPPORTED: return "configuration not supported by this build";
+    case VFM_ERR_UNSUPPORTED: return "configuration not supported by the library";
     case VFM_ERR_WORKSPACE: return "workspace missing or too small";
     case VFM_ERR_HIP: return "HIP runtime error";
   }
